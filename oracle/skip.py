@@ -1,0 +1,106 @@
+"""Mask statistics and the adaptive reordering skip (test infrastructure only).
+
+Sec. IV-E states the three situations in which reordering does not pay, and that
+the decision combines cheap mask statistics with offline profiles of kernel
+latency and reordering cost; Sec. VI-F shows it firing for short sequences and
+very sparse masks. The paper gives no formula, so the reading here is:
+
+  case 1 "fits in cache": the head's distinct K/V blocks fit in one L2
+          (on the target, the L2 private to one XCD):
+          distinct_h * kv_block_bytes <= l2_bytes_per_xcd
+  case 2 "too little work": the expected kernel-time saving does not exceed
+          the reordering overhead, both linear models from offline profiles:
+          nnz_h * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row*m + ovh_ns_per_nnz*nnz_h
+  case 3 "already local": adjacent rows already share most blocks:
+          J_h = sum_i |M_i & M_{i+1}| / sum_i |M_i | M_{i+1}| >= j_max
+  case 4 (our addition) "no low-rank structure": the rank-2 embedding keeps too
+          little of the centred mask's energy for Stage 1 to group anything:
+          eta_h = (lambda_1 + lambda_2) / ||M~||_F^2 < eta_min,
+          with lambda_1 + lambda_2 the exact Rayleigh-Ritz trace (Alg. 1) and
+          ||M~||_F^2 = (m*nnz - sum_j c_j^2) / m (centring, Eq. 2).
+
+Each floating-point expression below is evaluated in fp64 with one IEEE
+rounding per operation in the order written, so that an independent
+implementation reaches the same decision.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import numpy as np
+
+FLAG_FITS_L2 = 1
+FLAG_LITTLE_WORK = 2
+FLAG_LOCAL = 4
+FLAG_UNSTRUCTURED = 8
+FLAG_DEGENERATE = 16
+FLAG_IDENTITY = 64
+
+SKIP_AUTO, SKIP_NEVER, SKIP_ALWAYS = 0, 1, 2
+
+
+@dataclass(frozen=True)
+class SkipProfile:
+    l2_bytes_per_xcd: float = 4.0 * 1024 * 1024
+    gain_ns_per_block: float = 1.0
+    ovh_ns_fixed: float = 2000.0
+    ovh_ns_per_row: float = 2.0
+    ovh_ns_per_nnz: float = 0.05
+    j_max: float = 0.75
+    eta_min: float = 0.05
+
+
+@dataclass
+class HeadStats:
+    m: int
+    n: int
+    row_nnz: np.ndarray      # int32 [m]
+    col_cnt: np.ndarray      # int32 [n]
+    nnz: int
+    distinct: int            # columns with at least one kept entry
+    adj_and: int             # sum_i |M_i & M_{i+1}|
+    adj_or: int              # sum_i |M_i | M_{i+1}|
+    sum_c2: int              # sum_j c_j^2
+
+
+def head_stats(mask_h: np.ndarray) -> HeadStats:
+    mb = np.asarray(mask_h) != 0
+    m, n = mb.shape
+    rn = mb.sum(axis=1).astype(np.int64)
+    cc = mb.sum(axis=0).astype(np.int64)
+    a = int((mb[:-1] & mb[1:]).sum()) if m > 1 else 0
+    o = int((mb[:-1] | mb[1:]).sum()) if m > 1 else 0
+    return HeadStats(m, n, rn.astype(np.int32), cc.astype(np.int32), int(rn.sum()), int((cc > 0).sum()),
+                     a, o, int((cc * cc).sum()))
+
+
+def kv_block_bytes(block: int, head_dim: int) -> int:
+    return 2 * block * head_dim * 2   # K and V, bf16
+
+
+def tier1_flags(st: HeadStats, prof: SkipProfile, block: int, head_dim: int) -> int:
+    flags = 0
+    if float(st.distinct) * float(kv_block_bytes(block, head_dim)) <= prof.l2_bytes_per_xcd:
+        flags |= FLAG_FITS_L2
+    saving = float(st.nnz) * prof.gain_ns_per_block
+    cost = prof.ovh_ns_fixed + prof.ovh_ns_per_row * float(st.m) + prof.ovh_ns_per_nnz * float(st.nnz)
+    if saving < cost:
+        flags |= FLAG_LITTLE_WORK
+    if st.adj_or > 0 and float(st.adj_and) / float(st.adj_or) >= prof.j_max:
+        flags |= FLAG_LOCAL
+    return flags
+
+
+def eta(st: HeadStats, trace: int, scale_exp: int) -> float:
+    """Share of ||M~||_F^2 captured by the rank-2 embedding."""
+    den = float(st.m) * float(st.m * st.nnz - st.sum_c2)
+    if den <= 0.0:
+        return 0.0
+    return math.ldexp(float(trace), scale_exp) / den
+
+
+def tier2_flags(st: HeadStats, prof: SkipProfile, trace: int, scale_exp: int, degenerate: bool) -> int:
+    if degenerate:
+        return FLAG_DEGENERATE
+    return FLAG_UNSTRUCTURED if eta(st, trace, scale_exp) < prof.eta_min else 0

@@ -1,0 +1,100 @@
+"""Pins of the mask statistics, the skip rule and the whole-mask permutation driver."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import compaction as C
+from oracle import permutation as P
+from oracle import reorder as R
+from oracle import skip as S
+from workloads import CONFIGS, custom, make_mask, make_mask_head
+
+
+def test_head_stats_brute_force():
+    rng = np.random.default_rng(1)
+    mask = (rng.random((23, 23)) < 0.3).astype(np.uint8)
+    st = S.head_stats(mask)
+    m, n = mask.shape
+    assert [sum(int(mask[i, j]) for j in range(n)) for i in range(m)] == list(st.row_nnz)
+    assert [sum(int(mask[i, j]) for i in range(m)) for j in range(n)] == list(st.col_cnt)
+    a = sum(int(mask[i, j] and mask[i + 1, j]) for i in range(m - 1) for j in range(n))
+    o = sum(int(mask[i, j] or mask[i + 1, j]) for i in range(m - 1) for j in range(n))
+    assert (a, o) == (st.adj_and, st.adj_or)
+    assert st.distinct == sum(1 for j in range(n) if any(mask[:, j]))
+    # ||M~||_F^2 from the statistics equals the explicitly centred matrix's
+    cen = mask - mask.mean(0, keepdims=True)
+    assert abs((m * st.nnz - st.sum_c2) / m - (cen ** 2).sum()) < 1e-9
+
+
+def test_eta_equals_svd_energy_share():
+    mask = make_mask_head(CONFIGS["wan1.3b-480p-81f"], 0, 2)
+    st = S.head_stats(mask)
+    s1 = P.stage1(mask, 0, 2, iters=300)
+    cen = mask - mask.mean(0, keepdims=True)
+    sv = np.linalg.svd(cen, compute_uv=False)
+    ref = (sv[0] ** 2 + sv[1] ** 2) / (sv ** 2).sum()
+    assert abs(S.eta(st, s1.trace, s1.scale_exp) / ref - 1) < 1e-6
+
+
+def test_eta_separates_random_from_structured():
+    wl = CONFIGS["skip-d64"]
+    for h, lo, hi in ((0, 0.0, 0.05), (20, 0.1, 1.0)):
+        mask = make_mask_head(wl, 0, h)
+        st = S.head_stats(mask)
+        s1 = P.stage1(mask, 0, h, 10)
+        assert lo <= S.eta(st, s1.trace, s1.scale_exp) < hi
+
+
+def test_tier1_cases():
+    prof = S.SkipProfile()
+    tiny = make_mask_head(CONFIGS["tiny"], 0, 0)
+    f = S.tier1_flags(S.head_stats(tiny), prof, 64, 64)
+    assert f & S.FLAG_FITS_L2          # 64 KV blocks of 16 KiB = 1 MiB < 4 MiB
+    big = make_mask_head(CONFIGS["wan14b-720p-81f"], 0, 0)
+    assert S.tier1_flags(S.head_stats(big), prof, 128, 128) == 0
+    # already local: every row equal to its neighbour except one column
+    band = np.zeros((100, 100), dtype=np.uint8)
+    for i in range(100):
+        band[i, max(0, i - 30):i + 30] = 1
+    assert S.tier1_flags(S.head_stats(band), prof, 128, 128) & S.FLAG_LOCAL
+    # little work: a nearly empty mask
+    sparse = np.eye(300, dtype=np.uint8)
+    assert S.tier1_flags(S.head_stats(sparse), prof, 128, 128) & S.FLAG_LITTLE_WORK
+    # boundary of case 1 is inclusive: exactly one L2 of distinct blocks fits
+    st = S.head_stats(np.eye(128, dtype=np.uint8))
+    exact = S.SkipProfile(l2_bytes_per_xcd=128 * S.kv_block_bytes(128, 128))
+    assert S.tier1_flags(st, exact, 128, 128) & S.FLAG_FITS_L2
+    below = S.SkipProfile(l2_bytes_per_xcd=128 * S.kv_block_bytes(128, 128) - 1)
+    assert not (S.tier1_flags(st, below, 128, 128) & S.FLAG_FITS_L2)
+
+
+def test_driver_modes():
+    wl = CONFIGS["skip-d64"]
+    mask = make_mask(wl)[:, [0, 1, 20, 21]]
+    kw = dict(block=wl.block, head_dim=wl.head_dim, wave=64, n_xcd=8, iters=10, seed=0)
+    p_always, f_always, _ = R.build_permutation(mask, skip_mode=S.SKIP_ALWAYS, **kw)
+    assert np.all(p_always == np.arange(wl.mb)) and np.all(f_always & S.FLAG_IDENTITY)
+    p_never, f_never, _ = R.build_permutation(mask, skip_mode=S.SKIP_NEVER, **kw)
+    for h in range(4):
+        ref, _ = P.two_stage_permutation(mask[0, h], seed=0, flat_head=h, wave=64, n_xcd=8, iters=10)
+        assert np.array_equal(p_never[0, h], ref)
+    assert not np.any(f_never & S.FLAG_IDENTITY)
+    p_auto, f_auto, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, **kw)
+    # random heads: unstructured -> identity; locality heads: reordered
+    assert f_auto[0, 0] & S.FLAG_UNSTRUCTURED and np.all(p_auto[0, 0] == np.arange(wl.mb))
+    assert f_auto[0, 2] == 0 and np.array_equal(p_auto[0, 2], p_never[0, 2])
+
+
+def test_compaction_brute_force():
+    wl = custom("c", heads=2, head_dim=64, block=64, grid=(2, 8, 16), rule=dict(kind="empty_rows", p=0.3))
+    mask = make_mask(wl)
+    row_ptr, lists = C.compact_mask(mask)
+    for h in range(2):
+        pos = 0
+        for i in range(wl.mb):
+            cols = [j for j in range(wl.mb) if mask[0, h, i, j]]
+            assert row_ptr[0, h, i] == pos
+            assert list(lists[0][h][pos:pos + len(cols)]) == cols
+            pos += len(cols)
+        assert row_ptr[0, h, wl.mb] == pos == len(lists[0][h])
