@@ -1,0 +1,204 @@
+/*
+ * wavealign.h - C ABI of the MI355X (gfx950) block-sparse attention path with
+ * cache-aware query-row reordering (WaveAlign, arXiv 2609.34814).
+ *
+ * Two operations follow the paper's problem statement:
+ *   - wa_build_permutation: block mask M_h in {0,1}^{M_B x N_B} per head in,
+ *     row permutation P_h out (Sec. IV-B, Eq. 1; Alg. 1 and Alg. 2; the
+ *     adaptive skip of Sec. IV-E);
+ *   - wa_sparse_attn: Q, K, V and M in, O out in the original row order
+ *     (Sec. II-B, II-C: FlashAttention-style query-block outer loop over the
+ *     mask-selected KV blocks; Sec. IV-A: only the execution order changes).
+ *
+ * Conventions (all entry points)
+ *   - Tensor and mask pointers are DEVICE pointers owned by the caller.
+ *     Scalar parameter structs are HOST pointers, read during the call only.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
+ *     and is asynchronous: no entry point synchronises, allocates device
+ *     memory or frees caller memory. Scratch memory comes from the caller's
+ *     `workspace` (device memory, 256-byte aligned, of at least the size the
+ *     matching *_workspace_size call reports).
+ *   - Every argument is validated before anything is enqueued; on error the
+ *     call returns a negative wa_status, enqueues nothing and leaves all
+ *     outputs untouched. wa_last_error() then describes the failure
+ *     (thread-local, valid until the thread's next call). WA_ERR_HIP means a
+ *     HIP runtime call or a launch failed after validation.
+ *   - No C++ exception crosses the ABI.
+ *   - Shapes: Q, K, V, O are bf16 [batch][heads][seq_len][head_dim],
+ *     contiguous. Blocks are runs of `block` consecutive tokens; block j holds
+ *     tokens [j*block, min((j+1)*block, seq_len)), so M_B = N_B =
+ *     ceil(seq_len / block) and the last block may be ragged. The mask is
+ *     uint8 [batch][heads][M_B][N_B], row-major; nonzero = the query block
+ *     attends to the KV block.
+ *   - Supported: head_dim in {64, 128}; block in {64, 128}; 1 <= M_B <= 4096;
+ *     batch*heads*M_B*N_B < 2^31.
+ *   - perm[b][h][s] is the original query block executed at slot s (row s of
+ *     P_h M_h, Eq. 1). Each perm[b][h] must be a permutation of 0..M_B-1.
+ */
+#ifndef WAVEALIGN_H
+#define WAVEALIGN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WA_ABI_VERSION 1
+#define WA_MAX_BLOCKS 4096
+
+typedef enum wa_status {
+  WA_OK = 0,
+  WA_ERR_INVALID_ARG = -1,  /* null pointer, non-positive size, bad enum value */
+  WA_ERR_UNSUPPORTED = -2,  /* head_dim / block / size outside the supported set */
+  WA_ERR_ALIGNMENT = -3,    /* tensor not 16-byte aligned, workspace not 256-byte aligned */
+  WA_ERR_WORKSPACE = -4,    /* workspace smaller than required */
+  WA_ERR_HIP = -6           /* a HIP runtime call or kernel launch failed */
+} wa_status;
+
+typedef struct wa_shape {
+  int32_t batch;
+  int32_t heads;
+  int32_t seq_len;   /* tokens N */
+  int32_t head_dim;  /* d */
+  int32_t block;     /* tokens per query / KV block */
+} wa_shape;
+
+/* Offline-profile constants of the adaptive skip (Sec. IV-E). A head keeps the
+ * identity order when any case fires (skip_mode = WA_SKIP_AUTO):
+ *   1  distinct_kv_blocks * kv_block_bytes <= l2_bytes_per_xcd        (fits in L2)
+ *   2  nnz * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row * M_B
+ *                                 + ovh_ns_per_nnz * nnz                (too little work)
+ *   3  sum_i |M_i & M_i+1| / sum_i |M_i | M_i+1| >= j_max              (already local)
+ *   4  (lambda_1 + lambda_2) / ||M~||_F^2 < eta_min                      (no rank-2 structure)
+ * Each comparison is one fixed sequence of IEEE fp64 operations. */
+typedef struct wa_skip_profile {
+  double l2_bytes_per_xcd;
+  double gain_ns_per_block;
+  double ovh_ns_fixed;
+  double ovh_ns_per_row;
+  double ovh_ns_per_nnz;
+  double j_max;
+  double eta_min;
+} wa_skip_profile;
+
+enum { WA_SKIP_AUTO = 0, WA_SKIP_NEVER = 1, WA_SKIP_ALWAYS = 2 };
+
+/* head_flags bits written by wa_build_permutation */
+enum {
+  WA_FLAG_FITS_L2 = 1,
+  WA_FLAG_LITTLE_WORK = 2,
+  WA_FLAG_LOCAL = 4,
+  WA_FLAG_UNSTRUCTURED = 8,
+  WA_FLAG_DEGENERATE = 16,  /* centred mask has no direction; Stage 1 kept the identity order */
+  WA_FLAG_IDENTITY = 64     /* the identity permutation was returned */
+};
+
+typedef struct wa_perm_params {
+  int32_t wave_per_xcd;  /* W: resident query-block tasks per XCD; 0 = wa_wave_size() for the shape */
+  int32_t n_xcd;         /* contiguous segments, one per XCD (8 on MI355X); 1 = Alg. 2 as printed */
+  int32_t iters;         /* T subspace iterations (Alg. 1), 1..64; the paper uses 5-15 */
+  int32_t skip_mode;     /* WA_SKIP_AUTO / WA_SKIP_NEVER / WA_SKIP_ALWAYS */
+  uint64_t seed;         /* SplitMix64 counter base of the random start block */
+  const wa_skip_profile* profile;  /* host pointer; NULL = wa_default_skip_profile() */
+} wa_perm_params;
+
+/* Library version (WA_ABI_VERSION). */
+int32_t wa_abi_version(void);
+
+/* Static description of a status code. */
+const char* wa_status_string(wa_status status);
+
+/* Detail of the calling thread's last failed call ("" if none). */
+const char* wa_last_error(void);
+
+/* Built-in skip-profile constants. */
+wa_status wa_default_skip_profile(wa_skip_profile* out);
+
+/* Query blocks resident per XCD for the attention kernel of this head_dim and
+ * block (32 CUs per XCD x workgroups per CU). Queries the current device. */
+wa_status wa_wave_size(int32_t head_dim, int32_t block, int32_t* wave_per_xcd);
+
+/* Per-head mask statistics (Sec. II-B row NNZ n_i; Alg. 1 column counts c = M^T 1;
+ * the inputs of the skip rule of Sec. IV-E).
+ *   row_nnz    out int32 [B][H][M_B]
+ *   col_cnt    out int32 [B][H][N_B]
+ *   head_stats out int64 [B][H][6]: nnz, distinct columns, sum_i |M_i & M_i+1|,
+ *              sum_i |M_i | M_i+1|, sum_j c_j^2, 0
+ *   workspace  >= wa_perm_workspace_size(shape). */
+wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row_nnz, int32_t* col_cnt,
+                        int64_t* head_stats, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by wa_build_permutation and wa_mask_stats. */
+wa_status wa_perm_workspace_size(const wa_shape* shape, size_t* bytes);
+
+/* Two-stage cache-aware row permutation per head (Alg. 2 with MFCSI, Alg. 1):
+ * Stage 1 orders rows by the polar angle of their rank-2 centred spectral
+ * embedding (Eq. 2-4); the order is split into n_xcd contiguous segments and
+ * each segment into buckets of wave_per_xcd rows; Stage 2 sorts each bucket
+ * by descending n_i (stable). Integer-exact fixed-point arithmetic makes the
+ * result identical on every run and to the reference reading.
+ *   perm         out int32 [B][H][M_B] (required)
+ *   head_flags   out uint8 [B][H] WA_FLAG_* bits, nullable
+ *   embedding    out int32 [B][H][M_B][2] canonical (u1, u2), 2^30 per unit, nullable
+ *                (zeros for heads that skipped Stage 1)
+ *   stage1_order out int32 [B][H][M_B] Stage-1 order, nullable (identity when skipped) */
+wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const wa_perm_params* params,
+                               int32_t* perm, uint8_t* head_flags, int32_t* embedding, int32_t* stage1_order,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Compacted per-row KV-block index lists (the mask-selected inner loop of Sec. II-C):
+ *   row_ptr out int32 [B][H][M_B+1]: exclusive prefix sum of n_i, local to the head
+ *   col_idx out int32, capacity B*H*M_B*N_B: head (b,h)'s list starts at
+ *           (b*H+h)*M_B*N_B; row i's indices are ascending j with M[i][j] != 0. */
+wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* row_ptr, int32_t* col_idx,
+                          void* stream);
+
+/* Workspace bytes needed by wa_sparse_attn (the compacted lists). */
+wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
+
+/* Block-sparse attention forward: for every query block i and token q in it,
+ * O_q = softmax(scale * Q_q K_S^T) V_S over the tokens of the KV blocks with
+ * M[i][j] != 0, visited in ascending j (Sec. II-B, II-C). bf16 inputs, fp32
+ * accumulation, bf16 output. Query block i runs at the slot s with perm[s] = i
+ * and is read and written at its original rows (the inverse permutation of
+ * Sec. IV-A is fused into the store), so O is identical for every perm.
+ * A query block with no kept KV block gets O = 0 and LSE = -inf.
+ *   q, k, v      bf16 [B][H][N][d], 16-byte aligned
+ *   perm         int32 [B][H][M_B], NULL = identity (not checked for bijectivity)
+ *   softmax_scale  <= 0 selects 1/sqrt(d)
+ *   n_xcd        8: slot s of a head runs on XCD x of the contiguous segment containing s
+ *                (workgroup g of the head runs slot seg_start(g mod 8) + g / 8);
+ *                1: slot = workgroup index (plain dispatch order)
+ *   o            out bf16 [B][H][N][d]
+ *   lse          out float [B][H][N] natural-log sum-exp of the scaled scores, nullable
+ *   workspace    >= wa_attn_workspace_size(shape) */
+wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint8_t* mask, const int32_t* perm,
+                         const wa_shape* shape, float softmax_scale, int32_t n_xcd, void* o, float* lse,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* As wa_sparse_attn, from lists already built by wa_compact_mask. */
+wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
+                             const int32_t* col_idx, const int32_t* perm, const wa_shape* shape,
+                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* stream);
+
+/* ---- diagnostics (used by the test suite; not needed by callers) ---- */
+
+/* Evaluates on the GPU the fp64 operations the exact permutation relies on, for
+ * comparison bit for bit with IEEE results on the host. Device pointers:
+ * a, b double [n]; c int64 [n]; out double [n][6] =
+ * { sqrt(|a|), a / b, (double)c, rint(a * 2^30), a*b - b*3 (two roundings, no
+ * fused multiply-add), ldexp(a, (c & 31) - 16) }. */
+wa_status wa_fp64_probe(const double* a, const double* b, const int64_t* c, double* out, int32_t n, void* stream);
+
+/* Writes the XCD index each workgroup of an n_wg-workgroup grid ran on
+ * (out: device int32 [n_wg]), to check the round-robin dispatch that the
+ * XCD-aware slot mapping of wa_sparse_attn assumes. */
+wa_status wa_xcc_probe(int32_t* out, int32_t n_wg, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WAVEALIGN_H */

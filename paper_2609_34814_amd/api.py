@@ -1,0 +1,196 @@
+"""Python binding of the block-sparse attention path (argument marshalling only).
+
+Every computation runs in the HIP kernels of libwavealign.so; torch supplies
+device memory and the current HIP stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from typing import Optional
+
+import torch
+
+from . import _lib as L
+
+_SKIP = {"auto": L.WA_SKIP_AUTO, "never": L.WA_SKIP_NEVER, "always": L.WA_SKIP_ALWAYS}
+
+
+def _stream() -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t: torch.Tensor, name: str) -> None:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _mask_u8(mask: torch.Tensor) -> torch.Tensor:
+    _dev(mask, "mask")
+    if mask.dtype == torch.bool:
+        return mask.view(torch.uint8)
+    if mask.dtype != torch.uint8:
+        raise ValueError("mask must be uint8 or bool")
+    return mask
+
+
+def shape_of(batch: int, heads: int, seq_len: int, head_dim: int, block: int) -> L.WaShape:
+    return L.WaShape(batch, heads, seq_len, head_dim, block)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def wave_size(head_dim: int, block: int) -> int:
+    lib = L.load()
+    out = ctypes.c_int32(0)
+    L.check(lib.wa_wave_size(head_dim, block, ctypes.byref(out)))
+    return out.value
+
+
+def default_skip_profile() -> L.WaSkipProfile:
+    lib = L.load()
+    p = L.WaSkipProfile()
+    L.check(lib.wa_default_skip_profile(ctypes.byref(p)))
+    return p
+
+
+def perm_workspace_size(shape: L.WaShape) -> int:
+    lib = L.load()
+    n = ctypes.c_size_t(0)
+    L.check(lib.wa_perm_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
+    return n.value
+
+
+def attn_workspace_size(shape: L.WaShape) -> int:
+    lib = L.load()
+    n = ctypes.c_size_t(0)
+    L.check(lib.wa_attn_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
+    return n.value
+
+
+def mask_stats(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 128):
+    """(row_nnz [B][H][M_B], col_cnt [B][H][N_B], head_stats [B][H][6]) as device tensors."""
+    lib = L.load()
+    mask = _mask_u8(mask)
+    b, h, mb, _ = mask.shape
+    shape = shape_of(b, h, seq_len, head_dim, block)
+    dev = mask.device
+    row_nnz = torch.empty((b, h, mb), dtype=torch.int32, device=dev)
+    col_cnt = torch.empty((b, h, mb), dtype=torch.int32, device=dev)
+    stats = torch.empty((b, h, 6), dtype=torch.int64, device=dev)
+    ws = _workspace(perm_workspace_size(shape), dev)
+    L.check(lib.wa_mask_stats(_ptr(mask), ctypes.byref(shape), _ptr(row_nnz), _ptr(col_cnt), _ptr(stats),
+                              _ptr(ws), ws.numel(), _stream()))
+    return row_nnz, col_cnt, stats
+
+
+def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int, wave: Optional[int] = None,
+                      n_xcd: int = 8, iters: int = 10, seed: int = 0, skip: str = "auto",
+                      profile: Optional[L.WaSkipProfile] = None, workspace: Optional[torch.Tensor] = None,
+                      return_info: bool = False):
+    """perm int32 [B][H][M_B] and head flags uint8 [B][H] (plus embedding and Stage-1 order if asked)."""
+    lib = L.load()
+    mask = _mask_u8(mask)
+    b, h, mb, nb = mask.shape
+    shape = shape_of(b, h, seq_len, head_dim, block)
+    dev = mask.device
+    perm = torch.empty((b, h, mb), dtype=torch.int32, device=dev)
+    flags = torch.empty((b, h), dtype=torch.uint8, device=dev)
+    emb = torch.empty((b, h, mb, 2), dtype=torch.int32, device=dev) if return_info else None
+    s1 = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if return_info else None
+    params = L.WaPermParams(0 if wave is None else int(wave), int(n_xcd), int(iters), _SKIP[skip],
+                            int(seed) & ((1 << 64) - 1),
+                            ctypes.pointer(profile) if profile is not None else None)
+    need = perm_workspace_size(shape)
+    if workspace is None or workspace.numel() < need:
+        workspace = _workspace(need, dev)
+    L.check(lib.wa_build_permutation(_ptr(mask), ctypes.byref(shape), ctypes.byref(params), _ptr(perm),
+                                     _ptr(flags), _ptr(emb), _ptr(s1), _ptr(workspace), workspace.numel(),
+                                     _stream()))
+    if return_info:
+        return perm, flags, emb, s1
+    return perm, flags
+
+
+def compact_mask(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 128):
+    """CSR lists: row_ptr int32 [B][H][M_B+1] (head-local offsets), col_idx int32 [B*H*M_B*N_B]."""
+    lib = L.load()
+    mask = _mask_u8(mask)
+    b, h, mb, nb = mask.shape
+    shape = shape_of(b, h, seq_len, head_dim, block)
+    row_ptr = torch.empty((b, h, mb + 1), dtype=torch.int32, device=mask.device)
+    col_idx = torch.empty((b * h * mb * nb,), dtype=torch.int32, device=mask.device)
+    L.check(lib.wa_compact_mask(_ptr(mask), ctypes.byref(shape), _ptr(row_ptr), _ptr(col_idx), _stream()))
+    return row_ptr, col_idx
+
+
+def _attn_args(q, k, v, block):
+    for t, nm in ((q, "q"), (k, "k"), (v, "v")):
+        _dev(t, nm)
+        if t.dtype != torch.bfloat16:
+            raise ValueError(f"{nm} must be bfloat16")
+    if q.shape != k.shape or q.shape != v.shape or q.dim() != 4:
+        raise ValueError("q, k, v must share one [B][H][N][d] shape")
+    b, h, n, d = q.shape
+    return shape_of(b, h, n, d, block)
+
+
+def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: torch.Tensor,
+                perm: Optional[torch.Tensor] = None, *, block: int, scale: Optional[float] = None,
+                n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None):
+    """O = block-sparse softmax attention of q over the kept KV blocks, in the original row order."""
+    lib = L.load()
+    shape = _attn_args(q, k, v, block)
+    mask = _mask_u8(mask)
+    if perm is not None:
+        _dev(perm, "perm")
+        if perm.dtype != torch.int32:
+            raise ValueError("perm must be int32")
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if return_lse else None
+    need = attn_workspace_size(shape)
+    if workspace is None or workspace.numel() < need:
+        workspace = _workspace(need, q.device)
+    L.check(lib.wa_sparse_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(mask), _ptr(perm), ctypes.byref(shape),
+                               float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse), _ptr(workspace),
+                               workspace.numel(), _stream()))
+    return (o, lse) if return_lse else o
+
+
+def sparse_attn_csr(q, k, v, row_ptr, col_idx, perm=None, *, block: int, scale: Optional[float] = None,
+                    n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None):
+    lib = L.load()
+    shape = _attn_args(q, k, v, block)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if return_lse else None
+    L.check(lib.wa_sparse_attn_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr), _ptr(col_idx), _ptr(perm),
+                                   ctypes.byref(shape), float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse),
+                                   _stream()))
+    return (o, lse) if return_lse else o
+
+
+def fp64_probe(a: torch.Tensor, b: torch.Tensor, c: torch.Tensor) -> torch.Tensor:
+    lib = L.load()
+    out = torch.empty((a.numel(), 6), dtype=torch.float64, device=a.device)
+    L.check(lib.wa_fp64_probe(_ptr(a), _ptr(b), _ptr(c), _ptr(out), a.numel(), _stream()))
+    return out
+
+
+def xcc_probe(n_wg: int, device="cuda") -> torch.Tensor:
+    lib = L.load()
+    out = torch.full((n_wg,), -1, dtype=torch.int32, device=device)
+    L.check(lib.wa_xcc_probe(_ptr(out), int(n_wg), _stream()))
+    return out
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

@@ -1,0 +1,363 @@
+// C ABI of the library: argument validation, workspace layout and kernel dispatch.
+// Every argument is checked before any HIP call; nothing here allocates or synchronises.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "common.h"
+#include "perm_launch.h"
+#include "wavealign.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+wa_status fail(wa_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+wa_status ok() {
+  g_err[0] = '\0';
+  return WA_OK;
+}
+
+wa_status hip_fail(hipError_t e, const char* what) {
+  return fail(WA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Dims {
+  int64_t bh;
+  int mb;
+  int n;  // tokens
+  int d;
+  int blk;
+};
+
+wa_status check_shape(const wa_shape* s, Dims* out) {
+  if (!s) return fail(WA_ERR_INVALID_ARG, "shape is null");
+  if (s->batch < 1 || s->heads < 1 || s->seq_len < 1)
+    return fail(WA_ERR_INVALID_ARG, "batch, heads and seq_len must be >= 1 (got %d, %d, %d)", s->batch, s->heads,
+                s->seq_len);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(WA_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", s->head_dim);
+  if (s->block != 64 && s->block != 128)
+    return fail(WA_ERR_UNSUPPORTED, "block %d not supported (64 or 128)", s->block);
+  const int64_t mb = ((int64_t)s->seq_len + s->block - 1) / s->block;
+  if (mb > WA_MAX_BLOCKS) return fail(WA_ERR_UNSUPPORTED, "%lld blocks per sequence exceeds %d", (long long)mb,
+                                      WA_MAX_BLOCKS);
+  const int64_t bh = (int64_t)s->batch * s->heads;
+  if (bh * mb * mb >= (int64_t(1) << 31))
+    return fail(WA_ERR_UNSUPPORTED, "batch*heads*M_B*N_B = %lld must be < 2^31", (long long)(bh * mb * mb));
+  if (bh * (int64_t)s->seq_len * s->head_dim >= (int64_t(1) << 40))
+    return fail(WA_ERR_UNSUPPORTED, "tensor too large");
+  out->bh = bh;
+  out->mb = (int)mb;
+  out->n = s->seq_len;
+  out->d = s->head_dim;
+  out->blk = s->block;
+  return WA_OK;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+struct PermWs {
+  size_t rowbits, colbits, row_nnz, col_cnt, head_stats, zbuf, ybuf, total;
+};
+
+PermWs perm_ws_layout(const Dims& d) {
+  PermWs w{};
+  const int64_t words = (d.mb + 63) / 64;
+  size_t off = 0;
+  w.rowbits = off; off = align_up(off + (size_t)d.bh * d.mb * words * 8);
+  w.colbits = off; off = align_up(off + (size_t)d.bh * d.mb * words * 8);
+  w.row_nnz = off; off = align_up(off + (size_t)d.bh * d.mb * 4);
+  w.col_cnt = off; off = align_up(off + (size_t)d.bh * d.mb * 4);
+  w.head_stats = off; off = align_up(off + (size_t)d.bh * 6 * 8);
+  w.zbuf = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 8);
+  w.ybuf = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 8);
+  w.total = off;
+  return w;
+}
+
+size_t attn_ws_bytes(const Dims& d) {
+  return align_up((size_t)d.bh * (d.mb + 1) * 4) + align_up((size_t)d.bh * d.mb * d.mb * 4);
+}
+
+wa_status check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return WA_OK;
+  if (!ws) return fail(WA_ERR_INVALID_ARG, "workspace is null (%zu bytes needed)", need);
+  if (!aligned(ws, kAlign)) return fail(WA_ERR_ALIGNMENT, "workspace must be 256-byte aligned");
+  if (have < need) return fail(WA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return WA_OK;
+}
+
+const wa_skip_profile kDefaultProfile = {
+    4.0 * 1024.0 * 1024.0,  // l2_bytes_per_xcd: MI355X L2 per XCD
+    1.0,                    // gain_ns_per_block
+    2000.0,                 // ovh_ns_fixed
+    2.0,                    // ovh_ns_per_row
+    0.05,                   // ovh_ns_per_nnz
+    0.75,                   // j_max
+    0.05,                   // eta_min
+};
+
+wa_status check_attn_common(const void* q, const void* k, const void* v, void* o, int32_t n_xcd) {
+  if (!q || !k || !v || !o) return fail(WA_ERR_INVALID_ARG, "q, k, v and o must be non-null");
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16))
+    return fail(WA_ERR_ALIGNMENT, "q, k, v and o must be 16-byte aligned");
+  if (n_xcd < 1 || n_xcd > 64) return fail(WA_ERR_INVALID_ARG, "n_xcd %d outside 1..64", n_xcd);
+  return WA_OK;
+}
+
+wa_status launch_compact(const uint8_t* mask, const Dims& d, int32_t* row_ptr, int32_t* col_idx, hipStream_t st) {
+  hipError_t e = wa_launch_row_count(mask, d.bh * d.mb, d.mb, row_ptr, d.mb + 1, 1, d.mb, st);
+  if (e != hipSuccess) return hip_fail(e, "row_count launch");
+  e = wa_launch_head_scan(row_ptr, (int)d.bh, d.mb, st);
+  if (e != hipSuccess) return hip_fail(e, "head_scan launch");
+  e = wa_launch_row_write(mask, (int)d.bh, d.mb, d.mb, row_ptr, col_idx, st);
+  if (e != hipSuccess) return hip_fail(e, "row_write launch");
+  return WA_OK;
+}
+
+wa_status launch_attn(const void* q, const void* k, const void* v, const int32_t* row_ptr, const int32_t* col_idx,
+                      const int32_t* perm, const Dims& d, float scale, int32_t n_xcd, void* o, float* lse,
+                      hipStream_t st) {
+  WaAttnLaunch a{};
+  a.q = q; a.k = k; a.v = v;
+  a.row_ptr = row_ptr; a.col_idx = col_idx; a.perm = perm;
+  a.o = o; a.lse = lse;
+  a.bh = (int32_t)d.bh; a.seq_len = d.n; a.mb = d.mb; a.head_dim = d.d; a.block = d.blk; a.n_xcd = n_xcd;
+  a.scale = (scale > 0.f && std::isfinite(scale)) ? scale : (float)(1.0 / std::sqrt((double)d.d));
+  hipError_t e = wa_launch_attention(a, st);
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  return WA_OK;
+}
+
+wa_status perm_launch_common(const uint8_t* mask, const Dims& d, const PermWs& L, char* base, hipStream_t st,
+                             int32_t* row_nnz_out) {
+  int32_t* row_nnz = row_nnz_out ? row_nnz_out : (int32_t*)(base + L.row_nnz);
+  hipError_t e = wa_launch_pack_rows(mask, d.bh * d.mb, d.mb, (uint64_t*)(base + L.rowbits), row_nnz, st);
+  if (e != hipSuccess) return hip_fail(e, "pack_rows launch");
+  e = wa_launch_transpose_bits((const uint64_t*)(base + L.rowbits), (int)d.bh, d.mb, d.mb,
+                               (uint64_t*)(base + L.colbits), st);
+  if (e != hipSuccess) return hip_fail(e, "transpose_bits launch");
+  return WA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t wa_abi_version(void) { return WA_ABI_VERSION; }
+
+const char* wa_status_string(wa_status s) {
+  switch (s) {
+    case WA_OK: return "ok";
+    case WA_ERR_INVALID_ARG: return "invalid argument";
+    case WA_ERR_UNSUPPORTED: return "unsupported shape or parameter";
+    case WA_ERR_ALIGNMENT: return "misaligned pointer";
+    case WA_ERR_WORKSPACE: return "workspace too small";
+    case WA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* wa_last_error(void) { return g_err; }
+
+wa_status wa_default_skip_profile(wa_skip_profile* out) {
+  if (!out) return fail(WA_ERR_INVALID_ARG, "out is null");
+  *out = kDefaultProfile;
+  return ok();
+}
+
+wa_status wa_wave_size(int32_t head_dim, int32_t block, int32_t* wave_per_xcd) {
+  if (!wave_per_xcd) return fail(WA_ERR_INVALID_ARG, "wave_per_xcd is null");
+  if ((head_dim != 64 && head_dim != 128) || (block != 64 && block != 128))
+    return fail(WA_ERR_UNSUPPORTED, "head_dim %d / block %d not supported", head_dim, block);
+  int dev = 0, cus = 0, wgs = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  e = wa_attention_occupancy(head_dim, block, &wgs);
+  if (e != hipSuccess) return hip_fail(e, "occupancy query");
+  // 8 XCDs share the compute units evenly on MI355X (256 CUs = 8 x 32)
+  const int per_xcd = cus >= 8 ? cus / 8 : cus;
+  *wave_per_xcd = per_xcd * (wgs > 0 ? wgs : 1);
+  return ok();
+}
+
+wa_status wa_perm_workspace_size(const wa_shape* shape, size_t* bytes) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!bytes) return fail(WA_ERR_INVALID_ARG, "bytes is null");
+  *bytes = perm_ws_layout(d).total;
+  return ok();
+}
+
+wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row_nnz, int32_t* col_cnt,
+                        int64_t* head_stats, void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!mask || !row_nnz || !col_cnt || !head_stats)
+    return fail(WA_ERR_INVALID_ARG, "mask, row_nnz, col_cnt and head_stats must be non-null");
+  const PermWs L = perm_ws_layout(d);
+  s = check_ws(workspace, workspace_bytes, L.total);
+  if (s != WA_OK) return s;
+  hipStream_t st = (hipStream_t)stream;
+  char* base = (char*)workspace;
+  s = perm_launch_common(mask, d, L, base, st, row_nnz);
+  if (s != WA_OK) return s;
+  WaPermLaunch a{};
+  a.rowbits = (const uint64_t*)(base + L.rowbits);
+  a.colbits = (const uint64_t*)(base + L.colbits);
+  a.row_nnz = row_nnz;
+  a.col_cnt = col_cnt;
+  a.head_stats = head_stats;
+  a.zbuf = (int64_t*)(base + L.zbuf);
+  a.ybuf = (int64_t*)(base + L.ybuf);
+  a.bh = (int32_t)d.bh; a.m = d.mb; a.n = d.mb;
+  a.wave = 1; a.n_xcd = 1; a.iters = 0; a.skip_mode = WA_SKIP_NEVER; a.stats_only = 1;
+  a.block = d.blk; a.head_dim = d.d;
+  a.prof = kDefaultProfile;
+  hipError_t e = wa_launch_perm_heads(a, st);
+  if (e != hipSuccess) return hip_fail(e, "mask stats launch");
+  return ok();
+}
+
+wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const wa_perm_params* params,
+                               int32_t* perm, uint8_t* head_flags, int32_t* embedding, int32_t* stage1_order,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!params) return fail(WA_ERR_INVALID_ARG, "params is null");
+  if (!mask || !perm) return fail(WA_ERR_INVALID_ARG, "mask and perm must be non-null");
+  if (params->n_xcd < 1 || params->n_xcd > 64) return fail(WA_ERR_INVALID_ARG, "n_xcd %d outside 1..64", params->n_xcd);
+  if (params->iters < 1 || params->iters > 64) return fail(WA_ERR_INVALID_ARG, "iters %d outside 1..64", params->iters);
+  if (params->skip_mode < WA_SKIP_AUTO || params->skip_mode > WA_SKIP_ALWAYS)
+    return fail(WA_ERR_INVALID_ARG, "skip_mode %d invalid", params->skip_mode);
+  if (params->wave_per_xcd < 0 || params->wave_per_xcd > WA_MAX_BLOCKS)
+    return fail(WA_ERR_INVALID_ARG, "wave_per_xcd %d outside 0..%d", params->wave_per_xcd, WA_MAX_BLOCKS);
+  if (embedding && !aligned(embedding, 8)) return fail(WA_ERR_ALIGNMENT, "embedding must be 8-byte aligned");
+  const PermWs L = perm_ws_layout(d);
+  s = check_ws(workspace, workspace_bytes, L.total);
+  if (s != WA_OK) return s;
+  int32_t wave = params->wave_per_xcd;
+  if (wave == 0) {
+    s = wa_wave_size(d.d, d.blk, &wave);
+    if (s != WA_OK) return s;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  char* base = (char*)workspace;
+  s = perm_launch_common(mask, d, L, base, st, nullptr);
+  if (s != WA_OK) return s;
+  WaPermLaunch a{};
+  a.rowbits = (const uint64_t*)(base + L.rowbits);
+  a.colbits = (const uint64_t*)(base + L.colbits);
+  a.row_nnz = (const int32_t*)(base + L.row_nnz);
+  a.col_cnt = nullptr;
+  a.head_stats = nullptr;
+  a.zbuf = (int64_t*)(base + L.zbuf);
+  a.ybuf = (int64_t*)(base + L.ybuf);
+  a.perm = perm; a.flags = head_flags; a.embedding = embedding; a.stage1 = stage1_order;
+  a.bh = (int32_t)d.bh; a.m = d.mb; a.n = d.mb;
+  a.wave = wave; a.n_xcd = params->n_xcd; a.iters = params->iters; a.skip_mode = params->skip_mode;
+  a.stats_only = 0; a.block = d.blk; a.head_dim = d.d; a.seed = params->seed;
+  a.prof = params->profile ? *params->profile : kDefaultProfile;
+  hipError_t e = wa_launch_perm_heads(a, st);
+  if (e != hipSuccess) return hip_fail(e, "permutation launch");
+  return ok();
+}
+
+wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* row_ptr, int32_t* col_idx,
+                          void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!mask || !row_ptr || !col_idx) return fail(WA_ERR_INVALID_ARG, "mask, row_ptr and col_idx must be non-null");
+  s = launch_compact(mask, d, row_ptr, col_idx, (hipStream_t)stream);
+  if (s != WA_OK) return s;
+  return ok();
+}
+
+wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!bytes) return fail(WA_ERR_INVALID_ARG, "bytes is null");
+  *bytes = attn_ws_bytes(d);
+  return ok();
+}
+
+wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint8_t* mask, const int32_t* perm,
+                         const wa_shape* shape, float softmax_scale, int32_t n_xcd, void* o, float* lse,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  s = check_attn_common(q, k, v, o, n_xcd);
+  if (s != WA_OK) return s;
+  if (!mask) return fail(WA_ERR_INVALID_ARG, "mask is null");
+  if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
+  s = check_ws(workspace, workspace_bytes, attn_ws_bytes(d));
+  if (s != WA_OK) return s;
+  hipStream_t st = (hipStream_t)stream;
+  int32_t* row_ptr = (int32_t*)workspace;
+  int32_t* col_idx = (int32_t*)((char*)workspace + align_up((size_t)d.bh * (d.mb + 1) * 4));
+  s = launch_compact(mask, d, row_ptr, col_idx, st);
+  if (s != WA_OK) return s;
+  s = launch_attn(q, k, v, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse, st);
+  if (s != WA_OK) return s;
+  return ok();
+}
+
+wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
+                             const int32_t* col_idx, const int32_t* perm, const wa_shape* shape,
+                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  s = check_attn_common(q, k, v, o, n_xcd);
+  if (s != WA_OK) return s;
+  if (!row_ptr || !col_idx) return fail(WA_ERR_INVALID_ARG, "row_ptr and col_idx must be non-null");
+  if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
+  s = launch_attn(q, k, v, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse, (hipStream_t)stream);
+  if (s != WA_OK) return s;
+  return ok();
+}
+
+/* Diagnostic: evaluates on the GPU the fp64 operations the exact permutation relies on
+ * (sqrt, division, int64 -> fp64, rint, uncontracted multiply-subtract, ldexp) so they can be
+ * compared bit for bit with IEEE results on the host. a, b: double [n]; c: int64 [n];
+ * out: double [n][6]. Device pointers. */
+wa_status wa_fp64_probe(const double* a, const double* b, const int64_t* c, double* out, int32_t n, void* stream) {
+  if (!a || !b || !c || !out) return fail(WA_ERR_INVALID_ARG, "null pointer");
+  if (n < 0) return fail(WA_ERR_INVALID_ARG, "n < 0");
+  hipError_t e = wa_launch_fp64_probe(a, b, c, out, n, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "fp64 probe launch");
+  return ok();
+}
+
+wa_status wa_xcc_probe(int32_t* out, int32_t n_wg, void* stream) {
+  if (!out) return fail(WA_ERR_INVALID_ARG, "out is null");
+  if (n_wg < 0) return fail(WA_ERR_INVALID_ARG, "n_wg < 0");
+  hipError_t e = wa_launch_xcc_probe(out, n_wg, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "xcc probe launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,180 @@
+// Mask scans for gfx950: row counts, per-row KV-index lists, and the bit-packed
+// row and column masks that the permutation builder iterates over.
+//
+// A wavefront scans one mask row 64 columns at a time: lane l tests column
+// 64t + l, a ballot gives the 64-bit word of kept columns, and the popcount of
+// the word below lane l is the lane's rank among the kept columns. Indices are
+// therefore written in ascending column order (the order in which the attention
+// kernel visits KV blocks) and the result is independent of scheduling.
+
+#include "common.h"
+#include "perm_launch.h"
+
+namespace {
+
+constexpr int kWavesPerWG = 4;
+
+__device__ __forceinline__ uint64_t ballot64(bool p) { return __ballot(p); }
+
+// counts[(row / mb) * count_stride_rows + counts_offset + row % mb] = n_row
+__global__ __launch_bounds__(256) void row_count_kernel(const uint8_t* __restrict__ mask, int64_t rows, int n,
+                                                         int32_t* __restrict__ counts, int64_t stride, int offset,
+                                                         int mb) {
+  const int64_t row = (int64_t)blockIdx.x * kWavesPerWG + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const uint8_t* p = mask + row * n;
+  int cnt = 0;
+  for (int j = lane; j < n; j += 64) cnt += p[j] != 0;
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+  if (lane == 0) counts[(row / mb) * stride + offset + row % mb] = cnt;
+}
+
+// In place: row_ptr[h][1..mb] holds counts on entry, the exclusive scan on exit (row_ptr[h][0] = 0).
+__global__ __launch_bounds__(1024) void head_scan_kernel(int32_t* __restrict__ row_ptr, int mb) {
+  __shared__ int32_t part[1024];
+  int32_t* rp = row_ptr + (int64_t)blockIdx.x * (mb + 1);
+  const int t = threadIdx.x;
+  // each thread scans a contiguous chunk
+  const int per = (mb + 1023) / 1024;
+  const int lo = t * per, hi = min(lo + per, mb);
+  int32_t s = 0;
+  for (int i = lo; i < hi; ++i) s += rp[i + 1];
+  part[t] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    int32_t v = t >= off ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  int32_t run = t > 0 ? part[t - 1] : 0;
+  for (int i = lo; i < hi; ++i) {
+    const int32_t c = rp[i + 1];
+    run += c;
+    rp[i + 1] = run;
+  }
+  if (t == 0) rp[0] = 0;
+}
+
+__global__ __launch_bounds__(256) void row_write_kernel(const uint8_t* __restrict__ mask, int bh, int mb, int n,
+                                                         const int32_t* __restrict__ row_ptr,
+                                                         int32_t* __restrict__ col_idx) {
+  const int64_t row = (int64_t)blockIdx.x * kWavesPerWG + (threadIdx.x >> 6);
+  if (row >= (int64_t)bh * mb) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t h = row / mb;
+  const int i = (int)(row % mb);
+  const uint8_t* p = mask + row * n;
+  int32_t* out = col_idx + h * (int64_t)mb * n + row_ptr[h * (mb + 1) + i];
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int base = 0;
+  for (int j0 = 0; j0 < n; j0 += 64) {
+    const int j = j0 + lane;
+    const bool keep = j < n && p[j] != 0;
+    const uint64_t word = ballot64(keep);
+    if (keep) out[base + __popcll(word & below)] = j;
+    base += __popcll(word);
+  }
+}
+
+// Bit-packed rows: rowbits[(h*mb + i)*nw + w] bit b = M[h][i][64w + b]; row_nnz[h*mb + i] = n_i.
+__global__ __launch_bounds__(256) void pack_rows_kernel(const uint8_t* __restrict__ mask, int64_t rows, int n, int nw,
+                                                        uint64_t* __restrict__ rowbits,
+                                                        int32_t* __restrict__ row_nnz) {
+  const int64_t row = (int64_t)blockIdx.x * kWavesPerWG + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const uint8_t* p = mask + row * n;
+  int cnt = 0;
+  for (int w = 0; w < nw; ++w) {
+    const int j = w * 64 + lane;
+    const uint64_t word = ballot64(j < n && p[j] != 0);
+    if (lane == 0) rowbits[row * nw + w] = word;
+    cnt += __popcll(word);
+  }
+  if (lane == 0) row_nnz[row] = cnt;
+}
+
+// Bit-packed columns from bit-packed rows: colbits[(h*n + j)*mw + v] bit r = M[h][64v + r][j].
+// One wavefront per (head, 64-column group, 64-row group): lane r holds row 64v + r's word.
+__global__ __launch_bounds__(256) void transpose_bits_kernel(const uint64_t* __restrict__ rowbits, int bh, int m,
+                                                             int n, int nw, int mw,
+                                                             uint64_t* __restrict__ colbits) {
+  const int64_t task = (int64_t)blockIdx.x * kWavesPerWG + (threadIdx.x >> 6);
+  const int64_t per_head = (int64_t)nw * mw;
+  if (task >= (int64_t)bh * per_head) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t h = task / per_head;
+  const int rem = (int)(task % per_head);
+  const int cw = rem / mw;   // column word
+  const int v = rem % mw;    // row word
+  const int r = v * 64 + lane;
+  const uint64_t mine = r < m ? rowbits[(h * m + r) * nw + cw] : 0ull;
+  uint64_t out = 0;
+  for (int c = 0; c < 64; ++c) {
+    const uint64_t b = ballot64((mine >> c) & 1ull);
+    if (lane == c) out = b;
+  }
+  const int j = cw * 64 + lane;
+  if (j < n) colbits[(h * n + j) * mw + v] = out;
+}
+
+// Each workgroup records the XCD it runs on (hardware register XCC_ID, bits [3:0]).
+__global__ void xcc_probe_kernel(int32_t* out, int n) {
+  if (threadIdx.x == 0 && (int)blockIdx.x < n)
+    out[blockIdx.x] = (int32_t)(__builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 0xF);
+}
+
+}  // namespace
+
+hipError_t wa_launch_xcc_probe(int32_t* out, int n_wg, hipStream_t stream) {
+  if (n_wg <= 0) return hipSuccess;
+  hipLaunchKernelGGL(xcc_probe_kernel, dim3(n_wg), dim3(64), 0, stream, out, n_wg);
+  return hipGetLastError();
+}
+
+hipError_t wa_launch_row_count(const uint8_t* mask, int64_t rows, int n, int32_t* counts, int64_t count_stride_rows,
+                               int counts_offset, int mb, hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  const int64_t grid = (rows + kWavesPerWG - 1) / kWavesPerWG;
+  hipLaunchKernelGGL(row_count_kernel, dim3((unsigned)grid), dim3(256), 0, stream, mask, rows, n, counts,
+                     count_stride_rows, counts_offset, mb);
+  return hipGetLastError();
+}
+
+hipError_t wa_launch_head_scan(int32_t* row_ptr, int bh, int mb, hipStream_t stream) {
+  if (bh <= 0) return hipSuccess;
+  hipLaunchKernelGGL(head_scan_kernel, dim3(bh), dim3(1024), 0, stream, row_ptr, mb);
+  return hipGetLastError();
+}
+
+hipError_t wa_launch_row_write(const uint8_t* mask, int bh, int mb, int n, const int32_t* row_ptr, int32_t* col_idx,
+                               hipStream_t stream) {
+  const int64_t rows = (int64_t)bh * mb;
+  if (rows <= 0) return hipSuccess;
+  const int64_t grid = (rows + kWavesPerWG - 1) / kWavesPerWG;
+  hipLaunchKernelGGL(row_write_kernel, dim3((unsigned)grid), dim3(256), 0, stream, mask, bh, mb, n, row_ptr, col_idx);
+  return hipGetLastError();
+}
+
+hipError_t wa_launch_pack_rows(const uint8_t* mask, int64_t rows, int n, uint64_t* rowbits, int32_t* row_nnz,
+                               hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  const int nw = (n + 63) / 64;
+  const int64_t grid = (rows + kWavesPerWG - 1) / kWavesPerWG;
+  hipLaunchKernelGGL(pack_rows_kernel, dim3((unsigned)grid), dim3(256), 0, stream, mask, rows, n, nw, rowbits,
+                     row_nnz);
+  return hipGetLastError();
+}
+
+hipError_t wa_launch_transpose_bits(const uint64_t* rowbits, int bh, int m, int n, uint64_t* colbits,
+                                    hipStream_t stream) {
+  const int nw = (n + 63) / 64, mw = (m + 63) / 64;
+  const int64_t tasks = (int64_t)bh * nw * mw;
+  if (tasks <= 0) return hipSuccess;
+  const int64_t grid = (tasks + kWavesPerWG - 1) / kWavesPerWG;
+  hipLaunchKernelGGL(transpose_bits_kernel, dim3((unsigned)grid), dim3(256), 0, stream, rowbits, bh, m, n, nw, mw,
+                     colbits);
+  return hipGetLastError();
+}

@@ -1,0 +1,555 @@
+// Cache-aware query-row permutation for gfx950: one 1024-thread workgroup per head.
+//
+// Phases (Sec. IV-C..IV-E, Alg. 1, Alg. 2):
+//   0  mask statistics from the bit-packed rows and columns (n_i, c_j, nnz,
+//      distinct columns, adjacent-row overlap, sum c_j^2);
+//   1  skip cases 1-3 (fits in L2, too little work, already local);
+//   2  matrix-free centred subspace iteration in exact fixed point: the centred
+//      products are integer sums over the set bits of the packed mask plus the
+//      rank-one centring corrections scaled by m (Alg. 1); the 2-column QR is a
+//      Cholesky-QR of the exactly summed Gram matrix (one IEEE fp64 rounding per
+//      operation, no contraction); then Rayleigh-Ritz with one Jacobi rotation
+//      and a canonical column sign;
+//   3  skip case 4 (the rank-2 embedding keeps too little of ||M~||_F^2);
+//   4  Stage 1: bitonic sort of the rows by polar angle (Eq. 4) with an exact
+//      integer comparator (half-plane class, then the sign of the cross product,
+//      then the row index);
+//   5  Stage 2: the order is cut into n_xcd contiguous segments and each into
+//      buckets of W rows; one bitonic sort over (bucket, -n_i, position) keys
+//      sorts every bucket by descending n_i, stably.
+// Every sum is an exact integer, so the order of parallel reductions does not
+// matter and the result is reproducible bit for bit. Supports m, n <= 4096.
+
+#pragma clang fp contract(off)
+
+#include "common.h"
+#include "perm_launch.h"
+
+namespace {
+
+constexpr int NT = 1024;
+constexpr int NWAVE = NT / 64;
+constexpr int MAXB = 4096;
+
+constexpr int FLAG_FITS_L2 = 1, FLAG_LITTLE_WORK = 2, FLAG_LOCAL = 4, FLAG_UNSTRUCTURED = 8, FLAG_DEGENERATE = 16,
+              FLAG_IDENTITY = 64;
+constexpr int SKIP_AUTO = 0, SKIP_ALWAYS = 2;
+
+struct Shared {
+  int32_t cc[MAXB];          // column counts; later the Stage-1 order
+  int32_t xs[2 * MAXB];      // X (2^30 fixed point), later U
+  int32_t ys[2 * MAXB];      // Ys; later sort scratch (indices, then 64-bit keys)
+  int64_t red[NWAVE * 4];
+  double dbl[8];
+  int64_t i64[8];
+  int32_t i32[8];
+};
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ int bitlen_u64(uint64_t v) { return v ? 64 - __clzll((long long)v) : 0; }
+__device__ __forceinline__ uint64_t uabs64(int64_t v) { return v < 0 ? (uint64_t)(-v) : (uint64_t)v; }
+
+__device__ __forceinline__ int64_t wave_sum(int64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_max(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t u = __shfl_xor(v, o);
+    v = u > v ? u : v;
+  }
+  return v;
+}
+
+// Sum of up to 4 int64 values over the workgroup; the result is returned to every thread.
+template <int K>
+__device__ void block_sum(Shared& sh, int64_t (&v)[K]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int k = 0; k < K; ++k) v[k] = wave_sum(v[k]);
+  if (lane == 0)
+#pragma unroll
+    for (int k = 0; k < K; ++k) sh.red[w * 4 + k] = v[k];
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    int64_t s = 0;
+    for (int i = 0; i < NWAVE; ++i) s += sh.red[i * 4 + k];
+    v[k] = s;
+  }
+  __syncthreads();
+}
+
+__device__ uint64_t block_max(Shared& sh, uint64_t v) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = wave_max(v);
+  if (lane == 0) sh.red[w * 4] = (int64_t)v;
+  __syncthreads();
+  uint64_t r = 0;
+  for (int i = 0; i < NWAVE; ++i) {
+    uint64_t u = (uint64_t)sh.red[i * 4];
+    r = u > r ? u : r;
+  }
+  __syncthreads();
+  return r;
+}
+
+struct Head {
+  const uint64_t* rowbits;  // [m][nw]
+  const uint64_t* colbits;  // [n][mw]
+  const int32_t* row_nnz;   // [m]
+  int64_t* zbuf;            // [m][2]
+  int64_t* ybuf;            // [n][2]
+  int m, n, nw, mw;
+};
+
+// Cholesky-QR of zbuf (m x 2) into sh.xs; returns true if degenerate (first column zero).
+__device__ bool orth(Shared& sh, const Head& H) {
+  const int tid = threadIdx.x;
+  uint64_t mx = 0;
+  for (int i = tid; i < H.m; i += NT) {
+    const uint64_t a = uabs64(H.zbuf[2 * i]), b = uabs64(H.zbuf[2 * i + 1]);
+    mx = a > mx ? a : mx;
+    mx = b > mx ? b : mx;
+  }
+  mx = block_max(sh, mx);
+  const int bl = bitlen_u64(mx);
+  const int s = bl > 24 ? bl - 24 : 0;
+  int64_t g[3] = {0, 0, 0};
+  for (int i = tid; i < H.m; i += NT) {
+    const int64_t z0 = H.zbuf[2 * i] >> s, z1 = H.zbuf[2 * i + 1] >> s;
+    g[0] += z0 * z0;
+    g[1] += z0 * z1;
+    g[2] += z1 * z1;
+  }
+  block_sum<3>(sh, g);
+  if (g[0] == 0) return true;
+  if (tid == 0) {
+    const double G11 = (double)g[0], G12 = (double)g[1], G22 = (double)g[2];
+    const double r11 = __builtin_sqrt(G11);
+    const double r12 = G12 / r11;
+    const double u = G22 - r12 * r12;
+    const bool rank2 = u > G22 * 0x1p-30;
+    sh.dbl[0] = r11;
+    sh.dbl[1] = r12;
+    sh.dbl[2] = rank2 ? __builtin_sqrt(u) : 0.0;
+    sh.i32[0] = rank2 ? 1 : 0;
+  }
+  __syncthreads();
+  const double r11 = sh.dbl[0], r12 = sh.dbl[1], r22 = sh.dbl[2];
+  const bool rank2 = sh.i32[0] != 0;
+  for (int i = tid; i < H.m; i += NT) {
+    const double q0 = (double)(H.zbuf[2 * i] >> s) / r11;
+    sh.xs[2 * i] = (int32_t)__builtin_rint(q0 * 1073741824.0);
+    if (rank2) {
+      const double q1 = ((double)(H.zbuf[2 * i + 1] >> s) - r12 * q0) / r22;
+      sh.xs[2 * i + 1] = (int32_t)__builtin_rint(q1 * 1073741824.0);
+    } else {
+      sh.xs[2 * i + 1] = 0;
+    }
+  }
+  __syncthreads();
+  return false;
+}
+
+// zbuf = m * M~ Ys with Ys = (m * M~^T X) >> sy, both exact; returns sy.
+__device__ int centred_apply(Shared& sh, const Head& H) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t m = H.m;
+  // YA[j] = sum_i M[i][j] X[i]: one wavefront per column, lanes over 64-row words
+  for (int j = w; j < H.n; j += NWAVE) {
+    int64_t s0 = 0, s1 = 0;
+    const uint64_t* cb = H.colbits + (int64_t)j * H.mw;
+    for (int v = lane; v < H.mw; v += 64) {
+      uint64_t word = cb[v];
+      while (word) {
+        const int b = __ffsll((long long)word) - 1;
+        word &= word - 1;
+        const int i = v * 64 + b;
+        s0 += sh.xs[2 * i];
+        s1 += sh.xs[2 * i + 1];
+      }
+    }
+    s0 = wave_sum(s0);
+    s1 = wave_sum(s1);
+    if (lane == 0) {
+      H.ybuf[2 * j] = s0;
+      H.ybuf[2 * j + 1] = s1;
+    }
+  }
+  int64_t sx[2] = {0, 0};
+  for (int i = tid; i < H.m; i += NT) {
+    sx[0] += sh.xs[2 * i];
+    sx[1] += sh.xs[2 * i + 1];
+  }
+  block_sum<2>(sh, sx);  // contains the barrier that publishes ybuf
+  uint64_t mx = 0;
+  for (int j = tid; j < H.n; j += NT) {
+    const int64_t c = sh.cc[j];
+    const int64_t y0 = m * H.ybuf[2 * j] - c * sx[0];
+    const int64_t y1 = m * H.ybuf[2 * j + 1] - c * sx[1];
+    H.ybuf[2 * j] = y0;
+    H.ybuf[2 * j + 1] = y1;
+    const uint64_t a = uabs64(y0), b = uabs64(y1);
+    mx = a > mx ? a : mx;
+    mx = b > mx ? b : mx;
+  }
+  mx = block_max(sh, mx);
+  const int bl = bitlen_u64(mx);
+  const int sy = bl > 30 ? bl - 30 : 0;
+  for (int j = tid; j < H.n; j += NT) {
+    sh.ys[2 * j] = (int32_t)(H.ybuf[2 * j] >> sy);
+    sh.ys[2 * j + 1] = (int32_t)(H.ybuf[2 * j + 1] >> sy);
+  }
+  __syncthreads();
+  // ZA[i] = sum_j M[i][j] Ys[j]: one wavefront per row
+  for (int i = w; i < H.m; i += NWAVE) {
+    int64_t s0 = 0, s1 = 0;
+    const uint64_t* rb = H.rowbits + (int64_t)i * H.nw;
+    for (int v = lane; v < H.nw; v += 64) {
+      uint64_t word = rb[v];
+      while (word) {
+        const int b = __ffsll((long long)word) - 1;
+        word &= word - 1;
+        const int j = v * 64 + b;
+        s0 += sh.ys[2 * j];
+        s1 += sh.ys[2 * j + 1];
+      }
+    }
+    s0 = wave_sum(s0);
+    s1 = wave_sum(s1);
+    if (lane == 0) {
+      H.zbuf[2 * i] = s0;
+      H.zbuf[2 * i + 1] = s1;
+    }
+  }
+  int64_t syy[2] = {0, 0};
+  for (int j = tid; j < H.n; j += NT) {
+    syy[0] += (int64_t)sh.cc[j] * sh.ys[2 * j];
+    syy[1] += (int64_t)sh.cc[j] * sh.ys[2 * j + 1];
+  }
+  block_sum<2>(sh, syy);
+  for (int i = tid; i < H.m; i += NT) {
+    H.zbuf[2 * i] = m * H.zbuf[2 * i] - syy[0];
+    H.zbuf[2 * i + 1] = m * H.zbuf[2 * i + 1] - syy[1];
+  }
+  __syncthreads();
+  return sy;
+}
+
+__device__ __forceinline__ int angle_class(int64_t x, int64_t y) {
+  if (y < 0) return 0;
+  if (y == 0) return x >= 0 ? 1 : 3;
+  return 2;
+}
+
+// true if row a precedes row b in ascending polar angle (ties: smaller index); -1 is +infinity
+__device__ __forceinline__ bool angle_less(const Shared& sh, int a, int b) {
+  if (a < 0) return false;
+  if (b < 0) return true;
+  const int64_t xa = sh.xs[2 * a], ya = sh.xs[2 * a + 1];
+  const int64_t xb = sh.xs[2 * b], yb = sh.xs[2 * b + 1];
+  const int ca = angle_class(xa, ya), cb = angle_class(xb, yb);
+  if (ca != cb) return ca < cb;
+  if (ca == 0 || ca == 2) {
+    const int64_t cross = xa * yb - ya * xb;
+    if (cross != 0) return cross > 0;
+  }
+  return a < b;
+}
+
+__global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+  const int tid = threadIdx.x;
+  const int h = blockIdx.x;
+  const int m = a.m, n = a.n;
+  Head H;
+  H.m = m;
+  H.n = n;
+  H.nw = (n + 63) / 64;
+  H.mw = (m + 63) / 64;
+  H.rowbits = a.rowbits + (int64_t)h * m * H.nw;
+  H.colbits = a.colbits + (int64_t)h * n * H.mw;
+  H.row_nnz = a.row_nnz + (int64_t)h * m;
+  H.zbuf = a.zbuf + (int64_t)h * 2 * m;
+  H.ybuf = a.ybuf + (int64_t)h * 2 * n;
+
+  // ---- phase 0: statistics ----
+  int64_t st[4] = {0, 0, 0, 0};  // nnz, distinct, sum c^2, (unused)
+  for (int j = tid; j < n; j += NT) {
+    int c = 0;
+    const uint64_t* cb = H.colbits + (int64_t)j * H.mw;
+    for (int v = 0; v < H.mw; ++v) c += __popcll(cb[v]);
+    sh.cc[j] = c;
+    if (a.col_cnt) a.col_cnt[(int64_t)h * n + j] = c;
+    st[1] += c > 0;
+    st[2] += (int64_t)c * c;
+  }
+  for (int i = tid; i < m; i += NT) st[0] += H.row_nnz[i];
+  int64_t adj[2] = {0, 0};
+  for (int t = tid; t < (m - 1) * H.nw; t += NT) {
+    const int i = t / H.nw, w = t % H.nw;
+    const uint64_t x = H.rowbits[(int64_t)i * H.nw + w], y = H.rowbits[(int64_t)(i + 1) * H.nw + w];
+    adj[0] += __popcll(x & y);
+    adj[1] += __popcll(x | y);
+  }
+  block_sum<4>(sh, st);
+  block_sum<2>(sh, adj);
+  const int64_t nnz = st[0], distinct = st[1], sum_c2 = st[2];
+  if (a.head_stats && tid == 0) {
+    int64_t* hs = a.head_stats + (int64_t)h * 6;
+    hs[0] = nnz;
+    hs[1] = distinct;
+    hs[2] = adj[0];
+    hs[3] = adj[1];
+    hs[4] = sum_c2;
+    hs[5] = 0;
+  }
+  if (a.stats_only) return;
+
+  // ---- phase 1: skip cases 1-3 ----
+  if (tid == 0) {
+    int f = 0;
+    const double kvb = (double)(2 * a.block * a.head_dim * 2);
+    if ((double)distinct * kvb <= a.prof.l2_bytes_per_xcd) f |= FLAG_FITS_L2;
+    const double saving = (double)nnz * a.prof.gain_ns_per_block;
+    const double cost = a.prof.ovh_ns_fixed + a.prof.ovh_ns_per_row * (double)m + a.prof.ovh_ns_per_nnz * (double)nnz;
+    if (saving < cost) f |= FLAG_LITTLE_WORK;
+    if (adj[1] > 0 && (double)adj[0] / (double)adj[1] >= a.prof.j_max) f |= FLAG_LOCAL;
+    sh.i32[1] = f;
+  }
+  __syncthreads();
+  int flags = sh.i32[1];
+  int32_t* perm = a.perm + (int64_t)h * m;
+  if (a.skip_mode == SKIP_ALWAYS || (a.skip_mode == SKIP_AUTO && flags != 0)) {
+    for (int i = tid; i < m; i += NT) {
+      perm[i] = i;
+      if (a.stage1) a.stage1[(int64_t)h * m + i] = i;
+      if (a.embedding) {
+        a.embedding[((int64_t)h * m + i) * 2] = 0;
+        a.embedding[((int64_t)h * m + i) * 2 + 1] = 0;
+      }
+    }
+    if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
+    return;
+  }
+
+  // ---- phase 2: MFCSI ----
+  for (int i = tid; i < m; i += NT) {
+    const uint64_t base = a.seed + 2ull * ((uint64_t)h * (uint64_t)m + (uint64_t)i);
+    H.zbuf[2 * i] = (int64_t)(splitmix64(base) >> 40) - (1ll << 23);
+    H.zbuf[2 * i + 1] = (int64_t)(splitmix64(base + 1ull) >> 40) - (1ll << 23);
+  }
+  __syncthreads();
+  bool degen = orth(sh, H);
+  for (int it = 0; it < a.iters && !degen; ++it) {
+    centred_apply(sh, H);
+    degen = orth(sh, H);
+  }
+  int64_t trace = 0;
+  int scale_exp = 0;
+  if (!degen) {
+    const int sy = centred_apply(sh, H);
+    uint64_t mx = 0;
+    for (int i = tid; i < m; i += NT) {
+      const uint64_t p = uabs64(H.zbuf[2 * i]), q = uabs64(H.zbuf[2 * i + 1]);
+      mx = p > mx ? p : mx;
+      mx = q > mx ? q : mx;
+    }
+    mx = block_max(sh, mx);
+    const int bl = bitlen_u64(mx);
+    const int s_r = bl > 24 ? bl - 24 : 0;
+    int64_t b[4] = {0, 0, 0, 0};
+    for (int i = tid; i < m; i += NT) {
+      const int64_t x0 = sh.xs[2 * i] >> 6, x1 = sh.xs[2 * i + 1] >> 6;
+      const int64_t z0 = H.zbuf[2 * i] >> s_r, z1 = H.zbuf[2 * i + 1] >> s_r;
+      b[0] += x0 * z0;
+      b[1] += x0 * z1;
+      b[2] += x1 * z0;
+      b[3] += x1 * z1;
+    }
+    block_sum<4>(sh, b);
+    trace = b[0] + b[3];
+    scale_exp = sy + s_r + 6 - 60;
+    if (tid == 0) {
+      const double A = (double)b[0], C = (double)b[3], B = (double)((b[1] + b[2]) >> 1);
+      double t = 0.0, cs = 1.0, sn = 0.0;
+      if (B != 0.0) {
+        const double tau = (C - A) / (2.0 * B);
+        const double sgn = tau >= 0.0 ? 1.0 : -1.0;
+        t = sgn / (__builtin_fabs(tau) + __builtin_sqrt(1.0 + tau * tau));
+        cs = 1.0 / __builtin_sqrt(1.0 + t * t);
+        sn = t * cs;
+      }
+      const double lam0 = A - t * B, lam1 = C + t * B;
+      sh.dbl[3] = cs;
+      sh.dbl[4] = sn;
+      sh.i32[2] = lam1 > lam0 ? 1 : 0;
+    }
+    __syncthreads();
+    const double cs = sh.dbl[3], sn = sh.dbl[4];
+    const bool swp = sh.i32[2] != 0;
+    for (int i = tid; i < m; i += NT) {
+      const double x0 = (double)sh.xs[2 * i], x1 = (double)sh.xs[2 * i + 1];
+      const int32_t u0 = (int32_t)__builtin_rint(cs * x0 - sn * x1);
+      const int32_t u1 = (int32_t)__builtin_rint(sn * x0 + cs * x1);
+      sh.xs[2 * i] = swp ? u1 : u0;
+      sh.xs[2 * i + 1] = swp ? u0 : u1;
+    }
+    __syncthreads();
+    // canonical sign: the entry of largest magnitude (smallest row on ties) is positive
+    for (int k = 0; k < 2; ++k) {
+      uint64_t key = 0;
+      for (int i = tid; i < m; i += NT) {
+        const uint64_t c = ((uint64_t)uabs64(sh.xs[2 * i + k]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+        key = c > key ? c : key;
+      }
+      key = block_max(sh, key);
+      const int istar = (int)(0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull));
+      const bool neg = sh.xs[2 * istar + k] < 0;
+      __syncthreads();
+      if (neg)
+        for (int i = tid; i < m; i += NT) sh.xs[2 * i + k] = -sh.xs[2 * i + k];
+      __syncthreads();
+    }
+  }
+
+  // ---- phase 3: skip case 4 ----
+  if (tid == 0) {
+    int f = flags;
+    if (degen) {
+      f |= FLAG_DEGENERATE;
+    } else {
+      const double den = (double)m * (double)((int64_t)m * nnz - sum_c2);
+      const double eta = den <= 0.0 ? 0.0 : __builtin_ldexp((double)trace, scale_exp) / den;
+      if (eta < a.prof.eta_min) f |= FLAG_UNSTRUCTURED;
+    }
+    sh.i32[1] = f;
+  }
+  __syncthreads();
+  flags = sh.i32[1];
+  if (a.embedding)
+    for (int i = tid; i < m; i += NT) {
+      a.embedding[((int64_t)h * m + i) * 2] = degen ? 0 : sh.xs[2 * i];
+      a.embedding[((int64_t)h * m + i) * 2 + 1] = degen ? 0 : sh.xs[2 * i + 1];
+    }
+  if (a.skip_mode == SKIP_AUTO && (flags & FLAG_UNSTRUCTURED)) {
+    for (int i = tid; i < m; i += NT) {
+      perm[i] = i;
+      if (a.stage1) a.stage1[(int64_t)h * m + i] = i;
+    }
+    if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
+    return;
+  }
+
+  // ---- phase 4: Stage 1, exact polar-angle order ----
+  int P = 1;
+  while (P < m) P <<= 1;
+  int32_t* idx = sh.ys;
+  for (int i = tid; i < P; i += NT) idx[i] = i < m ? i : -1;
+  __syncthreads();
+  if (!degen) {
+    for (int k = 2; k <= P; k <<= 1)
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        for (int t = tid; t < P / 2; t += NT) {
+          const int i = (t / j) * 2 * j + (t % j);
+          const int p = i + j;
+          const int x = idx[i], y = idx[p];
+          const bool up = (i & k) == 0;
+          const bool sw = up ? angle_less(sh, y, x) : angle_less(sh, x, y);
+          if (sw) {
+            idx[i] = y;
+            idx[p] = x;
+          }
+        }
+        __syncthreads();
+      }
+  }
+  for (int i = tid; i < m; i += NT) sh.cc[i] = idx[i];
+  __syncthreads();
+  if (a.stage1)
+    for (int i = tid; i < m; i += NT) a.stage1[(int64_t)h * m + i] = sh.cc[i];
+
+  // ---- phase 5: segments, wave buckets, Stage 2 ----
+  uint64_t* keys = reinterpret_cast<uint64_t*>(sh.ys);
+  const int base = m / a.n_xcd, extra = m % a.n_xcd;
+  for (int p = tid; p < P; p += NT) {
+    if (p >= m) {
+      keys[p] = ~0ull;
+      continue;
+    }
+    int x, off;
+    const int big = extra * (base + 1);
+    if (p < big) {
+      x = p / (base + 1);
+      off = p - x * (base + 1);
+    } else {
+      x = extra + (p - big) / base;
+      off = p - big - (x - extra) * base;
+    }
+    const uint64_t bucket = ((uint64_t)x << 12) | (uint64_t)(off / a.wave);
+    const int row = sh.cc[p];
+    const uint64_t nz = (uint64_t)H.row_nnz[row];
+    keys[p] = (bucket << 32) | ((0xFFFFull - nz) << 16) | (uint64_t)p;
+  }
+  __syncthreads();
+  for (int k = 2; k <= P; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int t = tid; t < P / 2; t += NT) {
+        const int i = (t / j) * 2 * j + (t % j);
+        const int p = i + j;
+        const uint64_t x = keys[i], y = keys[p];
+        const bool up = (i & k) == 0;
+        if (up ? (y < x) : (x < y)) {
+          keys[i] = y;
+          keys[p] = x;
+        }
+      }
+      __syncthreads();
+    }
+  for (int s = tid; s < m; s += NT) perm[s] = sh.cc[(int)(keys[s] & 0xFFFFull)];
+  if (a.flags && tid == 0) a.flags[h] = (uint8_t)flags;
+}
+
+// Arithmetic self-check: the fp64 operations the permutation relies on, evaluated on the GPU.
+__global__ void fp64_probe_kernel(const double* a, const double* b, const int64_t* c, double* out, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const double x = a[i], y = b[i];
+  out[6 * i + 0] = __builtin_sqrt(__builtin_fabs(x));
+  out[6 * i + 1] = x / y;
+  out[6 * i + 2] = (double)c[i];
+  out[6 * i + 3] = __builtin_rint(x * 1073741824.0);
+  out[6 * i + 4] = x * y - y * 3.0;
+  out[6 * i + 5] = __builtin_ldexp(x, (int)(c[i] & 31) - 16);
+}
+
+}  // namespace
+
+size_t wa_perm_shared_bytes() { return sizeof(Shared); }
+
+hipError_t wa_launch_perm_heads(const WaPermLaunch& a, hipStream_t stream) {
+  if (a.bh <= 0) return hipSuccess;
+  const size_t smem = sizeof(Shared);
+  hipError_t e = hipFuncSetAttribute((const void*)perm_head_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)smem);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(perm_head_kernel, dim3(a.bh), dim3(NT), smem, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t wa_launch_fp64_probe(const double* a, const double* b, const int64_t* c, double* out, int n,
+                                hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fp64_probe_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a, b, c, out, n);
+  return hipGetLastError();
+}
