@@ -155,7 +155,9 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
 wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* row_ptr, int32_t* col_idx,
                           void* stream);
 
-/* Workspace bytes needed by wa_sparse_attn (the compacted lists). */
+/* Workspace bytes needed by wa_sparse_attn: a zero-padded transposed copy of V
+ * (bf16 [B][H][head_dim][M_B*block]) followed by the compacted lists. The V^T
+ * copy alone (the leading part) suffices for wa_sparse_attn_csr. */
 wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Block-sparse attention forward: for every query block i and token q in it,
@@ -178,10 +180,13 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
                          const wa_shape* shape, float softmax_scale, int32_t n_xcd, void* o, float* lse,
                          void* workspace, size_t workspace_bytes, void* stream);
 
-/* As wa_sparse_attn, from lists already built by wa_compact_mask. */
+/* As wa_sparse_attn, from lists already built by wa_compact_mask (row i of head
+ * (b,h) visits col_idx[(b*H+h)*M_B*N_B + row_ptr[b][h][i] ...] in list order).
+ * workspace >= B*H*head_dim*M_B*block*2 bytes (rounded up to 256), 256-byte aligned. */
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                              const int32_t* col_idx, const int32_t* perm, const wa_shape* shape,
-                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* stream);
+                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* workspace,
+                             size_t workspace_bytes, void* stream);
 
 /* ---- diagnostics (used by the test suite; not needed by callers) ---- */
 

@@ -56,7 +56,8 @@ _SIGNATURES = {
     "wa_sparse_attn": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(WaShape), c_float,
                                  c_int32, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "wa_sparse_attn_csr": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                     POINTER(WaShape), c_float, c_int32, c_void_p, c_void_p, c_void_p]),
+                                     POINTER(WaShape), c_float, c_int32, c_void_p, c_void_p, c_void_p, c_size_t,
+                                     c_void_p]),
     "wa_fp64_probe": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p]),
     "wa_xcc_probe": (c_int32, [c_void_p, c_int32, c_void_p]),
 }

@@ -95,15 +95,16 @@ def mask_stats(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 
 def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int, wave: Optional[int] = None,
                       n_xcd: int = 8, iters: int = 10, seed: int = 0, skip: str = "auto",
                       profile: Optional[L.WaSkipProfile] = None, workspace: Optional[torch.Tensor] = None,
-                      return_info: bool = False):
+                      return_info: bool = False, out: Optional[torch.Tensor] = None,
+                      flags_out: Optional[torch.Tensor] = None):
     """perm int32 [B][H][M_B] and head flags uint8 [B][H] (plus embedding and Stage-1 order if asked)."""
     lib = L.load()
     mask = _mask_u8(mask)
     b, h, mb, nb = mask.shape
     shape = shape_of(b, h, seq_len, head_dim, block)
     dev = mask.device
-    perm = torch.empty((b, h, mb), dtype=torch.int32, device=dev)
-    flags = torch.empty((b, h), dtype=torch.uint8, device=dev)
+    perm = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if out is None else out
+    flags = torch.empty((b, h), dtype=torch.uint8, device=dev) if flags_out is None else flags_out
     emb = torch.empty((b, h, mb, 2), dtype=torch.int32, device=dev) if return_info else None
     s1 = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if return_info else None
     params = L.WaPermParams(0 if wave is None else int(wave), int(n_xcd), int(iters), _SKIP[skip],
@@ -120,14 +121,19 @@ def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim:
     return perm, flags
 
 
-def compact_mask(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 128):
+def compact_mask(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 128,
+                 row_ptr: Optional[torch.Tensor] = None, col_idx: Optional[torch.Tensor] = None):
     """CSR lists: row_ptr int32 [B][H][M_B+1] (head-local offsets), col_idx int32 [B*H*M_B*N_B]."""
     lib = L.load()
     mask = _mask_u8(mask)
     b, h, mb, nb = mask.shape
     shape = shape_of(b, h, seq_len, head_dim, block)
-    row_ptr = torch.empty((b, h, mb + 1), dtype=torch.int32, device=mask.device)
-    col_idx = torch.empty((b * h * mb * nb,), dtype=torch.int32, device=mask.device)
+    if row_ptr is None:
+        row_ptr = torch.empty((b, h, mb + 1), dtype=torch.int32, device=mask.device)
+    if col_idx is None:
+        col_idx = torch.empty((b * h * mb * nb,), dtype=torch.int32, device=mask.device)
+    if row_ptr.numel() < b * h * (mb + 1) or col_idx.numel() < b * h * mb * nb:
+        raise ValueError("row_ptr / col_idx too small")
     L.check(lib.wa_compact_mask(_ptr(mask), ctypes.byref(shape), _ptr(row_ptr), _ptr(col_idx), _stream()))
     return row_ptr, col_idx
 
@@ -167,14 +173,18 @@ def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: torch.T
 
 
 def sparse_attn_csr(q, k, v, row_ptr, col_idx, perm=None, *, block: int, scale: Optional[float] = None,
-                    n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None):
+                    n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None):
     lib = L.load()
     shape = _attn_args(q, k, v, block)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if return_lse else None
+    need = attn_workspace_size(shape)
+    if workspace is None or workspace.numel() < need:
+        workspace = _workspace(need, q.device)
     L.check(lib.wa_sparse_attn_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr), _ptr(col_idx), _ptr(perm),
                                    ctypes.byref(shape), float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse),
-                                   _stream()))
+                                   _ptr(workspace), workspace.numel(), _stream()))
     return (o, lse) if return_lse else o
 
 

@@ -90,8 +90,10 @@ PermWs perm_ws_layout(const Dims& d) {
   return w;
 }
 
+// Attention workspace: [V^T copy][row_ptr][col_idx]; the CSR entry point uses only the V^T part.
+size_t attn_vt_bytes(const Dims& d) { return align_up(wa_vt_bytes(d.bh, d.mb, d.d, d.blk)); }
 size_t attn_ws_bytes(const Dims& d) {
-  return align_up((size_t)d.bh * (d.mb + 1) * 4) + align_up((size_t)d.bh * d.mb * d.mb * 4);
+  return attn_vt_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4) + align_up((size_t)d.bh * d.mb * d.mb * 4);
 }
 
 wa_status check_ws(void* ws, size_t have, size_t need) {
@@ -130,11 +132,11 @@ wa_status launch_compact(const uint8_t* mask, const Dims& d, int32_t* row_ptr, i
   return WA_OK;
 }
 
-wa_status launch_attn(const void* q, const void* k, const void* v, const int32_t* row_ptr, const int32_t* col_idx,
-                      const int32_t* perm, const Dims& d, float scale, int32_t n_xcd, void* o, float* lse,
-                      hipStream_t st) {
+wa_status launch_attn(const void* q, const void* k, const void* v, void* vt, const int32_t* row_ptr,
+                      const int32_t* col_idx, const int32_t* perm, const Dims& d, float scale, int32_t n_xcd, void* o,
+                      float* lse, hipStream_t st) {
   WaAttnLaunch a{};
-  a.q = q; a.k = k; a.v = v;
+  a.q = q; a.k = k; a.v = v; a.vt = vt;
   a.row_ptr = row_ptr; a.col_idx = col_idx; a.perm = perm;
   a.o = o; a.lse = lse;
   a.bh = (int32_t)d.bh; a.seq_len = d.n; a.mb = d.mb; a.head_dim = d.d; a.block = d.blk; a.n_xcd = n_xcd;
@@ -316,18 +318,20 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
   s = check_ws(workspace, workspace_bytes, attn_ws_bytes(d));
   if (s != WA_OK) return s;
   hipStream_t st = (hipStream_t)stream;
-  int32_t* row_ptr = (int32_t*)workspace;
-  int32_t* col_idx = (int32_t*)((char*)workspace + align_up((size_t)d.bh * (d.mb + 1) * 4));
+  char* base = (char*)workspace;
+  int32_t* row_ptr = (int32_t*)(base + attn_vt_bytes(d));
+  int32_t* col_idx = (int32_t*)(base + attn_vt_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4));
   s = launch_compact(mask, d, row_ptr, col_idx, st);
   if (s != WA_OK) return s;
-  s = launch_attn(q, k, v, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse, st);
+  s = launch_attn(q, k, v, base, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse, st);
   if (s != WA_OK) return s;
   return ok();
 }
 
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                              const int32_t* col_idx, const int32_t* perm, const wa_shape* shape,
-                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* stream) {
+                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* workspace,
+                             size_t workspace_bytes, void* stream) {
   Dims d;
   wa_status s = check_shape(shape, &d);
   if (s != WA_OK) return s;
@@ -335,7 +339,10 @@ wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const 
   if (s != WA_OK) return s;
   if (!row_ptr || !col_idx) return fail(WA_ERR_INVALID_ARG, "row_ptr and col_idx must be non-null");
   if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
-  s = launch_attn(q, k, v, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse, (hipStream_t)stream);
+  s = check_ws(workspace, workspace_bytes, attn_vt_bytes(d));
+  if (s != WA_OK) return s;
+  s = launch_attn(q, k, v, workspace, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse,
+                  (hipStream_t)stream);
   if (s != WA_OK) return s;
   return ok();
 }

@@ -107,7 +107,9 @@ def test_sparse_attn_validation():
     assert call(ws_bytes=ws_n.value - 1) == L.WA_ERR_WORKSPACE
     assert b"workspace" in lib.wa_last_error()
     assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, None, FAKE, None, ctypes.byref(s), 0.0, 8, FAKE, None,
-                                  None) == L.WA_ERR_INVALID_ARG
+                                  ctypes.c_void_p(1 << 24), ws_n.value, None) == L.WA_ERR_INVALID_ARG
+    assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, FAKE, FAKE, None, ctypes.byref(s), 0.0, 8, FAKE, None,
+                                  ctypes.c_void_p(1 << 24), 1024, None) == L.WA_ERR_WORKSPACE
 
 
 def test_build_permutation_validation():
