@@ -99,10 +99,14 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="long-720p-401f", choices=sorted(CONFIGS))
     ap.add_argument("--variants", default="reordered,natural",
-                    help="comma list of reordered (skip never), natural (identity), auto, naive (identity, "
-                         "plain dispatch order)")
+                    help="comma list of: reordered (two-stage order, work-balanced XCD segments, skip never), "
+                         "natural (identity order, equal row-count XCD segments), auto (adaptive skip), "
+                         "naive (identity, plain dispatch order), reordered-rowseg (two-stage order, equal "
+                         "row-count segments), natural-balanced (identity order, work-balanced segments)")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of this many MiB (3 times), to calibrate the HBM counters")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -114,6 +118,15 @@ def main() -> int:
     import paper_2609_34814_amd as W
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
+        return 0
     wl = CONFIGS[args.config]
     t0 = time.perf_counter()
     mask = make_mask(wl, threads=16)
@@ -135,26 +148,31 @@ def main() -> int:
     col_idx = torch.empty((b_ * h_ * mb * mb,), dtype=torch.int32, device="cuda")
     o = torch.empty_like(qd)
     flags = torch.empty((b_, h_), dtype=torch.uint8, device="cuda")
+    seg = torch.empty((b_, h_, 9), dtype=torch.int32, device="cuda")
     attn_ws = torch.empty(W.attn_workspace_size(shape), dtype=torch.uint8, device="cuda")
     wave = W.wave_size(wl.head_dim, wl.block)
     stream = torch.cuda.current_stream()
     log(f"uploaded; nnz={nnz} density={nnz / (b_ * h_ * mb * mb):.4f} wave_per_xcd={wave}")
 
     def make_step(variant):
-        skip = {"reordered": "never", "auto": "auto"}.get(variant)
+        skip = {"reordered": "never", "auto": "auto", "reordered-rowseg": "never",
+                "natural-balanced": "always"}.get(variant)
         n_xcd = 1 if variant == "naive" else 8
+        use_seg = variant in ("reordered", "auto", "natural-balanced")
 
         def step(ev=None):
             p = None
             if skip is not None:
                 W.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
-                                    wave=wave, n_xcd=8, skip=skip, workspace=perm_ws, out=perm, flags_out=flags)
+                                    wave=wave, n_xcd=8, skip=skip, workspace=perm_ws, out=perm, flags_out=flags,
+                                    seg_out=seg)
                 p = perm
             rp, ci = W.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
                                     row_ptr=row_ptr, col_idx=col_idx)
             if ev is not None:
                 ev[0].record(stream)
-            W.sparse_attn_csr(qd, kd, vd, rp, ci, p, block=wl.block, n_xcd=n_xcd, out=o, workspace=attn_ws)
+            W.sparse_attn_csr(qd, kd, vd, rp, ci, p, seg if use_seg else None, block=wl.block, n_xcd=n_xcd,
+                              out=o, workspace=attn_ws)
             if ev is not None:
                 ev[1].record(stream)
         return step

@@ -135,18 +135,21 @@ wa_status wa_perm_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Two-stage cache-aware row permutation per head (Alg. 2 with MFCSI, Alg. 1):
  * Stage 1 orders rows by the polar angle of their rank-2 centred spectral
- * embedding (Eq. 2-4); the order is split into n_xcd contiguous segments and
- * each segment into buckets of wave_per_xcd rows; Stage 2 sorts each bucket
- * by descending n_i (stable). Integer-exact fixed-point arithmetic makes the
- * result identical on every run and to the reference reading.
+ * embedding (Eq. 2-4); the order is split into n_xcd contiguous segments of
+ * equal work (sum of n_i + 1), one per XCD, and each segment into buckets of
+ * wave_per_xcd rows; Stage 2 sorts each bucket by descending n_i (stable).
+ * Integer-exact fixed-point arithmetic makes the result identical on every run
+ * and to the reference reading.
  *   perm         out int32 [B][H][M_B] (required)
+ *   seg_start    out int32 [B][H][n_xcd+1] slot where each XCD segment starts
+ *                (last entry M_B), nullable; pass it to wa_sparse_attn with the same n_xcd
  *   head_flags   out uint8 [B][H] WA_FLAG_* bits, nullable
  *   embedding    out int32 [B][H][M_B][2] canonical (u1, u2), 2^30 per unit, nullable
  *                (zeros for heads that skipped Stage 1)
  *   stage1_order out int32 [B][H][M_B] Stage-1 order, nullable (identity when skipped) */
 wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const wa_perm_params* params,
-                               int32_t* perm, uint8_t* head_flags, int32_t* embedding, int32_t* stage1_order,
-                               void* workspace, size_t workspace_bytes, void* stream);
+                               int32_t* perm, int32_t* seg_start, uint8_t* head_flags, int32_t* embedding,
+                               int32_t* stage1_order, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Compacted per-row KV-block index lists (the mask-selected inner loop of Sec. II-C):
  *   row_ptr out int32 [B][H][M_B+1]: exclusive prefix sum of n_i, local to the head
@@ -169,22 +172,26 @@ wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
  * A query block with no kept KV block gets O = 0 and LSE = -inf.
  *   q, k, v      bf16 [B][H][N][d], 16-byte aligned
  *   perm         int32 [B][H][M_B], NULL = identity (not checked for bijectivity)
+ *   seg_start    int32 [B][H][n_xcd+1] XCD segment table from wa_build_permutation,
+ *                NULL = segments of equal row count (the first M_B mod n_xcd one longer)
  *   softmax_scale  <= 0 selects 1/sqrt(d)
- *   n_xcd        8: slot s of a head runs on XCD x of the contiguous segment containing s
- *                (workgroup g of the head runs slot seg_start(g mod 8) + g / 8);
- *                1: slot = workgroup index (plain dispatch order)
+ *   n_xcd        number of XCD segments: the workgroups of a head are dispatched round-robin
+ *                over the XCDs, and the ceil(M_B/n_xcd) workgroups of XCD x run the slots of
+ *                segment x in order, each taking ceil(len_x / ceil(M_B/n_xcd)) consecutive
+ *                slots; 1: slot = workgroup index (plain dispatch order)
  *   o            out bf16 [B][H][N][d]
  *   lse          out float [B][H][N] natural-log sum-exp of the scaled scores, nullable
  *   workspace    >= wa_attn_workspace_size(shape) */
 wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint8_t* mask, const int32_t* perm,
-                         const wa_shape* shape, float softmax_scale, int32_t n_xcd, void* o, float* lse,
-                         void* workspace, size_t workspace_bytes, void* stream);
+                         const int32_t* seg_start, const wa_shape* shape, float softmax_scale, int32_t n_xcd,
+                         void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream);
 
 /* As wa_sparse_attn, from lists already built by wa_compact_mask (row i of head
  * (b,h) visits col_idx[(b*H+h)*M_B*N_B + row_ptr[b][h][i] ...] in list order).
  * workspace >= B*H*head_dim*M_B*block*2 bytes (rounded up to 256), 256-byte aligned. */
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
-                             const int32_t* col_idx, const int32_t* perm, const wa_shape* shape,
+                             const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
+                             const wa_shape* shape,
                              float softmax_scale, int32_t n_xcd, void* o, float* lse, void* workspace,
                              size_t workspace_bytes, void* stream);
 

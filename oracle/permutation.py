@@ -41,9 +41,11 @@ that two independent implementations agree exactly):
      equal angles (and the origin, angle 0) keep ascending row index.
   R7 degenerate heads (the centred mask has no direction at all, e.g. all rows
      equal): Stage 1 returns the identity order.
-  R8 waves: the Stage-1 order is first split into n_xcd contiguous segments (the
-     first m mod n_xcd get ceil(m/n_xcd) rows, the others floor(m/n_xcd)), one per
-     group of compute units that shares a private L2; each segment is cut into
+  R8 waves: the Stage-1 order is first split into n_xcd contiguous segments, one
+     per group of compute units that shares a private L2 (an XCD), balanced by
+     work: with w_i = n_i + 1 (one block-time of fixed cost per row) and W_p the
+     sum of w over the first p positions of the order, position p belongs to
+     segment min(n_xcd - 1, floor(n_xcd * W_p / W_m)). Each segment is cut into
      buckets of W rows from its start (the last bucket may be shorter); Stage 2
      sorts each bucket by descending n_i, stably (ties keep Stage-1 order).
      n_xcd = 1 is Alg. 2 as printed.
@@ -289,7 +291,8 @@ def stage1(mask: np.ndarray, seed: int, flat_head: int, iters: int = 10) -> Stag
 # R8: XCD segments, wave buckets and Stage 2
 # ---------------------------------------------------------------------------------------
 def segment_bounds(m: int, n_xcd: int):
-    """[start, end) of each of the n_xcd contiguous segments of m slots."""
+    """[start, end) of n_xcd contiguous segments of m slots with equal row counts
+    (the first m mod n_xcd get one more row): the slot layout of an unscheduled launch."""
     base, extra = divmod(m, n_xcd)
     bounds, s = [], 0
     for x in range(n_xcd):
@@ -299,11 +302,29 @@ def segment_bounds(m: int, n_xcd: int):
     return bounds
 
 
-def stage2(order: np.ndarray, row_nnz: np.ndarray, n_xcd: int, wave: int) -> np.ndarray:
+def work_segments(order: np.ndarray, row_nnz: np.ndarray, n_xcd: int):
+    """seg_start[0..n_xcd]: work-balanced contiguous segments of the order (reading R8)."""
+    m = order.size
+    w = [int(row_nnz[int(r)]) + 1 for r in order]
+    total = sum(w)
+    seg_of = []
+    prefix = 0
+    for p in range(m):
+        seg_of.append(min(n_xcd - 1, (n_xcd * prefix) // total))
+        prefix += w[p]
+    starts = []
+    for x in range(n_xcd):
+        starts.append(next((p for p in range(m) if seg_of[p] >= x), m))
+    return starts + [m]
+
+
+def stage2(order: np.ndarray, row_nnz: np.ndarray, n_xcd: int, wave: int, seg_start=None) -> np.ndarray:
     """Descending-n_i stable sort inside every wave bucket of every segment (Alg. 2)."""
     m = order.size
     perm = np.empty(m, dtype=np.int32)
-    for s0, s1 in segment_bounds(m, n_xcd):
+    if seg_start is None:
+        seg_start = work_segments(order, row_nnz, n_xcd)
+    for s0, s1 in zip(seg_start[:-1], seg_start[1:]):
         for b0 in range(s0, s1, wave):
             b1 = min(b0 + wave, s1)
             bucket = [int(r) for r in order[b0:b1]]
@@ -318,6 +339,14 @@ def two_stage_permutation(mask: np.ndarray, *, seed: int, flat_head: int, wave: 
     s1 = stage1(mask, seed, flat_head, iters)
     nnz = (np.asarray(mask) != 0).sum(axis=1)
     return stage2(s1.order, nnz, n_xcd, wave), s1
+
+
+def two_stage_schedule(mask: np.ndarray, *, seed: int, flat_head: int, wave: int, n_xcd: int = 8, iters: int = 10):
+    """(perm, seg_start, Stage-1 result): the permutation and its work-balanced XCD segments."""
+    s1 = stage1(mask, seed, flat_head, iters)
+    nnz = (np.asarray(mask) != 0).sum(axis=1)
+    seg = work_segments(s1.order, nnz, n_xcd)
+    return stage2(s1.order, nnz, n_xcd, wave, seg), seg, s1
 
 
 def identity_permutation(m: int) -> np.ndarray:

@@ -17,17 +17,18 @@ from . import skip as S
 def build_permutation(mask: np.ndarray, *, block: int, head_dim: int, wave: int, n_xcd: int = 8,
                       iters: int = 10, seed: int = 0, skip_mode: int = S.SKIP_AUTO,
                       profile: Optional[S.SkipProfile] = None):
-    """mask u8 [B][H][M_B][N_B] -> (perm int32 [B][H][M_B], flags uint8 [B][H], stage1 info list).
+    """mask u8 [B][H][M_B][N_B] -> (perm int32 [B][H][M_B], flags uint8 [B][H], stage1 info).
 
     ``flags`` holds the skip-rule bits that fired (S.FLAG_*) and S.FLAG_IDENTITY when the
     identity order was returned. With skip_mode NEVER the rule is still evaluated and
     reported but never applied; with ALWAYS every head returns the identity.
+    ``info["seg"][(b, h)]`` is the work-balanced XCD segment table of the returned order.
     """
     profile = profile or S.SkipProfile()
     b_, h_, m, n = mask.shape
     perm = np.empty((b_, h_, m), dtype=np.int32)
     flags = np.zeros((b_, h_), dtype=np.uint8)
-    info = {}
+    info = {"seg": {}}
     for b in range(b_):
         for h in range(h_):
             hh = b * h_ + h
@@ -36,6 +37,7 @@ def build_permutation(mask: np.ndarray, *, block: int, head_dim: int, wave: int,
             if skip_mode == S.SKIP_ALWAYS or (skip_mode == S.SKIP_AUTO and f != 0):
                 perm[b, h] = P.identity_permutation(m)
                 flags[b, h] = f | S.FLAG_IDENTITY
+                info["seg"][(b, h)] = P.work_segments(perm[b, h], st.row_nnz, n_xcd)
                 continue
             s1 = P.stage1(mask[b, h], seed, hh, iters)
             f |= S.tier2_flags(st, profile, s1.trace, s1.scale_exp, s1.degenerate)
@@ -43,7 +45,10 @@ def build_permutation(mask: np.ndarray, *, block: int, head_dim: int, wave: int,
             if skip_mode == S.SKIP_AUTO and (f & S.FLAG_UNSTRUCTURED):
                 perm[b, h] = P.identity_permutation(m)
                 flags[b, h] = f | S.FLAG_IDENTITY
+                info["seg"][(b, h)] = P.work_segments(perm[b, h], st.row_nnz, n_xcd)
                 continue
-            perm[b, h] = P.stage2(s1.order, st.row_nnz, n_xcd, wave)
+            seg = P.work_segments(s1.order, st.row_nnz, n_xcd)
+            perm[b, h] = P.stage2(s1.order, st.row_nnz, n_xcd, wave, seg)
+            info["seg"][(b, h)] = seg
             flags[b, h] = f
     return perm, flags, info

@@ -96,8 +96,9 @@ def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim:
                       n_xcd: int = 8, iters: int = 10, seed: int = 0, skip: str = "auto",
                       profile: Optional[L.WaSkipProfile] = None, workspace: Optional[torch.Tensor] = None,
                       return_info: bool = False, out: Optional[torch.Tensor] = None,
-                      flags_out: Optional[torch.Tensor] = None):
-    """perm int32 [B][H][M_B] and head flags uint8 [B][H] (plus embedding and Stage-1 order if asked)."""
+                      flags_out: Optional[torch.Tensor] = None, seg_out: Optional[torch.Tensor] = None):
+    """(perm int32 [B][H][M_B], seg_start int32 [B][H][n_xcd+1], head flags uint8 [B][H])
+    (plus embedding and Stage-1 order if asked)."""
     lib = L.load()
     mask = _mask_u8(mask)
     b, h, mb, nb = mask.shape
@@ -105,6 +106,7 @@ def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim:
     dev = mask.device
     perm = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if out is None else out
     flags = torch.empty((b, h), dtype=torch.uint8, device=dev) if flags_out is None else flags_out
+    seg = torch.empty((b, h, n_xcd + 1), dtype=torch.int32, device=dev) if seg_out is None else seg_out
     emb = torch.empty((b, h, mb, 2), dtype=torch.int32, device=dev) if return_info else None
     s1 = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if return_info else None
     params = L.WaPermParams(0 if wave is None else int(wave), int(n_xcd), int(iters), _SKIP[skip],
@@ -113,12 +115,12 @@ def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim:
     need = perm_workspace_size(shape)
     if workspace is None or workspace.numel() < need:
         workspace = _workspace(need, dev)
-    L.check(lib.wa_build_permutation(_ptr(mask), ctypes.byref(shape), ctypes.byref(params), _ptr(perm),
+    L.check(lib.wa_build_permutation(_ptr(mask), ctypes.byref(shape), ctypes.byref(params), _ptr(perm), _ptr(seg),
                                      _ptr(flags), _ptr(emb), _ptr(s1), _ptr(workspace), workspace.numel(),
                                      _stream()))
     if return_info:
-        return perm, flags, emb, s1
-    return perm, flags
+        return perm, seg, flags, emb, s1
+    return perm, seg, flags
 
 
 def compact_mask(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 128,
@@ -150,7 +152,8 @@ def _attn_args(q, k, v, block):
 
 
 def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: torch.Tensor,
-                perm: Optional[torch.Tensor] = None, *, block: int, scale: Optional[float] = None,
+                perm: Optional[torch.Tensor] = None, seg: Optional[torch.Tensor] = None, *, block: int,
+                scale: Optional[float] = None,
                 n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None):
     """O = block-sparse softmax attention of q over the kept KV blocks, in the original row order."""
@@ -166,13 +169,13 @@ def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: torch.T
     need = attn_workspace_size(shape)
     if workspace is None or workspace.numel() < need:
         workspace = _workspace(need, q.device)
-    L.check(lib.wa_sparse_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(mask), _ptr(perm), ctypes.byref(shape),
+    L.check(lib.wa_sparse_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(mask), _ptr(perm), _ptr(seg), ctypes.byref(shape),
                                float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse), _ptr(workspace),
                                workspace.numel(), _stream()))
     return (o, lse) if return_lse else o
 
 
-def sparse_attn_csr(q, k, v, row_ptr, col_idx, perm=None, *, block: int, scale: Optional[float] = None,
+def sparse_attn_csr(q, k, v, row_ptr, col_idx, perm=None, seg=None, *, block: int, scale: Optional[float] = None,
                     n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None,
                     workspace: Optional[torch.Tensor] = None):
     lib = L.load()
@@ -182,7 +185,7 @@ def sparse_attn_csr(q, k, v, row_ptr, col_idx, perm=None, *, block: int, scale: 
     need = attn_workspace_size(shape)
     if workspace is None or workspace.numel() < need:
         workspace = _workspace(need, q.device)
-    L.check(lib.wa_sparse_attn_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr), _ptr(col_idx), _ptr(perm),
+    L.check(lib.wa_sparse_attn_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr), _ptr(col_idx), _ptr(perm), _ptr(seg),
                                    ctypes.byref(shape), float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse),
                                    _ptr(workspace), workspace.numel(), _stream()))
     return (o, lse) if return_lse else o

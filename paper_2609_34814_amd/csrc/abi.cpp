@@ -133,11 +133,11 @@ wa_status launch_compact(const uint8_t* mask, const Dims& d, int32_t* row_ptr, i
 }
 
 wa_status launch_attn(const void* q, const void* k, const void* v, void* vt, const int32_t* row_ptr,
-                      const int32_t* col_idx, const int32_t* perm, const Dims& d, float scale, int32_t n_xcd, void* o,
-                      float* lse, hipStream_t st) {
+                      const int32_t* col_idx, const int32_t* perm, const int32_t* seg, const Dims& d, float scale,
+                      int32_t n_xcd, void* o, float* lse, hipStream_t st) {
   WaAttnLaunch a{};
   a.q = q; a.k = k; a.v = v; a.vt = vt;
-  a.row_ptr = row_ptr; a.col_idx = col_idx; a.perm = perm;
+  a.row_ptr = row_ptr; a.col_idx = col_idx; a.perm = perm; a.seg = seg;
   a.o = o; a.lse = lse;
   a.bh = (int32_t)d.bh; a.seq_len = d.n; a.mb = d.mb; a.head_dim = d.d; a.block = d.blk; a.n_xcd = n_xcd;
   a.scale = (scale > 0.f && std::isfinite(scale)) ? scale : (float)(1.0 / std::sqrt((double)d.d));
@@ -241,8 +241,8 @@ wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row
 }
 
 wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const wa_perm_params* params,
-                               int32_t* perm, uint8_t* head_flags, int32_t* embedding, int32_t* stage1_order,
-                               void* workspace, size_t workspace_bytes, void* stream) {
+                               int32_t* perm, int32_t* seg_start, uint8_t* head_flags, int32_t* embedding,
+                               int32_t* stage1_order, void* workspace, size_t workspace_bytes, void* stream) {
   Dims d;
   wa_status s = check_shape(shape, &d);
   if (s != WA_OK) return s;
@@ -275,7 +275,7 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
   a.head_stats = nullptr;
   a.zbuf = (int64_t*)(base + L.zbuf);
   a.ybuf = (int64_t*)(base + L.ybuf);
-  a.perm = perm; a.flags = head_flags; a.embedding = embedding; a.stage1 = stage1_order;
+  a.perm = perm; a.flags = head_flags; a.embedding = embedding; a.stage1 = stage1_order; a.seg_start = seg_start;
   a.bh = (int32_t)d.bh; a.m = d.mb; a.n = d.mb;
   a.wave = wave; a.n_xcd = params->n_xcd; a.iters = params->iters; a.skip_mode = params->skip_mode;
   a.stats_only = 0; a.block = d.blk; a.head_dim = d.d; a.seed = params->seed;
@@ -306,8 +306,8 @@ wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes) {
 }
 
 wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint8_t* mask, const int32_t* perm,
-                         const wa_shape* shape, float softmax_scale, int32_t n_xcd, void* o, float* lse,
-                         void* workspace, size_t workspace_bytes, void* stream) {
+                         const int32_t* seg_start, const wa_shape* shape, float softmax_scale, int32_t n_xcd,
+                         void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   Dims d;
   wa_status s = check_shape(shape, &d);
   if (s != WA_OK) return s;
@@ -323,13 +323,14 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
   int32_t* col_idx = (int32_t*)(base + attn_vt_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4));
   s = launch_compact(mask, d, row_ptr, col_idx, st);
   if (s != WA_OK) return s;
-  s = launch_attn(q, k, v, base, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse, st);
+  s = launch_attn(q, k, v, base, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, o, lse, st);
   if (s != WA_OK) return s;
   return ok();
 }
 
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
-                             const int32_t* col_idx, const int32_t* perm, const wa_shape* shape,
+                             const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
+                             const wa_shape* shape,
                              float softmax_scale, int32_t n_xcd, void* o, float* lse, void* workspace,
                              size_t workspace_bytes, void* stream) {
   Dims d;
@@ -341,7 +342,7 @@ wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const 
   if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
   s = check_ws(workspace, workspace_bytes, attn_vt_bytes(d));
   if (s != WA_OK) return s;
-  s = launch_attn(q, k, v, workspace, row_ptr, col_idx, perm, d, softmax_scale, n_xcd, o, lse,
+  s = launch_attn(q, k, v, workspace, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, o, lse,
                   (hipStream_t)stream);
   if (s != WA_OK) return s;
   return ok();

@@ -31,8 +31,9 @@
 //     rows (the inverse permutation is fused into the store).
 // Keys past the end of the sequence (ragged last block) get score -inf.
 //
-// Workgroup -> query block: workgroup g of head bh runs slot xcd_slot(g) and slot
-// s computes original block perm[s] (identity when perm is null).
+// Workgroup -> query blocks: workgroup g of head bh runs the slots xcd_slots(g)
+// (its share of its XCD's segment) and slot s computes original block perm[s]
+// (identity when perm is null).
 
 #include "common.h"
 
@@ -171,10 +172,12 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
 
   const int wgh = wa::wg_per_head(a.mb, a.n_xcd);
   const int bh = blockIdx.x / wgh;
-  const int slot = wa::xcd_slot(blockIdx.x % wgh, a.mb, a.n_xcd);
-  if (slot < 0) return;
+  int slot_first, slot_last;
+  wa::xcd_slots(blockIdx.x % wgh, a.mb, a.n_xcd, a.seg ? a.seg + (int64_t)bh * (a.n_xcd + 1) : nullptr,
+                &slot_first, &slot_last);
+  for (int slot = slot_first; slot < slot_last; ++slot) {
   const int row = a.perm ? a.perm[(int64_t)bh * a.mb + slot] : slot;
-  if ((unsigned)row >= (unsigned)a.mb) return;  // not a valid block index: nothing to compute
+  if ((unsigned)row >= (unsigned)a.mb) continue;  // not a valid block index: nothing to compute
 
   const int n = a.seq_len;
   const int64_t npad = (int64_t)a.mb * BLK;
@@ -338,6 +341,7 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     if (a.lse && hf == 0)
       a.lse[(int64_t)bh * n + qi] = ltot > 0.f ? (m_run + __log2f(ltot)) * kLn2 : -INFINITY;
   }
+  }  // slots
 }
 
 // V [bh][n][D] -> V^T [bh][D][mb*BLK], zero beyond n. One 64x64 tile per workgroup.

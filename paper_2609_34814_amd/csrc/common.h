@@ -9,23 +9,30 @@ namespace wa {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// Slot of workgroup `g` of one head under the XCD-aware mapping: workgroups are
-// dispatched round-robin over the XCDs (g mod n_xcd), and XCD x runs the
-// contiguous slot segment [seg_start(x), seg_start(x) + seg_len(x)) in order.
-// Returns -1 for a workgroup with no slot (the last partial round).
-__host__ __device__ inline int xcd_slot(int g, int m, int n_xcd) {
-  if (n_xcd <= 1) return g < m ? g : -1;
-  int x = g % n_xcd;
-  int l = g / n_xcd;
-  int base = m / n_xcd, extra = m % n_xcd;
-  int len = base + (x < extra ? 1 : 0);
-  if (l >= len) return -1;
-  return x * base + (x < extra ? x : extra) + l;
-}
+// Workgroups of one head: ceil(m / n_xcd) per XCD.
+__host__ __device__ inline int wg_per_xcd(int m, int n_xcd) { return (m + n_xcd - 1) / n_xcd; }
+__host__ __device__ inline int wg_per_head(int m, int n_xcd) { return n_xcd * wg_per_xcd(m, n_xcd); }
 
-__host__ __device__ inline int wg_per_head(int m, int n_xcd) {
-  if (n_xcd <= 1) return m;
-  return n_xcd * ((m + n_xcd - 1) / n_xcd);
+// Slots [first, last) run by workgroup g of one head. Workgroups are dispatched round-robin
+// over the XCDs (g mod n_xcd); the L = ceil(m / n_xcd) workgroups of XCD x run segment
+// [s0, s1) of the slots in order, each taking c = ceil((s1 - s0) / L) consecutive slots.
+// seg (n_xcd + 1 entries) gives the segments; without it the segments have equal row counts.
+__host__ __device__ inline void xcd_slots(int g, int m, int n_xcd, const int32_t* seg, int* first, int* last) {
+  const int x = g % n_xcd;
+  const int l = g / n_xcd;
+  const int L = wg_per_xcd(m, n_xcd);
+  int s0, s1;
+  if (seg) {
+    s0 = min(max(seg[x], 0), m);
+    s1 = min(max(seg[x + 1], s0), m);
+  } else {
+    const int base = m / n_xcd, extra = m % n_xcd;
+    s0 = x * base + (x < extra ? x : extra);
+    s1 = s0 + base + (x < extra ? 1 : 0);
+  }
+  const int c = (s1 - s0 + L - 1) / L;
+  *first = min(s0 + l * c, s1);
+  *last = min(*first + c, s1);
 }
 
 }  // namespace wa
@@ -39,6 +46,7 @@ struct WaAttnLaunch {
   const int32_t* row_ptr;
   const int32_t* col_idx;
   const int32_t* perm;
+  const int32_t* seg;  // [bh][n_xcd+1] XCD segment starts, nullable
   void* o;
   float* lse;
   int32_t bh;        // batch * heads

@@ -14,9 +14,12 @@
 //   4  Stage 1: bitonic sort of the rows by polar angle (Eq. 4) with an exact
 //      integer comparator (half-plane class, then the sign of the cross product,
 //      then the row index);
-//   5  Stage 2: the order is cut into n_xcd contiguous segments and each into
-//      buckets of W rows; one bitonic sort over (bucket, -n_i, position) keys
-//      sorts every bucket by descending n_i, stably.
+//   5  Stage 2: the order is cut into n_xcd contiguous segments of equal work
+//      (w_i = n_i + 1, a prefix sum over the order decides each row's segment)
+//      and each segment into buckets of W rows; one bitonic sort over
+//      (bucket, -n_i, position) keys sorts every bucket by descending n_i,
+//      stably. The segment table is an output: the attention kernel runs
+//      segment x on XCD x.
 // Every sum is an exact integer, so the order of parallel reductions does not
 // matter and the result is reproducible bit for bit. Supports m, n <= 4096.
 
@@ -40,6 +43,8 @@ struct Shared {
   int32_t xs[2 * MAXB];      // X (2^30 fixed point), later U
   int32_t ys[2 * MAXB];      // Ys; later sort scratch (indices, then 64-bit keys)
   int64_t red[NWAVE * 4];
+  int32_t part[NT];          // scan partials
+  int32_t seg[65];           // XCD segment starts of the current order
   double dbl[8];
   int64_t i64[8];
   int32_t i32[8];
@@ -266,6 +271,43 @@ __device__ __forceinline__ bool angle_less(const Shared& sh, int a, int b) {
   return a < b;
 }
 
+// Work-balanced XCD segments of the order held in sh.cc[0..m): position p belongs to segment
+// min(n_xcd - 1, n_xcd * W_p / W_m) with W_p the sum of (n_i + 1) over the first p positions.
+// Fills sh.seg[0..n_xcd] (and seg_out, if given). Uses sh.xs as scratch.
+__device__ void compute_segments(Shared& sh, const int32_t* row_nnz, int m, int n_xcd, int32_t* seg_out) {
+  const int tid = threadIdx.x;
+  const int per = (m + NT - 1) / NT;
+  const int lo = min(tid * per, m), hi = min(lo + per, m);
+  int32_t local = 0;
+  for (int p = lo; p < hi; ++p) local += row_nnz[sh.cc[p]] + 1;
+  sh.part[tid] = local;
+  __syncthreads();
+  for (int off = 1; off < NT; off <<= 1) {
+    const int32_t v = tid >= off ? sh.part[tid - off] : 0;
+    __syncthreads();
+    sh.part[tid] += v;
+    __syncthreads();
+  }
+  const int64_t total = sh.part[NT - 1];
+  int32_t run = tid > 0 ? sh.part[tid - 1] : 0;   // W_lo
+  int32_t* segof = sh.xs;
+  for (int p = lo; p < hi; ++p) {
+    const int64_t x = ((int64_t)n_xcd * run) / total;
+    segof[p] = (int32_t)(x < n_xcd - 1 ? x : n_xcd - 1);
+    run += row_nnz[sh.cc[p]] + 1;
+  }
+  __syncthreads();
+  for (int p = tid; p < m; p += NT) {
+    const int prev = p > 0 ? segof[p - 1] : -1;
+    for (int x = prev + 1; x <= segof[p]; ++x) sh.seg[x] = p;
+  }
+  if (tid == 0)
+    for (int x = segof[m - 1] + 1; x <= n_xcd; ++x) sh.seg[x] = m;
+  __syncthreads();
+  if (seg_out)
+    for (int x = tid; x <= n_xcd; x += NT) seg_out[x] = sh.seg[x];
+}
+
 __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
   Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
@@ -330,15 +372,19 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
   __syncthreads();
   int flags = sh.i32[1];
   int32_t* perm = a.perm + (int64_t)h * m;
+  int32_t* seg_out = a.seg_start ? a.seg_start + (int64_t)h * (a.n_xcd + 1) : nullptr;
   if (a.skip_mode == SKIP_ALWAYS || (a.skip_mode == SKIP_AUTO && flags != 0)) {
     for (int i = tid; i < m; i += NT) {
       perm[i] = i;
+      sh.cc[i] = i;
       if (a.stage1) a.stage1[(int64_t)h * m + i] = i;
       if (a.embedding) {
         a.embedding[((int64_t)h * m + i) * 2] = 0;
         a.embedding[((int64_t)h * m + i) * 2 + 1] = 0;
       }
     }
+    __syncthreads();
+    compute_segments(sh, H.row_nnz, m, a.n_xcd, seg_out);
     if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
     return;
   }
@@ -443,10 +489,14 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
       a.embedding[((int64_t)h * m + i) * 2 + 1] = degen ? 0 : sh.xs[2 * i + 1];
     }
   if (a.skip_mode == SKIP_AUTO && (flags & FLAG_UNSTRUCTURED)) {
+    __syncthreads();  // every thread has written its embedding rows (read from sh.xs)
     for (int i = tid; i < m; i += NT) {
       perm[i] = i;
+      sh.cc[i] = i;
       if (a.stage1) a.stage1[(int64_t)h * m + i] = i;
     }
+    __syncthreads();
+    compute_segments(sh, H.row_nnz, m, a.n_xcd, seg_out);
     if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
     return;
   }
@@ -479,23 +529,17 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
   if (a.stage1)
     for (int i = tid; i < m; i += NT) a.stage1[(int64_t)h * m + i] = sh.cc[i];
 
-  // ---- phase 5: segments, wave buckets, Stage 2 ----
+  // ---- phase 5: work-balanced segments, wave buckets, Stage 2 ----
+  compute_segments(sh, H.row_nnz, m, a.n_xcd, seg_out);
+  int32_t* segof = sh.xs;  // segment of each position, left by compute_segments
   uint64_t* keys = reinterpret_cast<uint64_t*>(sh.ys);
-  const int base = m / a.n_xcd, extra = m % a.n_xcd;
   for (int p = tid; p < P; p += NT) {
     if (p >= m) {
       keys[p] = ~0ull;
       continue;
     }
-    int x, off;
-    const int big = extra * (base + 1);
-    if (p < big) {
-      x = p / (base + 1);
-      off = p - x * (base + 1);
-    } else {
-      x = extra + (p - big) / base;
-      off = p - big - (x - extra) * base;
-    }
+    const int x = segof[p];
+    const int off = p - sh.seg[x];
     const uint64_t bucket = ((uint64_t)x << 12) | (uint64_t)(off / a.wave);
     const int row = sh.cc[p];
     const uint64_t nz = (uint64_t)H.row_nnz[row];

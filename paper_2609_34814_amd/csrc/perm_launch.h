@@ -18,6 +18,7 @@ struct WaPermLaunch {
   uint8_t* flags;           // [bh], nullable
   int32_t* embedding;       // [bh][m][2], nullable
   int32_t* stage1;          // [bh][m], nullable
+  int32_t* seg_start;       // [bh][n_xcd+1], nullable
   int32_t bh, m, n;
   int32_t wave, n_xcd, iters, skip_mode, stats_only;
   int32_t block, head_dim;

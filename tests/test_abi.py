@@ -93,8 +93,8 @@ def test_sparse_attn_validation():
     def call(**kw):
         a = dict(args)
         a.update(kw)
-        return lib.wa_sparse_attn(a["q"], a["k"], a["v"], a["mask"], a["perm"], ctypes.byref(s), 0.0, a["n_xcd"],
-                                  a["o"], None, a["ws"], a["ws_bytes"], None)
+        return lib.wa_sparse_attn(a["q"], a["k"], a["v"], a["mask"], a["perm"], None, ctypes.byref(s), 0.0,
+                                  a["n_xcd"], a["o"], None, a["ws"], a["ws_bytes"], None)
 
     assert call(q=None) == L.WA_ERR_INVALID_ARG
     assert call(o=None) == L.WA_ERR_INVALID_ARG
@@ -106,9 +106,9 @@ def test_sparse_attn_validation():
     assert call(ws=ctypes.c_void_p((1 << 24) + 64)) == L.WA_ERR_ALIGNMENT
     assert call(ws_bytes=ws_n.value - 1) == L.WA_ERR_WORKSPACE
     assert b"workspace" in lib.wa_last_error()
-    assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, None, FAKE, None, ctypes.byref(s), 0.0, 8, FAKE, None,
+    assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, None, FAKE, None, None, ctypes.byref(s), 0.0, 8, FAKE, None,
                                   ctypes.c_void_p(1 << 24), ws_n.value, None) == L.WA_ERR_INVALID_ARG
-    assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, FAKE, FAKE, None, ctypes.byref(s), 0.0, 8, FAKE, None,
+    assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, ctypes.byref(s), 0.0, 8, FAKE, None,
                                   ctypes.c_void_p(1 << 24), 1024, None) == L.WA_ERR_WORKSPACE
 
 
@@ -121,7 +121,7 @@ def test_build_permutation_validation():
 
     def call(params, mask=FAKE, perm=FAKE, wsb=ws_n.value, wsp=ws):
         return lib.wa_build_permutation(mask, ctypes.byref(s), ctypes.byref(params) if params else None, perm,
-                                        None, None, None, wsp, wsb, None)
+                                        None, None, None, None, wsp, wsb, None)
 
     good = dict(wave_per_xcd=64, n_xcd=8, iters=10, skip_mode=0, seed=0, profile=None)
 

@@ -125,7 +125,7 @@ def test_mask_stats_bit_exact(name):
 # ------------------------------------------------------------------------------------------------
 def _perm_case(wl, mask, *, wave, n_xcd, mode, iters=10, seed=0, profile=None):
     prof = profile or S.SkipProfile()
-    perm, flags, emb, s1 = _w().build_permutation(
+    perm, seg, flags, emb, s1 = _w().build_permutation(
         u8_dev(mask), seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim, wave=wave, n_xcd=n_xcd,
         iters=iters, seed=seed, skip={0: "auto", 1: "never", 2: "always"}[mode], profile=_profile_np_to_c(prof),
         return_info=True)
@@ -134,9 +134,11 @@ def _perm_case(wl, mask, *, wave, n_xcd, mode, iters=10, seed=0, profile=None):
                                                     n_xcd=n_xcd, iters=iters, seed=seed, skip_mode=mode,
                                                     profile=prof)
     perm, flags, emb, s1 = perm.cpu().numpy(), flags.cpu().numpy(), emb.cpu().numpy(), s1.cpu().numpy()
+    seg = seg.cpu().numpy()
     for b in range(wl.batch):
         for h in range(wl.heads):
             assert np.array_equal(np.sort(perm[b, h]), np.arange(wl.mb)), (b, h)
+            assert list(seg[b, h]) == list(info["seg"][(b, h)]), ("seg", b, h, seg[b, h], info["seg"][(b, h)])
             if (b, h) in info:
                 assert np.array_equal(emb[b, h], info[(b, h)].embedding.astype(np.int32)), ("embedding", b, h)
                 if not (ref_flags[b, h] & S.FLAG_IDENTITY):
@@ -177,8 +179,8 @@ def _check(stats):
         assert stats[k] <= v, (k, stats)
 
 
-def _run_attn(wl, mask, q, k, v, perm=None, n_xcd=8):
-    o, lse = _w().sparse_attn(q, k, v, u8_dev(mask), perm, block=wl.block, n_xcd=n_xcd, return_lse=True)
+def _run_attn(wl, mask, q, k, v, perm=None, n_xcd=8, seg=None):
+    o, lse = _w().sparse_attn(q, k, v, u8_dev(mask), perm, seg, block=wl.block, n_xcd=n_xcd, return_lse=True)
     torch.cuda.synchronize()
     return o, lse
 
@@ -226,9 +228,9 @@ def test_attention_sampled_vs_oracle(name, count):
     q, k, v = make_qkv(wl)
     mask = make_mask(wl)
     qd, kd, vd = bf16_dev(q), bf16_dev(k), bf16_dev(v)
-    perm, _ = _w().build_permutation(u8_dev(mask), seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
-                                     skip="never")
-    o, lse = _run_attn(wl, mask, qd, kd, vd, perm=perm)
+    perm, seg, _ = _w().build_permutation(u8_dev(mask), seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
+                                          skip="never")
+    o, lse = _run_attn(wl, mask, qd, kd, vd, perm=perm, seg=seg)
     picks = sample_blocks(mask, count, seed=1)
     ref = A.block_sparse_attention_rows(q, k, v, mask, wl.block, picks)
     st = compare_blocks(dev_f64(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
@@ -243,12 +245,19 @@ def test_output_bit_identical_across_permutations(name):
     mask = make_mask(wl)
     md = u8_dev(mask)
     o_nat, l_nat = _run_attn(wl, mask, q, k, v, perm=None, n_xcd=8)
-    perm, _ = _w().build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim, skip="never")
+    perm, seg, _ = _w().build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
+                                          skip="never")
     rng = np.random.default_rng(3)
     rnd = np.stack([np.stack([rng.permutation(wl.mb) for _ in range(wl.heads)]) for _ in range(wl.batch)])
     rnd = torch.from_numpy(rnd.astype(np.int32)).cuda()
-    for p, nx in ((perm, 8), (perm, 1), (rnd, 8), (None, 1)):
-        o2, l2 = _run_attn(wl, mask, q, k, v, perm=p, n_xcd=nx)
+    # a lopsided segment table: segment 0 takes almost every slot (workgroups then run several slots)
+    lop = np.zeros((wl.batch, wl.heads, 9), dtype=np.int32)
+    lop[:, :, 1:] = wl.mb
+    lop[:, :, 1] = wl.mb - 2
+    lop = torch.from_numpy(lop).cuda()
+    for p, nx, sg in ((perm, 8, seg), (perm, 8, None), (perm, 1, None), (rnd, 8, None), (None, 1, None),
+                      (rnd, 8, lop)):
+        o2, l2 = _run_attn(wl, mask, q, k, v, perm=p, n_xcd=nx, seg=sg)
         assert torch.equal(o2.view(torch.int16), o_nat.view(torch.int16))
         assert torch.equal(l2.view(torch.int32), l_nat.view(torch.int32))
 

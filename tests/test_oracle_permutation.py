@@ -245,22 +245,34 @@ def test_stage2_hand_example():
     nnz = np.array([int(v) for v in lines[1][1:]])
     for ln in lines[2:]:
         n_xcd, w = int(ln[1]), int(ln[2])
-        expect = [int(v) for v in ln[4:]]
+        bar = ln.index("|")
+        expect = [int(v) for v in ln[4:bar]]
+        expect_seg = [int(v) for v in ln[bar + 1:]]
         assert list(P.stage2(order, nnz, n_xcd, w)) == expect
+        assert P.work_segments(order, nnz, n_xcd) == expect_seg
 
 
-@pytest.mark.parametrize("m,n_xcd,w", [(64, 8, 64), (591, 8, 64), (2841, 8, 128), (17, 1, 4), (9, 2, 3)])
+@pytest.mark.parametrize("m,n_xcd,w", [(64, 8, 64), (591, 8, 64), (2841, 8, 128), (17, 1, 4), (9, 2, 3), (5, 8, 2)])
 def test_stage2_invariants(m, n_xcd, w):
     rng = np.random.default_rng(m)
     order = rng.permutation(m).astype(np.int32)
-    nnz = rng.integers(1, 50, size=m)
+    nnz = rng.lognormal(2.0, 1.0, size=m).astype(np.int64)
     perm = P.stage2(order, nnz, n_xcd, w)
     assert np.array_equal(np.sort(perm), np.arange(m))
+    seg = P.work_segments(order, nnz, n_xcd)
+    assert seg[0] == 0 and seg[-1] == m and all(a <= b for a, b in zip(seg, seg[1:]))
+    # work balance: every segment's work differs from the even share by less than its heaviest row
+    wts = nnz[order] + 1
+    share = wts.sum() / n_xcd
+    for x in range(n_xcd):
+        sw = wts[seg[x]:seg[x + 1]].sum()
+        assert sw < share + wts.max() and (seg[x] == seg[x + 1] or sw > share - 2 * wts.max())
+    # the equal-count layout used without a schedule
     bounds = P.segment_bounds(m, n_xcd)
     assert bounds[0][0] == 0 and bounds[-1][1] == m
     lens = [b - a for a, b in bounds]
     assert max(lens) - min(lens) <= 1 and lens == sorted(lens, reverse=True)
-    for s0, s1 in bounds:
+    for s0, s1 in zip(seg[:-1], seg[1:]):
         for b0 in range(s0, s1, w):
             b1 = min(b0 + w, s1)
             assert sorted(perm[b0:b1]) == sorted(order[b0:b1])
@@ -276,6 +288,15 @@ def test_wave_objective_improves_on_shuffled_clusters():
     perm, _ = P.two_stage_permutation(mask, seed=0, flat_head=0, wave=16, n_xcd=1)
     ident = np.arange(96)
     assert OBJ.wave_objective(mask, perm, 16) < 0.7 * OBJ.wave_objective(mask, ident, 16)
+
+
+def test_planted_row_count_segments_are_caught(monkeypatch):
+    def by_rows(order, nnz, n_xcd):
+        return [b[0] for b in P.segment_bounds(order.size, n_xcd)] + [order.size]
+
+    monkeypatch.setattr(P, "work_segments", by_rows)
+    with pytest.raises(AssertionError):
+        test_stage2_hand_example()
 
 
 def test_golden_permutation_unchanged():
@@ -312,9 +333,10 @@ def test_planted_swapped_cross_sign_is_caught(monkeypatch):
 
 
 def test_planted_unstable_stage2_is_caught(monkeypatch):
-    def unstable(order, nnz, n_xcd, wave):
+    def unstable(order, nnz, n_xcd, wave, seg_start=None):
         perm = np.empty(order.size, dtype=np.int32)
-        for s0, s1 in P.segment_bounds(order.size, n_xcd):
+        seg = P.work_segments(order, nnz, n_xcd)
+        for s0, s1 in zip(seg[:-1], seg[1:]):
             for b0 in range(s0, s1, wave):
                 b1 = min(b0 + wave, s1)
                 bucket = list(order[b0:b1])
