@@ -72,7 +72,7 @@ wa_status check_shape(const wa_shape* s, Dims* out) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 struct PermWs {
-  size_t rowbits, colbits, row_nnz, col_cnt, head_stats, zbuf, ybuf, total;
+  size_t rowbits, colbits, row_nnz, col_cnt, head_stats, total;
 };
 
 PermWs perm_ws_layout(const Dims& d) {
@@ -84,8 +84,6 @@ PermWs perm_ws_layout(const Dims& d) {
   w.row_nnz = off; off = align_up(off + (size_t)d.bh * d.mb * 4);
   w.col_cnt = off; off = align_up(off + (size_t)d.bh * d.mb * 4);
   w.head_stats = off; off = align_up(off + (size_t)d.bh * 6 * 8);
-  w.zbuf = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 8);
-  w.ybuf = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 8);
   w.total = off;
   return w;
 }
@@ -149,7 +147,7 @@ wa_status launch_attn(const void* q, const void* k, const void* v, void* vt, con
 wa_status perm_launch_common(const uint8_t* mask, const Dims& d, const PermWs& L, char* base, hipStream_t st,
                              int32_t* row_nnz_out) {
   int32_t* row_nnz = row_nnz_out ? row_nnz_out : (int32_t*)(base + L.row_nnz);
-  hipError_t e = wa_launch_pack_rows(mask, d.bh * d.mb, d.mb, (uint64_t*)(base + L.rowbits), row_nnz, st);
+  hipError_t e = wa_launch_pack_rows(mask, d.bh * d.mb, d.mb, d.mb, (uint64_t*)(base + L.rowbits), row_nnz, st);
   if (e != hipSuccess) return hip_fail(e, "pack_rows launch");
   e = wa_launch_transpose_bits((const uint64_t*)(base + L.rowbits), (int)d.bh, d.mb, d.mb,
                                (uint64_t*)(base + L.colbits), st);
@@ -229,8 +227,6 @@ wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row
   a.row_nnz = row_nnz;
   a.col_cnt = col_cnt;
   a.head_stats = head_stats;
-  a.zbuf = (int64_t*)(base + L.zbuf);
-  a.ybuf = (int64_t*)(base + L.ybuf);
   a.bh = (int32_t)d.bh; a.m = d.mb; a.n = d.mb;
   a.wave = 1; a.n_xcd = 1; a.iters = 0; a.skip_mode = WA_SKIP_NEVER; a.stats_only = 1;
   a.block = d.blk; a.head_dim = d.d;
@@ -273,8 +269,6 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
   a.row_nnz = (const int32_t*)(base + L.row_nnz);
   a.col_cnt = nullptr;
   a.head_stats = nullptr;
-  a.zbuf = (int64_t*)(base + L.zbuf);
-  a.ybuf = (int64_t*)(base + L.ybuf);
   a.perm = perm; a.flags = head_flags; a.embedding = embedding; a.stage1 = stage1_order; a.seg_start = seg_start;
   a.bh = (int32_t)d.bh; a.m = d.mb; a.n = d.mb;
   a.wave = wave; a.n_xcd = params->n_xcd; a.iters = params->iters; a.skip_mode = params->skip_mode;

@@ -78,25 +78,28 @@ __global__ __launch_bounds__(256) void row_write_kernel(const uint8_t* __restric
   }
 }
 
-// Bit-packed rows: rowbits[(h*mb + i)*nw + w] bit b = M[h][i][64w + b]; row_nnz[h*mb + i] = n_i.
-__global__ __launch_bounds__(256) void pack_rows_kernel(const uint8_t* __restrict__ mask, int64_t rows, int n, int nw,
-                                                        uint64_t* __restrict__ rowbits,
+// Bit-packed rows, word-major per head: rowbits[(h*nw + w)*m + i] bit b = M[h][i][64w + b];
+// row_nnz[h*m + i] = n_i.
+__global__ __launch_bounds__(256) void pack_rows_kernel(const uint8_t* __restrict__ mask, int64_t rows, int m, int n,
+                                                        int nw, uint64_t* __restrict__ rowbits,
                                                         int32_t* __restrict__ row_nnz) {
   const int64_t row = (int64_t)blockIdx.x * kWavesPerWG + (threadIdx.x >> 6);
   if (row >= rows) return;
   const int lane = threadIdx.x & 63;
+  const int64_t h = row / m;
+  const int i = (int)(row % m);
   const uint8_t* p = mask + row * n;
   int cnt = 0;
   for (int w = 0; w < nw; ++w) {
     const int j = w * 64 + lane;
     const uint64_t word = ballot64(j < n && p[j] != 0);
-    if (lane == 0) rowbits[row * nw + w] = word;
+    if (lane == 0) rowbits[(h * nw + w) * m + i] = word;
     cnt += __popcll(word);
   }
   if (lane == 0) row_nnz[row] = cnt;
 }
 
-// Bit-packed columns from bit-packed rows: colbits[(h*n + j)*mw + v] bit r = M[h][64v + r][j].
+// Bit-packed columns from bit-packed rows, word-major: colbits[(h*mw + v)*n + j] bit r = M[h][64v + r][j].
 // One wavefront per (head, 64-column group, 64-row group): lane r holds row 64v + r's word.
 __global__ __launch_bounds__(256) void transpose_bits_kernel(const uint64_t* __restrict__ rowbits, int bh, int m,
                                                              int n, int nw, int mw,
@@ -110,14 +113,14 @@ __global__ __launch_bounds__(256) void transpose_bits_kernel(const uint64_t* __r
   const int cw = rem / mw;   // column word
   const int v = rem % mw;    // row word
   const int r = v * 64 + lane;
-  const uint64_t mine = r < m ? rowbits[(h * m + r) * nw + cw] : 0ull;
+  const uint64_t mine = r < m ? rowbits[(h * nw + cw) * m + r] : 0ull;
   uint64_t out = 0;
   for (int c = 0; c < 64; ++c) {
     const uint64_t b = ballot64((mine >> c) & 1ull);
     if (lane == c) out = b;
   }
   const int j = cw * 64 + lane;
-  if (j < n) colbits[(h * n + j) * mw + v] = out;
+  if (j < n) colbits[(h * mw + v) * n + j] = out;
 }
 
 // Each workgroup records the XCD it runs on (hardware register XCC_ID, bits [3:0]).
@@ -158,12 +161,12 @@ hipError_t wa_launch_row_write(const uint8_t* mask, int bh, int mb, int n, const
   return hipGetLastError();
 }
 
-hipError_t wa_launch_pack_rows(const uint8_t* mask, int64_t rows, int n, uint64_t* rowbits, int32_t* row_nnz,
-                               hipStream_t stream) {
+hipError_t wa_launch_pack_rows(const uint8_t* mask, int64_t rows, int m, int n, uint64_t* rowbits,
+                               int32_t* row_nnz, hipStream_t stream) {
   if (rows <= 0) return hipSuccess;
   const int nw = (n + 63) / 64;
   const int64_t grid = (rows + kWavesPerWG - 1) / kWavesPerWG;
-  hipLaunchKernelGGL(pack_rows_kernel, dim3((unsigned)grid), dim3(256), 0, stream, mask, rows, n, nw, rowbits,
+  hipLaunchKernelGGL(pack_rows_kernel, dim3((unsigned)grid), dim3(256), 0, stream, mask, rows, m, n, nw, rowbits,
                      row_nnz);
   return hipGetLastError();
 }

@@ -38,10 +38,13 @@ constexpr int FLAG_FITS_L2 = 1, FLAG_LITTLE_WORK = 2, FLAG_LOCAL = 4, FLAG_UNSTR
               FLAG_IDENTITY = 64;
 constexpr int SKIP_AUTO = 0, SKIP_ALWAYS = 2;
 
+constexpr int PER = MAXB / NT;  // rows or columns per thread
+
 struct Shared {
   int32_t cc[MAXB];          // column counts; later the Stage-1 order
   int32_t xs[2 * MAXB];      // X (2^30 fixed point), later U
   int32_t ys[2 * MAXB];      // Ys; later sort scratch (indices, then 64-bit keys)
+  int64_t za[2 * MAXB];      // M Ys accumulators
   int64_t red[NWAVE * 4];
   int32_t part[NT];          // scan partials
   int32_t seg[65];           // XCD segment starts of the current order
@@ -108,33 +111,35 @@ __device__ uint64_t block_max(Shared& sh, uint64_t v) {
 }
 
 struct Head {
-  const uint64_t* rowbits;  // [m][nw]
-  const uint64_t* colbits;  // [n][mw]
+  const uint64_t* rowbits;  // [nw][m] word-major: word w of row i at w * m + i
+  const uint64_t* colbits;  // [mw][n] word-major: word v of column j at v * n + j
   const int32_t* row_nnz;   // [m]
-  int64_t* zbuf;            // [m][2]
-  int64_t* ybuf;            // [n][2]
   int m, n, nw, mw;
 };
 
-// Cholesky-QR of zbuf (m x 2) into sh.xs; returns true if degenerate (first column zero).
-__device__ bool orth(Shared& sh, const Head& H) {
+// Cholesky-QR of Z (thread-owned rows i = tid + k NT, zr[k]) into sh.xs; true if degenerate.
+__device__ bool orth(Shared& sh, const Head& H, const int64_t (&zr)[PER][2]) {
   const int tid = threadIdx.x;
   uint64_t mx = 0;
-  for (int i = tid; i < H.m; i += NT) {
-    const uint64_t a = uabs64(H.zbuf[2 * i]), b = uabs64(H.zbuf[2 * i + 1]);
-    mx = a > mx ? a : mx;
-    mx = b > mx ? b : mx;
-  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k)
+    if (tid + k * NT < H.m) {
+      const uint64_t a = uabs64(zr[k][0]), b = uabs64(zr[k][1]);
+      mx = a > mx ? a : mx;
+      mx = b > mx ? b : mx;
+    }
   mx = block_max(sh, mx);
   const int bl = bitlen_u64(mx);
   const int s = bl > 24 ? bl - 24 : 0;
   int64_t g[3] = {0, 0, 0};
-  for (int i = tid; i < H.m; i += NT) {
-    const int64_t z0 = H.zbuf[2 * i] >> s, z1 = H.zbuf[2 * i + 1] >> s;
-    g[0] += z0 * z0;
-    g[1] += z0 * z1;
-    g[2] += z1 * z1;
-  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k)
+    if (tid + k * NT < H.m) {
+      const int64_t z0 = zr[k][0] >> s, z1 = zr[k][1] >> s;
+      g[0] += z0 * z0;
+      g[1] += z0 * z1;
+      g[2] += z1 * z1;
+    }
   block_sum<3>(sh, g);
   if (g[0] == 0) return true;
   if (tid == 0) {
@@ -151,89 +156,107 @@ __device__ bool orth(Shared& sh, const Head& H) {
   __syncthreads();
   const double r11 = sh.dbl[0], r12 = sh.dbl[1], r22 = sh.dbl[2];
   const bool rank2 = sh.i32[0] != 0;
-  for (int i = tid; i < H.m; i += NT) {
-    const double q0 = (double)(H.zbuf[2 * i] >> s) / r11;
-    sh.xs[2 * i] = (int32_t)__builtin_rint(q0 * 1073741824.0);
-    if (rank2) {
-      const double q1 = ((double)(H.zbuf[2 * i + 1] >> s) - r12 * q0) / r22;
-      sh.xs[2 * i + 1] = (int32_t)__builtin_rint(q1 * 1073741824.0);
-    } else {
-      sh.xs[2 * i + 1] = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = tid + k * NT;
+    if (i < H.m) {
+      const double q0 = (double)(zr[k][0] >> s) / r11;
+      sh.xs[2 * i] = (int32_t)__builtin_rint(q0 * 1073741824.0);
+      if (rank2) {
+        const double q1 = ((double)(zr[k][1] >> s) - r12 * q0) / r22;
+        sh.xs[2 * i + 1] = (int32_t)__builtin_rint(q1 * 1073741824.0);
+      } else {
+        sh.xs[2 * i + 1] = 0;
+      }
     }
   }
   __syncthreads();
   return false;
 }
 
-// zbuf = m * M~ Ys with Ys = (m * M~^T X) >> sy, both exact; returns sy.
-__device__ int centred_apply(Shared& sh, const Head& H) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int64_t m = H.m;
-  // YA[j] = sum_i M[i][j] X[i]: one wavefront per column, lanes over 64-row words
-  for (int j = w; j < H.n; j += NWAVE) {
-    int64_t s0 = 0, s1 = 0;
-    const uint64_t* cb = H.colbits + (int64_t)j * H.mw;
-    for (int v = lane; v < H.mw; v += 64) {
-      uint64_t word = cb[v];
+// Calls f(k) for every set bit k of a word-major bitmask line (words[w * stride + line] for
+// w < nwords), reading the words eight at a time so that the loads are in flight together.
+template <typename F>
+__device__ __forceinline__ void for_bits(const uint64_t* words, int nwords, int64_t stride, int line, F&& f) {
+  constexpr int CH = 8;
+  for (int v0 = 0; v0 < nwords; v0 += CH) {
+    uint64_t wd[CH];
+#pragma unroll
+    for (int t = 0; t < CH; ++t) wd[t] = v0 + t < nwords ? words[(int64_t)(v0 + t) * stride + line] : 0ull;
+#pragma unroll
+    for (int t = 0; t < CH; ++t) {
+      uint64_t word = wd[t];
       while (word) {
-        const int b = __ffsll((long long)word) - 1;
+        f((v0 + t) * 64 + __ffsll((long long)word) - 1);
         word &= word - 1;
-        const int i = v * 64 + b;
-        s0 += sh.xs[2 * i];
-        s1 += sh.xs[2 * i + 1];
       }
     }
-    s0 = wave_sum(s0);
-    s1 = wave_sum(s1);
-    if (lane == 0) {
-      H.ybuf[2 * j] = s0;
-      H.ybuf[2 * j + 1] = s1;
-    }
+  }
+}
+
+// zr = m * M~ Ys for the thread's rows, with Ys = (m * M~^T X) >> sy, both exact; returns sy.
+// One lane per column: M^T X gathers X over the set bits of the column's 64-row words; M Ys
+// scatters Ys[j] into the rows of those bits with 64-bit LDS atomics (integer, so exact in any
+// order). Column counts are far more even than the heavy-tailed row counts, so both halves stay
+// balanced across the workgroup.
+__device__ int centred_apply(Shared& sh, const Head& H, int64_t (&zr)[PER][2]) {
+  const int tid = threadIdx.x;
+  const int64_t m = H.m;
+  int64_t ya[PER][2];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    ya[k][0] = 0;
+    ya[k][1] = 0;
+    const int j = tid + k * NT;
+    if (j < H.n)
+      for_bits(H.colbits, H.mw, H.n, j, [&](int i) {
+        const int2 x = *(const int2*)&sh.xs[2 * i];
+        ya[k][0] += x.x;
+        ya[k][1] += x.y;
+      });
   }
   int64_t sx[2] = {0, 0};
   for (int i = tid; i < H.m; i += NT) {
     sx[0] += sh.xs[2 * i];
     sx[1] += sh.xs[2 * i + 1];
   }
-  block_sum<2>(sh, sx);  // contains the barrier that publishes ybuf
+  block_sum<2>(sh, sx);
   uint64_t mx = 0;
-  for (int j = tid; j < H.n; j += NT) {
-    const int64_t c = sh.cc[j];
-    const int64_t y0 = m * H.ybuf[2 * j] - c * sx[0];
-    const int64_t y1 = m * H.ybuf[2 * j + 1] - c * sx[1];
-    H.ybuf[2 * j] = y0;
-    H.ybuf[2 * j + 1] = y1;
-    const uint64_t a = uabs64(y0), b = uabs64(y1);
-    mx = a > mx ? a : mx;
-    mx = b > mx ? b : mx;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int j = tid + k * NT;
+    if (j < H.n) {
+      const int64_t c = sh.cc[j];
+      ya[k][0] = m * ya[k][0] - c * sx[0];
+      ya[k][1] = m * ya[k][1] - c * sx[1];
+      const uint64_t a = uabs64(ya[k][0]), b = uabs64(ya[k][1]);
+      mx = a > mx ? a : mx;
+      mx = b > mx ? b : mx;
+    }
   }
   mx = block_max(sh, mx);
   const int bl = bitlen_u64(mx);
   const int sy = bl > 30 ? bl - 30 : 0;
-  for (int j = tid; j < H.n; j += NT) {
-    sh.ys[2 * j] = (int32_t)(H.ybuf[2 * j] >> sy);
-    sh.ys[2 * j + 1] = (int32_t)(H.ybuf[2 * j + 1] >> sy);
-  }
-  __syncthreads();
-  // ZA[i] = sum_j M[i][j] Ys[j]: one wavefront per row
-  for (int i = w; i < H.m; i += NWAVE) {
-    int64_t s0 = 0, s1 = 0;
-    const uint64_t* rb = H.rowbits + (int64_t)i * H.nw;
-    for (int v = lane; v < H.nw; v += 64) {
-      uint64_t word = rb[v];
-      while (word) {
-        const int b = __ffsll((long long)word) - 1;
-        word &= word - 1;
-        const int j = v * 64 + b;
-        s0 += sh.ys[2 * j];
-        s1 += sh.ys[2 * j + 1];
-      }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int j = tid + k * NT;
+    if (j < H.n) {
+      sh.ys[2 * j] = (int32_t)(ya[k][0] >> sy);
+      sh.ys[2 * j + 1] = (int32_t)(ya[k][1] >> sy);
     }
-    s0 = wave_sum(s0);
-    s1 = wave_sum(s1);
-    if (lane == 0) {
-      H.zbuf[2 * i] = s0;
-      H.zbuf[2 * i + 1] = s1;
+  }
+  for (int i = tid; i < 2 * H.m; i += NT) sh.za[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int j = tid + k * NT;
+    if (j < H.n) {
+      const int2 y = *(const int2*)&sh.ys[2 * j];
+      const unsigned long long y0 = (unsigned long long)(int64_t)y.x, y1 = (unsigned long long)(int64_t)y.y;
+      for_bits(H.colbits, H.mw, H.n, j, [&](int i) {
+        atomicAdd((unsigned long long*)&sh.za[2 * i], y0);
+        atomicAdd((unsigned long long*)&sh.za[2 * i + 1], y1);
+      });
     }
   }
   int64_t syy[2] = {0, 0};
@@ -241,12 +264,18 @@ __device__ int centred_apply(Shared& sh, const Head& H) {
     syy[0] += (int64_t)sh.cc[j] * sh.ys[2 * j];
     syy[1] += (int64_t)sh.cc[j] * sh.ys[2 * j + 1];
   }
-  block_sum<2>(sh, syy);
-  for (int i = tid; i < H.m; i += NT) {
-    H.zbuf[2 * i] = m * H.zbuf[2 * i] - syy[0];
-    H.zbuf[2 * i + 1] = m * H.zbuf[2 * i + 1] - syy[1];
+  block_sum<2>(sh, syy);  // its barriers also complete the scatter
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = tid + k * NT;
+    if (i < H.m) {
+      zr[k][0] = m * sh.za[2 * i] - syy[0];
+      zr[k][1] = m * sh.za[2 * i + 1] - syy[1];
+    } else {
+      zr[k][0] = 0;
+      zr[k][1] = 0;
+    }
   }
-  __syncthreads();
   return sy;
 }
 
@@ -322,15 +351,12 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
   H.rowbits = a.rowbits + (int64_t)h * m * H.nw;
   H.colbits = a.colbits + (int64_t)h * n * H.mw;
   H.row_nnz = a.row_nnz + (int64_t)h * m;
-  H.zbuf = a.zbuf + (int64_t)h * 2 * m;
-  H.ybuf = a.ybuf + (int64_t)h * 2 * n;
 
   // ---- phase 0: statistics ----
   int64_t st[4] = {0, 0, 0, 0};  // nnz, distinct, sum c^2, (unused)
   for (int j = tid; j < n; j += NT) {
     int c = 0;
-    const uint64_t* cb = H.colbits + (int64_t)j * H.mw;
-    for (int v = 0; v < H.mw; ++v) c += __popcll(cb[v]);
+    for (int v = 0; v < H.mw; ++v) c += __popcll(H.colbits[(int64_t)v * n + j]);
     sh.cc[j] = c;
     if (a.col_cnt) a.col_cnt[(int64_t)h * n + j] = c;
     st[1] += c > 0;
@@ -339,8 +365,8 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
   for (int i = tid; i < m; i += NT) st[0] += H.row_nnz[i];
   int64_t adj[2] = {0, 0};
   for (int t = tid; t < (m - 1) * H.nw; t += NT) {
-    const int i = t / H.nw, w = t % H.nw;
-    const uint64_t x = H.rowbits[(int64_t)i * H.nw + w], y = H.rowbits[(int64_t)(i + 1) * H.nw + w];
+    const int w = t / (m - 1), i = t % (m - 1);
+    const uint64_t x = H.rowbits[(int64_t)w * m + i], y = H.rowbits[(int64_t)w * m + i + 1];
     adj[0] += __popcll(x & y);
     adj[1] += __popcll(x | y);
   }
@@ -390,38 +416,46 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
   }
 
   // ---- phase 2: MFCSI ----
-  for (int i = tid; i < m; i += NT) {
+  int64_t zr[PER][2];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = tid + k * NT;
     const uint64_t base = a.seed + 2ull * ((uint64_t)h * (uint64_t)m + (uint64_t)i);
-    H.zbuf[2 * i] = (int64_t)(splitmix64(base) >> 40) - (1ll << 23);
-    H.zbuf[2 * i + 1] = (int64_t)(splitmix64(base + 1ull) >> 40) - (1ll << 23);
+    zr[k][0] = i < m ? (int64_t)(splitmix64(base) >> 40) - (1ll << 23) : 0;
+    zr[k][1] = i < m ? (int64_t)(splitmix64(base + 1ull) >> 40) - (1ll << 23) : 0;
   }
-  __syncthreads();
-  bool degen = orth(sh, H);
+  bool degen = orth(sh, H, zr);
   for (int it = 0; it < a.iters && !degen; ++it) {
-    centred_apply(sh, H);
-    degen = orth(sh, H);
+    centred_apply(sh, H, zr);
+    degen = orth(sh, H, zr);
   }
   int64_t trace = 0;
   int scale_exp = 0;
   if (!degen) {
-    const int sy = centred_apply(sh, H);
+    const int sy = centred_apply(sh, H, zr);
     uint64_t mx = 0;
-    for (int i = tid; i < m; i += NT) {
-      const uint64_t p = uabs64(H.zbuf[2 * i]), q = uabs64(H.zbuf[2 * i + 1]);
-      mx = p > mx ? p : mx;
-      mx = q > mx ? q : mx;
-    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k)
+      if (tid + k * NT < m) {
+        const uint64_t p = uabs64(zr[k][0]), q = uabs64(zr[k][1]);
+        mx = p > mx ? p : mx;
+        mx = q > mx ? q : mx;
+      }
     mx = block_max(sh, mx);
     const int bl = bitlen_u64(mx);
     const int s_r = bl > 24 ? bl - 24 : 0;
     int64_t b[4] = {0, 0, 0, 0};
-    for (int i = tid; i < m; i += NT) {
-      const int64_t x0 = sh.xs[2 * i] >> 6, x1 = sh.xs[2 * i + 1] >> 6;
-      const int64_t z0 = H.zbuf[2 * i] >> s_r, z1 = H.zbuf[2 * i + 1] >> s_r;
-      b[0] += x0 * z0;
-      b[1] += x0 * z1;
-      b[2] += x1 * z0;
-      b[3] += x1 * z1;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = tid + k * NT;
+      if (i < m) {
+        const int64_t x0 = sh.xs[2 * i] >> 6, x1 = sh.xs[2 * i + 1] >> 6;
+        const int64_t z0 = zr[k][0] >> s_r, z1 = zr[k][1] >> s_r;
+        b[0] += x0 * z0;
+        b[1] += x0 * z1;
+        b[2] += x1 * z0;
+        b[3] += x1 * z1;
+      }
     }
     block_sum<4>(sh, b);
     trace = b[0] + b[3];

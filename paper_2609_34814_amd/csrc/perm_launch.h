@@ -7,13 +7,11 @@
 #include "wavealign.h"
 
 struct WaPermLaunch {
-  const uint64_t* rowbits;  // [bh][m][ceil(n/64)]
-  const uint64_t* colbits;  // [bh][n][ceil(m/64)]
+  const uint64_t* rowbits;  // [bh][ceil(n/64)][m] word-major
+  const uint64_t* colbits;  // [bh][ceil(m/64)][n] word-major
   const int32_t* row_nnz;   // [bh][m]
   int32_t* col_cnt;         // [bh][n], nullable
   int64_t* head_stats;      // [bh][6], nullable
-  int64_t* zbuf;            // [bh][m][2] scratch
-  int64_t* ybuf;            // [bh][n][2] scratch
   int32_t* perm;            // [bh][m]
   uint8_t* flags;           // [bh], nullable
   int32_t* embedding;       // [bh][m][2], nullable
@@ -30,8 +28,8 @@ hipError_t wa_launch_perm_heads(const WaPermLaunch& a, hipStream_t stream);
 size_t wa_perm_shared_bytes();
 hipError_t wa_launch_fp64_probe(const double* a, const double* b, const int64_t* c, double* out, int n,
                                 hipStream_t stream);
-hipError_t wa_launch_pack_rows(const uint8_t* mask, int64_t rows, int n, uint64_t* rowbits, int32_t* row_nnz,
-                               hipStream_t stream);
+hipError_t wa_launch_pack_rows(const uint8_t* mask, int64_t rows, int m, int n, uint64_t* rowbits,
+                               int32_t* row_nnz, hipStream_t stream);
 hipError_t wa_launch_transpose_bits(const uint64_t* rowbits, int bh, int m, int n, uint64_t* colbits,
                                     hipStream_t stream);
 hipError_t wa_launch_xcc_probe(int32_t* out, int n_wg, hipStream_t stream);
