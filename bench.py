@@ -54,6 +54,64 @@ def load_traffic(workload: str, variant: str):
     return entry.get("hbm_bytes_per_launch")
 
 
+def _pmc_means(csv_path: str, kernel_substr: str):
+    import csv
+    vals = {}
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            if kernel_substr in r["Kernel_Name"]:
+                vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in vals.items()}, max((len(v) for v in vals.values()), default=0)
+
+
+def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_note: str) -> None:
+    """Turn rocprofv3 --pmc CSV passes into the traffic figure and a text summary.
+
+    Expects <root>/<variant>_{A,B,C}/run_counter_collection.csv for the attention kernel
+    (A: TCC_HIT_sum TCC_MISS_sum SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES
+    GRBM_GUI_ACTIVE; B: FETCH_SIZE; C: WRITE_SIZE TCC_EA0_RDREQ_DRAM_sum) and copy_{B,C} for a plain
+    1 GiB device copy, whose FETCH_SIZE / WRITE_SIZE give the byte-scaling factors.
+    """
+    cb, _ = _pmc_means(os.path.join(root, "copy_B", "run_counter_collection.csv"), "copyBuffer")
+    cc, _ = _pmc_means(os.path.join(root, "copy_C", "run_counter_collection.csv"), "copyBuffer")
+    copy_bytes = float(1 << 30)
+    f_fetch = copy_bytes / (cb["FETCH_SIZE"] * 1024.0)
+    f_write = copy_bytes / (cc["WRITE_SIZE"] * 1024.0)
+    sha = kernel_source_hash()
+    try:
+        with open(out_json) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        data = {}
+    lines = [f"# attention kernel counters, workload {workload}", "", f"Command: {command_note}", "",
+             f"Copy calibration (1 GiB device copy): FETCH_SIZE x {f_fetch:.3f}, WRITE_SIZE x {f_write:.3f}", "",
+             "| variant | dispatches | L2 hit % | L2->fabric read GB/launch (scaled) | write GB/launch (scaled) | "
+             "DRAM read req | MFMA FLOP (MOPS x 512) | MFMA busy % |",
+             "|---|---|---|---|---|---|---|---|"]
+    entry = data.setdefault(workload, {})
+    variants = sorted({d.rsplit("_", 1)[0] for d in os.listdir(root) if d.endswith("_A")})
+    for v in variants:
+        a, na = _pmc_means(os.path.join(root, f"{v}_A", "run_counter_collection.csv"), "attn_fwd")
+        b, _ = _pmc_means(os.path.join(root, f"{v}_B", "run_counter_collection.csv"), "attn_fwd")
+        c, _ = _pmc_means(os.path.join(root, f"{v}_C", "run_counter_collection.csv"), "attn_fwd")
+        hit = a["TCC_HIT_sum"] / (a["TCC_HIT_sum"] + a["TCC_MISS_sum"])
+        fetch = b["FETCH_SIZE"] * 1024.0 * f_fetch
+        write = c["WRITE_SIZE"] * 1024.0 * f_write
+        cycles = a["GRBM_GUI_ACTIVE"] / 8.0          # summed over the 8 XCDs
+        busy = a["SQ_VALU_MFMA_BUSY_CYCLES"] / (256 * 4 * cycles)
+        entry[v] = {"kernel_sha": sha, "hbm_bytes_per_launch": fetch + write, "fetch_bytes": fetch,
+                    "write_bytes": write, "l2_hit": hit, "dram_read_requests": c["TCC_EA0_RDREQ_DRAM_sum"],
+                    "mfma_flop": a["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512, "mfma_busy": busy}
+        lines.append(f"| {v} | {na} | {100 * hit:.2f} | {fetch / 1e9:.1f} | {write / 1e9:.2f} | "
+                     f"{c['TCC_EA0_RDREQ_DRAM_sum']:.4g} | {a['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.4g} | "
+                     f"{100 * busy:.1f} |")
+    with open(out_json, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def cpu_baseline(wl, q, k, v, mask, total_flop, budget_s: float):
     """The oracle, as it stands, timed on a bounded sample of the workload on the host cores."""
     from oracle import attention as A
@@ -107,7 +165,15 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (3 times), to calibrate the HBM counters")
+    ap.add_argument("--summarize-pmc", metavar="DIR", help="summarize rocprofv3 counter passes found in DIR "
+                    "into profiles/attn_traffic.json and a markdown table (no GPU needed)")
+    ap.add_argument("--pmc-command", default="", help="command line recorded in the counter summary")
     args = ap.parse_args()
+
+    if args.summarize_pmc:
+        md = os.path.join(ROOT, "profiles", f"attn_fwd_{args.config}_counters.md")
+        summarize_pmc(args.summarize_pmc, args.config, TRAFFIC_FILE, md, args.pmc_command)
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the path is a single-GPU kernel pipeline "

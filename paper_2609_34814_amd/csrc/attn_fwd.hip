@@ -37,6 +37,8 @@
 
 #include "common.h"
 
+#include <type_traits>
+
 namespace {
 
 using wa::bf16x8;
@@ -46,6 +48,7 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kRescale = 8.0f;  // log2 headroom of the lazily rescaled running maximum
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
 #define WA_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14))
@@ -53,14 +56,13 @@ constexpr float kLn2 = 0.6931471805599453f;
 // memory accesses across it
 #define WA_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __builtin_bit_cast(uint32_t, f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
+// two floats -> two bf16 (round to nearest even; one v_cvt_pk_bf16_f32 on gfx950)
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return (uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16);
+  const f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -97,11 +99,19 @@ struct Cfg {
 
 // One 16-byte-per-lane copy from global memory (uniform base + per-lane byte offset) into LDS at the
 // uniform address lds (lane i writes lds + 16 i). Written as inline assembly so that only the
-// explicit vmcnt waits of the pipeline order it against LDS reads of the other tile.
+// explicit vmcnt waits of the pipeline order it against LDS reads of the other tile; M0 (the LDS
+// base of the copy) is restored afterwards.
 __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, const unsigned char* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)lds);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(gbase)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(m0), "v"(voff), "s"(gbase)
+      : "memory");
 }
 
 // DMA geometry of a tile with rows of RB bytes copied by NW wavefronts: instruction i of wavefront w
@@ -166,7 +176,7 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform within the wavefront
   const int l32 = lane & 31;
   const int hf = lane >> 5;
 
@@ -225,9 +235,12 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
   const float c2 = a.scale * kLog2e;
   const int krow_lane = 16 * (l32 >> 4) + perm16(l32 & 15);  // tile row supplied by this lane in a 32-row group
 
-  for (int e = beg; e < end; ++e) {
-    const int key0 = j_cur * BLK;
-    const int nvalid = min(BLK, n - key0);
+  // One KV block: wait for its tiles, S^T = K_j Q^T, online softmax, O^T += V_j^T P^T, and keep the
+  // copies of the next block in flight. MASKED handles the ragged last block (keys past the end of
+  // the sequence score -inf); the lists are ascending, so it can only be a row's last block.
+  int e = beg;
+  auto kv_block = [&](auto masked_tag) {
+    constexpr bool MASKED = decltype(masked_tag)::value;
     const bool has_next = e + 1 < end;
     int j_next = 0;
     if (has_next) {
@@ -257,7 +270,8 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     if (has_next) issue_k<D, BLK>(k_lds, kg, j_next * BLK, n, w, lane);
 
     // ---- online softmax (log2 domain) ----
-    if (nvalid < BLK) {
+    if constexpr (MASKED) {
+      const int nvalid = n - j_cur * BLK;
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
@@ -271,10 +285,20 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kt][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * c2);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+    // Lazy rescaling: the running maximum is raised (and O, l rescaled) only when some query of the
+    // wavefront sees a score above it by more than kRescale; otherwise the probabilities are taken
+    // against the old maximum and stay below 2^kRescale.
+    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescale)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
+    }
 
     float lsum = 0.f;
     uint32_t pb[C::KT][8];
@@ -282,16 +306,12 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
       for (int v = 0; v < 16; v += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v], c2, -m_new));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v + 1], c2, -m_new));
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v], c2, -m_run));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v + 1], c2, -m_run));
         lsum += p0 + p1;
         pb[kt][v >> 1] = pack_bf16x2(p0, p1);
       }
-    l_run = l_run * alpha + lsum;
-#pragma unroll
-    for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
+    l_run += lsum;
 
     // V_j resident (K_{j+1} may still be in flight)
     if (has_next) {
@@ -319,7 +339,10 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     WA_BARRIER();
     if (has_next) issue_v<D, BLK>(v_lds, vtg, vt_row_bytes, j_next * BLK, w, lane);
     j_cur = j_next;
-  }
+  };
+  const bool ragged_last = end > beg && (n % BLK) != 0 && cols[end - 1] == a.mb - 1;
+  for (; e < end - (ragged_last ? 1 : 0); ++e) kv_block(std::false_type{});
+  if (ragged_last) kv_block(std::true_type{});
 
   // ---- epilogue: normalise and store at the original rows ----
   const float ltot = l_run + __shfl_xor(l_run, 32);

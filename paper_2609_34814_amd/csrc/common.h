@@ -35,6 +35,32 @@ __host__ __device__ inline void xcd_slots(int g, int m, int n_xcd, const int32_t
   *last = min(*first + c, s1);
 }
 
+// Workgroups of one head when each workgroup runs pairs of consecutive slots.
+__host__ __device__ inline int pair_wg_per_xcd(int m, int n_xcd) { return (wg_per_xcd(m, n_xcd) + 1) / 2; }
+__host__ __device__ inline int pair_wg_per_head(int m, int n_xcd) { return n_xcd * pair_wg_per_xcd(m, n_xcd); }
+
+// Slots [first, last) run, two at a time, by workgroup g of one head: the L = ceil(ceil(m/n_xcd)/2)
+// workgroups of XCD x take the pairs of consecutive slots of segment x in order, c = ceil(pairs / L)
+// pairs each (the last pair of a segment of odd length has one slot).
+__host__ __device__ inline void xcd_pairs(int g, int m, int n_xcd, const int32_t* seg, int* first, int* last) {
+  const int x = g % n_xcd;
+  const int l = g / n_xcd;
+  const int L = pair_wg_per_xcd(m, n_xcd);
+  int s0, s1;
+  if (seg) {
+    s0 = min(max(seg[x], 0), m);
+    s1 = min(max(seg[x + 1], s0), m);
+  } else {
+    const int base = m / n_xcd, extra = m % n_xcd;
+    s0 = x * base + (x < extra ? x : extra);
+    s1 = s0 + base + (x < extra ? 1 : 0);
+  }
+  const int pairs = (s1 - s0 + 1) / 2;
+  const int c = (pairs + L - 1) / L;
+  *first = min(s0 + 2 * l * c, s1);
+  *last = min(*first + 2 * c, s1);
+}
+
 }  // namespace wa
 
 // Launch helpers (implemented in the .hip sources, called by the ABI layer).

@@ -156,6 +156,13 @@ def test_permutation_bit_exact(name, mode):
     _perm_case(wl, mask, wave=64, n_xcd=8, mode=mode)
 
 
+@pytest.mark.parametrize("name,mode", [("wan14b-720p-81f", S.SKIP_NEVER), ("wan14b-720p-81f", S.SKIP_AUTO),
+                                       ("long-720p-401f", S.SKIP_NEVER)])
+def test_permutation_bit_exact_full_size(name, mode):
+    wl = CONFIGS[name]
+    _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=mode)
+
+
 @pytest.mark.parametrize("n_xcd,wave,seed", [(1, 132, 5), (2, 7, 99), (8, 1, 3)])
 def test_permutation_bit_exact_params(n_xcd, wave, seed):
     wl = CONFIGS["wan1.3b-480p-81f"]
