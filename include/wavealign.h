@@ -158,9 +158,10 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
 wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* row_ptr, int32_t* col_idx,
                           void* stream);
 
-/* Workspace bytes needed by wa_sparse_attn: a zero-padded transposed copy of V
- * (bf16 [B][H][head_dim][M_B*block]) followed by the compacted lists. The V^T
- * copy alone (the leading part) suffices for wa_sparse_attn_csr. */
+/* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters
+ * and per-queue prefix tables, (64 + 64 * (B*H + 1)) int32 rounded up to 256 bytes)
+ * followed by the compacted lists. The scheduler part alone (the leading part)
+ * suffices for wa_sparse_attn_csr. Calls that share a workspace must not overlap. */
 wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Block-sparse attention forward: for every query block i and token q in it,
@@ -175,10 +176,11 @@ wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
  *   seg_start    int32 [B][H][n_xcd+1] XCD segment table from wa_build_permutation,
  *                NULL = segments of equal row count (the first M_B mod n_xcd one longer)
  *   softmax_scale  <= 0 selects 1/sqrt(d)
- *   n_xcd        number of XCD segments: the workgroups of a head are dispatched round-robin
- *                over the XCDs, and the ceil(M_B/n_xcd) workgroups of XCD x run the slots of
- *                segment x in order, each taking ceil(len_x / ceil(M_B/n_xcd)) consecutive
- *                slots; 1: slot = workgroup index (plain dispatch order)
+ *   n_xcd        number of XCD segments, 1..64. The kernel is persistent (one workgroup
+ *                per resident slot); queue x holds segment x of every head, heads in order,
+ *                and a workgroup takes the next slot of the queue of the XCD it runs on
+ *                (hardware XCC id mod n_xcd), then of the other queues once that one is
+ *                empty. 1: one queue, plain slot order on every XCD
  *   o            out bf16 [B][H][N][d]
  *   lse          out float [B][H][N] natural-log sum-exp of the scaled scores, nullable
  *   workspace    >= wa_attn_workspace_size(shape) */
@@ -188,7 +190,8 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
 
 /* As wa_sparse_attn, from lists already built by wa_compact_mask (row i of head
  * (b,h) visits col_idx[(b*H+h)*M_B*N_B + row_ptr[b][h][i] ...] in list order).
- * workspace >= B*H*head_dim*M_B*block*2 bytes (rounded up to 256), 256-byte aligned. */
+ * workspace >= the scheduler part of wa_attn_workspace_size ((64 + 64 * (B*H + 1)) int32,
+ * rounded up to 256 bytes), 256-byte aligned. */
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                              const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
                              const wa_shape* shape,

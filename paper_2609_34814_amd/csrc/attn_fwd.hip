@@ -5,14 +5,13 @@
 // and partial O kept on chip). The workgroup has BLK/32 wavefronts; wavefront w
 // owns query rows [32w, 32w+32) of the block. Two workgroups share a CU.
 //
-// Data movement. K_j and V_j^T (V transposed once per call into a zero-padded
-// [d][N_pad] copy) are copied from global memory straight into LDS with
-// global_load_lds_dwordx4 (no register staging; rows past the end of the
-// sequence are clamped to the last row and masked). Only explicit vmcnt waits
-// order these copies against LDS reads, so the copy into one tile stays in
-// flight while the other tile is read. The LDS tiles are XOR-swizzled
-// at 16-byte granularity so that the MFMA operand reads (ds_read_b128, one row
-// per lane) are free of bank conflicts; the swizzle is applied by choosing each
+// Data movement. K_j and V_j (both in their natural [token][d] layout) are
+// copied from global memory straight into LDS with global_load_lds_dwordx4 (no
+// register staging; rows past the end of the sequence are clamped to the last
+// row and masked). Only explicit vmcnt waits order these copies against LDS
+// reads, so the copy into one tile stays in flight while the other tile is read.
+// The LDS tiles are XOR-swizzled at 16-byte granularity so that the MFMA operand
+// reads are free of bank conflicts; the swizzle is applied by choosing each
 // lane's global source chunk. The loads of K_{j+1} are issued as soon as every
 // wavefront has finished reading K_j and overlap the softmax and P V of block j;
 // the loads of V_{j+1} overlap the next Q K^T.
@@ -25,18 +24,24 @@
 //     keys of one query (lane mod 32): the softmax max and sum are lane-local plus
 //     one exchange with lane^32, and
 //   * P^T in bf16 is the B operand of O^T += V^T P^T directly from those
-//     registers; the matching A operand is one 16-byte row chunk of V^T.
+//     registers; the matching A operand (8 keys of one column of V) is gathered
+//     from the row-major V tile with two transposing LDS reads (ds_read_b64_tr_b16).
 //   * O^T rows use the same permutation, so each lane finally holds 8 consecutive
 //     output columns and O is written with 16-byte stores at the block's original
 //     rows (the inverse permutation is fused into the store).
 // Keys past the end of the sequence (ragged last block) get score -inf.
 //
-// Workgroup -> query blocks: workgroup g of head bh runs the slots xcd_slots(g)
-// (its share of its XCD's segment) and slot s computes original block perm[s]
-// (identity when perm is null).
+// Scheduling. The kernel is persistent: one workgroup per resident slot of the
+// chip. Queue x holds, head after head, the slots of XCD segment x; a workgroup
+// takes the next slot of the queue of the XCD it runs on (hardware XCC id), so
+// that the query blocks that run together on one XCD, and share its L2, are
+// consecutive slots of one segment (Sec. IV-D), and when that queue is empty
+// it takes slots from the other queues. Slot s of head bh computes original
+// query block perm[bh][s] (identity when perm is null).
 
 #include "common.h"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace {
@@ -71,27 +76,35 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast
 // gives each lane half 8 consecutive tile rows.
 __device__ __forceinline__ int perm16(int r) { return ((r >> 2) & 1) * 8 + ((r >> 3) & 1) * 4 + (r & 3); }
 
-// Tile with rows of RB bytes (256 or 128) in 16-byte chunks; physical chunk of (row, chunk).
+// Tiles have rows of RB bytes (256 or 128) in 16-byte chunks. Physical chunk of (row, chunk):
+// K tiles are read one row per lane (ds_read_b128), 16 rows per wavefront quarter;
+// V tiles are read by the transposing loads, four consecutive rows at a time.
 template <int RB>
-__device__ __forceinline__ int swz(int row, int chunk) {
+__device__ __forceinline__ int swz_k(int row, int chunk) {
   return RB == 256 ? (chunk ^ (row & 15)) : (chunk ^ ((row >> 1) & 7));
+}
+template <int RB>
+__device__ __forceinline__ int swz_v(int row, int chunk) {
+  const int e = row & 3;  // XOR 0, 6, 12, 10 (256-byte rows) or 0, 2, 4, 6 (128-byte rows): stays in the row
+  return RB == 256 ? (chunk ^ ((e << 1) ^ (e << 2))) : (chunk ^ (e << 1));
+}
+template <int RB, bool V>
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return V ? swz_v<RB>(row, chunk) : swz_k<RB>(row, chunk);
 }
 
 template <int RB>
 __device__ __forceinline__ uint4 lds_chunk(const unsigned char* tile, int row, int chunk) {
-  return *(const uint4*)(tile + row * RB + swz<RB>(row, chunk) * 16);
+  return *(const uint4*)(tile + row * RB + swz_k<RB>(row, chunk) * 16);
 }
 
 template <int D, int BLK>
 struct Cfg {
   static constexpr int NW = BLK / 32;
   static constexpr int NT = NW * 64;
-  static constexpr int KRB = D * 2;       // K tile row bytes
-  static constexpr int VRB = BLK * 2;     // V^T tile row bytes
-  static constexpr int KBYTES = BLK * KRB;
-  static constexpr int VBYTES = D * VRB;
-  static constexpr int NK = KBYTES / (NT * 16);  // DMA instructions per thread, K tile
-  static constexpr int NV = VBYTES / (NT * 16);  // DMA instructions per thread, V^T tile
+  static constexpr int RB = D * 2;        // K and V tile row bytes
+  static constexpr int TBYTES = BLK * RB;
+  static constexpr int NK = TBYTES / (NT * 16);  // DMA instructions per thread and tile
   static constexpr int KT = BLK / 32;
   static constexpr int DT = D / 32;
   static constexpr int KS = D / 16;
@@ -116,291 +129,339 @@ __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, const un
 
 // DMA geometry of a tile with rows of RB bytes copied by NW wavefronts: instruction i of wavefront w
 // writes tile rows [(i*NW + w)*RPI, +RPI), lane l the chunk (l mod LPR) of row (l / LPR) among them.
-// The global source of that slot is chunk swz(row, slot) of the row (the swizzle is an involution).
-template <int RB, int NW>
+// The global source of that slot is chunk swz(row, slot) of the row (each swizzle is an involution).
+template <int RB, int NW, bool V>
 struct Dma {
   static constexpr int RPI = 1024 / RB;   // rows per instruction
   static constexpr int LPR = RB / 16;     // lanes per row
-  // the swizzle of a lane's slot is the same for every instruction when the row step is a multiple of 16
-  static constexpr bool kInvariant = (NW * RPI) % 16 == 0;
+  // the swizzle of a lane's slot is the same for every instruction when the row step is a multiple of
+  // the swizzle's row period
+  static constexpr bool kInvariant = (NW * RPI) % (V ? 4 : 16) == 0;
   __device__ static __forceinline__ int row(int i, int w, int lane) { return (i * NW + w) * RPI + lane / LPR; }
-  // per-lane source bytes relative to row (i*NW)*RPI of the tile (row stride `stride` bytes in memory)
-  __device__ static __forceinline__ uint32_t lane_bytes(int i, int w, int lane, uint32_t stride) {
+  // per-lane source bytes relative to tile row (i*NW)*RPI
+  __device__ static __forceinline__ uint32_t lane_bytes(int i, int w, int lane) {
     const int r0 = w * RPI + lane / LPR;
     const int rs = kInvariant ? r0 : row(i, w, lane);
-    return (uint32_t)r0 * stride + (uint32_t)(swz<RB>(rs, lane % LPR) * 16);
+    return (uint32_t)r0 * RB + (uint32_t)(swz<RB, V>(rs, lane % LPR) * 16);
   }
 };
 
-// DMA of K rows [key0, key0 + BLK) of the head (kg: its first row) into the swizzled K tile. In the
-// ragged last block, rows past the end of the sequence are clamped to the last row (their scores are
-// masked).
-template <int D, int BLK>
-__device__ __forceinline__ void issue_k(unsigned char* ktile, const unsigned char* kg, int key0, int n, int w,
-                                        int lane) {
+// DMA of rows [key0, key0 + BLK) of a K or V head (g: its first row) into a swizzled tile. In the
+// ragged last block, rows past the end of the sequence are clamped to the last row (their scores
+// are masked, so their probabilities are 0).
+template <int D, int BLK, bool V>
+__device__ __forceinline__ void issue_tile(unsigned char* tile, const unsigned char* g, int key0, int n, int w,
+                                           int lane) {
   using C = Cfg<D, BLK>;
-  using G = Dma<C::KRB, C::NW>;
+  using G = Dma<C::RB, C::NW, V>;
   if (key0 + BLK <= n) {
 #pragma unroll
     for (int i = 0; i < C::NK; ++i)
-      dma16(kg + (int64_t)(key0 + i * C::NW * G::RPI) * C::KRB, G::lane_bytes(i, w, lane, C::KRB),
-            ktile + (i * C::NW + w) * 1024);
+      dma16(g + (int64_t)(key0 + i * C::NW * G::RPI) * C::RB, G::lane_bytes(i, w, lane),
+            tile + (i * C::NW + w) * 1024);
   } else {
 #pragma unroll
     for (int i = 0; i < C::NK; ++i) {
       const int r = G::row(i, w, lane);
-      const uint32_t off = (uint32_t)min(key0 + r, n - 1) * (uint32_t)C::KRB +
-                           (uint32_t)(swz<C::KRB>(r, lane % G::LPR) * 16);
-      dma16(kg, off, ktile + (i * C::NW + w) * 1024);
+      const uint32_t off = (uint32_t)min(key0 + r, n - 1) * (uint32_t)C::RB +
+                           (uint32_t)(swz<C::RB, V>(r, lane % G::LPR) * 16);
+      dma16(g, off, tile + (i * C::NW + w) * 1024);
     }
   }
 }
 
-// DMA of the V^T tile: rows d of the transposed copy (row stride row_bytes), keys [key0, key0 + BLK).
-template <int D, int BLK>
-__device__ __forceinline__ void issue_v(unsigned char* vtile, const unsigned char* vtg, uint32_t row_bytes, int key0,
-                                        int w, int lane) {
-  using C = Cfg<D, BLK>;
-  using G = Dma<C::VRB, C::NW>;
-#pragma unroll
-  for (int i = 0; i < C::NV; ++i)
-    dma16(vtg + (int64_t)key0 * 2 + (int64_t)(i * C::NW * G::RPI) * row_bytes, G::lane_bytes(i, w, lane, row_bytes),
-          vtile + (i * C::NW + w) * 1024);
+// Transposing LDS read (gfx950 ds_read_b64_tr_b16): within each group of 16 lanes, lane i receives
+// element (i mod 4) of the 8-byte chunks addressed by lanes 4e + i/4 of the group, e = 0..3.
+__device__ __forceinline__ uint2 lds_read_tr(const unsigned char* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  const v4s r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(lds_void_t*)p);
+  return __builtin_bit_cast(uint2, r);
+}
+
+// Next task of this workgroup: slot of a head from the queue of its XCD, else from the others.
+// Run by one lane; returns false when every queue is exhausted.
+__device__ bool fetch_task(const WaAttnLaunch& a, int home, int* bh_out, int* slot_out) {
+  int32_t* cnt = a.sched;
+  const int32_t* pre = a.sched + 64;
+  for (int k = 0; k < a.n_xcd; ++k) {
+    const int x = (home + k) % a.n_xcd;
+    const int32_t* px = pre + (int64_t)x * (a.bh + 1);
+    const int total = px[a.bh];
+    if (__hip_atomic_load(cnt + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= total) continue;
+    const int t = atomicAdd(cnt + x, 1);
+    if (t >= total) continue;
+    // head h with px[h] <= t < px[h+1]
+    int lo = 0, hi = a.bh - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (px[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    int s0, s1;
+    wa::xcd_segment(x, a.mb, a.n_xcd, a.seg ? a.seg + (int64_t)lo * (a.n_xcd + 1) : nullptr, &s0, &s1);
+    *bh_out = lo;
+    *slot_out = s0 + (t - px[lo]);
+    return true;
+  }
+  return false;
 }
 
 template <int D, int BLK>
 __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
   using C = Cfg<D, BLK>;
-  __shared__ __attribute__((aligned(1024))) unsigned char k_lds[C::KBYTES];
-  __shared__ __attribute__((aligned(1024))) unsigned char v_lds[C::VBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char k_lds[C::TBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char v_lds[C::TBYTES];
+  __shared__ int task[2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform within the wavefront
   const int l32 = lane & 31;
   const int hf = lane >> 5;
-
-  const int wgh = wa::wg_per_head(a.mb, a.n_xcd);
-  const int bh = blockIdx.x / wgh;
-  int slot_first, slot_last;
-  wa::xcd_slots(blockIdx.x % wgh, a.mb, a.n_xcd, a.seg ? a.seg + (int64_t)bh * (a.n_xcd + 1) : nullptr,
-                &slot_first, &slot_last);
-  for (int slot = slot_first; slot < slot_last; ++slot) {
-  const int row = a.perm ? a.perm[(int64_t)bh * a.mb + slot] : slot;
-  if ((unsigned)row >= (unsigned)a.mb) continue;  // not a valid block index: nothing to compute
-
   const int n = a.seq_len;
-  const int64_t npad = (int64_t)a.mb * BLK;
-  const uint16_t* qg = (const uint16_t*)a.q + (int64_t)bh * n * D;
-  const unsigned char* kg = (const unsigned char*)a.k + (int64_t)bh * n * D * 2;
-  const unsigned char* vtg = (const unsigned char*)a.vt + (int64_t)bh * D * npad * 2;
-  const uint32_t vt_row_bytes = (uint32_t)(npad * 2);
-
-  const int32_t* rp = a.row_ptr + (int64_t)bh * (a.mb + 1);
-  const int beg = rp[row];
-  const int end = rp[row + 1];
-  // read-only for the whole kernel: the constant address space lets the list be read with scalar loads
-  typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
-  const const_i32_ptr cols = (const_i32_ptr)(a.col_idx + (int64_t)bh * a.mb * a.mb);
-
-  // Q columns of this wavefront: B operand of S^T = K Q^T
-  const int qi = row * BLK + w * 32 + l32;
-  bf16x8 qf[C::KS];
-#pragma unroll
-  for (int s = 0; s < C::KS; ++s) {
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (qi < n) val = *(const uint4*)(qg + (int64_t)qi * D + 16 * s + 8 * hf);
-    qf[s] = as_bf16x8(val);
-  }
-
-  int j_cur = 0;
-  if (beg < end) {
-    j_cur = cols[beg];
-    if ((unsigned)j_cur >= (unsigned)a.mb) j_cur = 0;
-    issue_k<D, BLK>(k_lds, kg, j_cur * BLK, n, w, lane);
-    issue_v<D, BLK>(v_lds, vtg, vt_row_bytes, j_cur * BLK, w, lane);
-  }
-  // the Q loads (issued first) are complete; the first tiles stay in flight
-  WA_WAIT_VM(C::NK + C::NV);
-
-
-  f32x16 oacc[C::DT];
-#pragma unroll
-  for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
-
-  float m_run = -INFINITY;
-  float l_run = 0.f;
   const float c2 = a.scale * kLog2e;
-  const int krow_lane = 16 * (l32 >> 4) + perm16(l32 & 15);  // tile row supplied by this lane in a 32-row group
+  const int krow_lane = 16 * (l32 >> 4) + perm16(l32 & 15);  // K tile row supplied by this lane in a 32-row group
 
-  // One KV block: wait for its tiles, S^T = K_j Q^T, online softmax, O^T += V_j^T P^T, and keep the
-  // copies of the next block in flight. MASKED handles the ragged last block (keys past the end of
-  // the sequence score -inf); the lists are ascending, so it can only be a row's last block.
-  int e = beg;
-  auto kv_block = [&](auto masked_tag) {
-    constexpr bool MASKED = decltype(masked_tag)::value;
-    const bool has_next = e + 1 < end;
-    int j_next = 0;
-    if (has_next) {
-      j_next = cols[e + 1];
-      if ((unsigned)j_next >= (unsigned)a.mb) j_next = 0;
+  // V tile addressing of the transposing reads (see lds_read_tr): lane (e, q) = ((lane mod 16) / 4,
+  // lane mod 4) of 16-lane group G = lane / 16 supplies row 8 (G / 2) + e (+ 32 kt + 16 k2 + 4 half)
+  // and columns 32 dt + 16 (G mod 2) + {0, 8, 4, 12}[q] .. +3, which are the O^T rows perm16 puts there.
+  const int ve = (lane & 15) >> 2, vq = lane & 3, vg = lane >> 4;
+  const unsigned char* v_lane = v_lds + (8 * (vg >> 1) + ve) * C::RB + 8 * (vq >> 1);
+  uint32_t v_chunk[C::DT];
+#pragma unroll
+  for (int dt = 0; dt < C::DT; ++dt)
+    v_chunk[dt] = 16u * (uint32_t)swz_v<C::RB>(ve, 4 * dt + 2 * (vg & 1) + (vq & 1));
+
+  const int home = (int)(__builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 0xF) % a.n_xcd;
+
+  for (;;) {
+    if (tid == 0) {
+      int tb = -1, ts = 0;
+      if (!fetch_task(a, home, &tb, &ts)) tb = -1;
+      task[0] = tb;
+      task[1] = ts;
+    }
+    __syncthreads();
+    const int bh = __builtin_amdgcn_readfirstlane(task[0]);
+    const int slot = __builtin_amdgcn_readfirstlane(task[1]);
+    __syncthreads();  // every wavefront has read the task before it is overwritten
+    if (bh < 0) break;
+    const int row = a.perm ? a.perm[(int64_t)bh * a.mb + slot] : slot;
+    if ((unsigned)row >= (unsigned)a.mb) continue;  // not a valid block index: nothing to compute
+
+    const uint16_t* qg = (const uint16_t*)a.q + (int64_t)bh * n * D;
+    const unsigned char* kg = (const unsigned char*)a.k + (int64_t)bh * n * D * 2;
+    const unsigned char* vg_ = (const unsigned char*)a.v + (int64_t)bh * n * D * 2;
+
+    const int32_t* rp = a.row_ptr + (int64_t)bh * (a.mb + 1);
+    const int beg = rp[row];
+    const int end = rp[row + 1];
+    // read-only for the whole kernel: the constant address space lets the list be read with scalar loads
+    typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
+    const const_i32_ptr cols = (const_i32_ptr)(a.col_idx + (int64_t)bh * a.mb * a.mb);
+
+    // Q columns of this wavefront: B operand of S^T = K Q^T
+    const int qi = row * BLK + w * 32 + l32;
+    bf16x8 qf[C::KS];
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s) {
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (qi < n) val = *(const uint4*)(qg + (int64_t)qi * D + 16 * s + 8 * hf);
+      qf[s] = as_bf16x8(val);
     }
 
-    // K_j resident (V_j may still be in flight)
-    WA_WAIT_VM(C::NV);
-    WA_BARRIER();
+    int j_cur = 0;
+    if (beg < end) {
+      j_cur = cols[beg];
+      if ((unsigned)j_cur >= (unsigned)a.mb) j_cur = 0;
+      issue_tile<D, BLK, false>(k_lds, kg, j_cur * BLK, n, w, lane);
+      issue_tile<D, BLK, true>(v_lds, vg_, j_cur * BLK, n, w, lane);
+    }
+    // the Q loads (issued first) are complete; the first tiles stay in flight
+    WA_WAIT_VM(2 * C::NK);
 
-    // ---- S^T = K_j Q^T ----
-    f32x16 sacc[C::KT];
+    f32x16 oacc[C::DT];
 #pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt) {
+    for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[kt][v] = 0.f;
-      const int krow = kt * 32 + krow_lane;
-#pragma unroll
-      for (int s = 0; s < C::KS; ++s) {
-        const bf16x8 av = as_bf16x8(lds_chunk<C::KRB>(k_lds, krow, 2 * s + hf));
-        sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[s], sacc[kt], 0, 0, 0);
+      for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
+
+    float m_run = -INFINITY;
+    float l_run = 0.f;
+
+    // One KV block: wait for its tiles, S^T = K_j Q^T, online softmax, O^T += V_j^T P^T, and keep the
+    // copies of the next block in flight. MASKED handles the ragged last block (keys past the end of
+    // the sequence score -inf); the lists are ascending, so it can only be a row's last block.
+    int e = beg;
+    auto kv_block = [&](auto masked_tag) {
+      constexpr bool MASKED = decltype(masked_tag)::value;
+      const bool has_next = e + 1 < end;
+      int j_next = 0;
+      if (has_next) {
+        j_next = cols[e + 1];
+        if ((unsigned)j_next >= (unsigned)a.mb) j_next = 0;
       }
-    }
-    // every wavefront is done with K_j: start K_{j+1}
-    WA_BARRIER();
-    if (has_next) issue_k<D, BLK>(k_lds, kg, j_next * BLK, n, w, lane);
 
-    // ---- online softmax (log2 domain) ----
-    if constexpr (MASKED) {
-      const int nvalid = n - j_cur * BLK;
-#pragma unroll
-      for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = kt * 32 + 16 * (v >> 3) + 8 * hf + (v & 7);
-          if (key >= nvalid) sacc[kt][v] = -INFINITY;
-        }
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kt][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
-    // Lazy rescaling: the running maximum is raised (and O, l rescaled) only when some query of the
-    // wavefront sees a score above it by more than kRescale; otherwise the probabilities are taken
-    // against the old maximum and stay below 2^kRescale.
-    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescale)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
-    }
-
-    float lsum = 0.f;
-    uint32_t pb[C::KT][8];
-#pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-      for (int v = 0; v < 16; v += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v], c2, -m_run));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v + 1], c2, -m_run));
-        lsum += p0 + p1;
-        pb[kt][v >> 1] = pack_bf16x2(p0, p1);
-      }
-    l_run += lsum;
-
-    // V_j resident (K_{j+1} may still be in flight)
-    if (has_next) {
+      // K_j resident (V_j may still be in flight)
       WA_WAIT_VM(C::NK);
-    } else {
-      WA_WAIT_VM(0);
-    }
-    WA_BARRIER();
+      WA_BARRIER();
 
-    // ---- O^T += V_j^T P^T ----
+      // ---- S^T = K_j Q^T ----
+      f32x16 sacc[C::KT];
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt) {
-      const int vrow = dt * 32 + krow_lane;
+      for (int kt = 0; kt < C::KT; ++kt) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[kt][v] = 0.f;
+        const int krow = kt * 32 + krow_lane;
+#pragma unroll
+        for (int s = 0; s < C::KS; ++s) {
+          const bf16x8 av = as_bf16x8(lds_chunk<C::RB>(k_lds, krow, 2 * s + hf));
+          sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[s], sacc[kt], 0, 0, 0);
+        }
+      }
+      // every wavefront is done with K_j: start K_{j+1}
+      WA_BARRIER();
+      if (has_next) issue_tile<D, BLK, false>(k_lds, kg, j_next * BLK, n, w, lane);
+
+      // ---- online softmax (log2 domain) ----
+      if constexpr (MASKED) {
+        const int nvalid = n - j_cur * BLK;
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int key = kt * 32 + 16 * (v >> 3) + 8 * hf + (v & 7);
+            if (key >= nvalid) sacc[kt][v] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2) {
-          const bf16x8 av = as_bf16x8(lds_chunk<C::VRB>(v_lds, vrow, 4 * kt + 2 * k2 + hf));
-          const uint32_t* p = &pb[kt][4 * k2];
-          const bf16x8 bv = as_bf16x8(make_uint4(p[0], p[1], p[2], p[3]));
-          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, oacc[dt], 0, 0, 0);
-        }
-    }
-    // every wavefront is done with V_j: start V_{j+1}
-    WA_BARRIER();
-    if (has_next) issue_v<D, BLK>(v_lds, vtg, vt_row_bytes, j_next * BLK, w, lane);
-    j_cur = j_next;
-  };
-  const bool ragged_last = end > beg && (n % BLK) != 0 && cols[end - 1] == a.mb - 1;
-  for (; e < end - (ragged_last ? 1 : 0); ++e) kv_block(std::false_type{});
-  if (ragged_last) kv_block(std::true_type{});
-
-  // ---- epilogue: normalise and store at the original rows ----
-  const float ltot = l_run + __shfl_xor(l_run, 32);
-  const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-  if (qi < n) {
-    uint16_t* og = (uint16_t*)a.o + ((int64_t)bh * n + qi) * D;
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kt][v]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+      // Lazy rescaling: the running maximum is raised (and O, l rescaled) only when some query of the
+      // wavefront sees a score above it by more than kRescale; otherwise the probabilities are taken
+      // against the old maximum and stay below 2^kRescale.
+      if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescale)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt)
+        for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        const int col = dt * 32 + 16 * h2 + 8 * hf;
-        uint4 st;
-        st.x = pack_bf16x2(oacc[dt][8 * h2 + 0] * inv, oacc[dt][8 * h2 + 1] * inv);
-        st.y = pack_bf16x2(oacc[dt][8 * h2 + 2] * inv, oacc[dt][8 * h2 + 3] * inv);
-        st.z = pack_bf16x2(oacc[dt][8 * h2 + 4] * inv, oacc[dt][8 * h2 + 5] * inv);
-        st.w = pack_bf16x2(oacc[dt][8 * h2 + 6] * inv, oacc[dt][8 * h2 + 7] * inv);
-        *(uint4*)(og + col) = st;
+          for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
       }
-    if (a.lse && hf == 0)
-      a.lse[(int64_t)bh * n + qi] = ltot > 0.f ? (m_run + __log2f(ltot)) * kLn2 : -INFINITY;
+
+      float lsum = 0.f;
+      uint32_t pb[C::KT][8];
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+        for (int v = 0; v < 16; v += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v], c2, -m_run));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][v + 1], c2, -m_run));
+          lsum += p0 + p1;
+          pb[kt][v >> 1] = pack_bf16x2(p0, p1);
+        }
+      l_run += lsum;
+
+      // V_j resident (K_{j+1} may still be in flight)
+      if (has_next) {
+        WA_WAIT_VM(C::NK);
+      } else {
+        WA_WAIT_VM(0);
+      }
+      WA_BARRIER();
+
+      // ---- O^T += V_j^T P^T ----
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt) {
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+          for (int k2 = 0; k2 < 2; ++k2) {
+            const unsigned char* vp = v_lane + (32 * kt + 16 * k2) * C::RB + v_chunk[dt];
+            const uint2 lo = lds_read_tr(vp);
+            const uint2 hi = lds_read_tr(vp + 4 * C::RB);
+            const bf16x8 av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+            const uint32_t* p = &pb[kt][4 * k2];
+            const bf16x8 bv = as_bf16x8(make_uint4(p[0], p[1], p[2], p[3]));
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, oacc[dt], 0, 0, 0);
+          }
+      }
+      // every wavefront is done with V_j: start V_{j+1}
+      WA_BARRIER();
+      if (has_next) issue_tile<D, BLK, true>(v_lds, vg_, j_next * BLK, n, w, lane);
+      j_cur = j_next;
+    };
+    const bool ragged_last = end > beg && (n % BLK) != 0 && cols[end - 1] == a.mb - 1;
+    for (; e < end - (ragged_last ? 1 : 0); ++e) kv_block(std::false_type{});
+    if (ragged_last) kv_block(std::true_type{});
+
+    // ---- epilogue: normalise and store at the original rows ----
+    const float ltot = l_run + __shfl_xor(l_run, 32);
+    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+    if (qi < n) {
+      uint16_t* og = (uint16_t*)a.o + ((int64_t)bh * n + qi) * D;
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int col = dt * 32 + 16 * h2 + 8 * hf;
+          uint4 st;
+          st.x = pack_bf16x2(oacc[dt][8 * h2 + 0] * inv, oacc[dt][8 * h2 + 1] * inv);
+          st.y = pack_bf16x2(oacc[dt][8 * h2 + 2] * inv, oacc[dt][8 * h2 + 3] * inv);
+          st.z = pack_bf16x2(oacc[dt][8 * h2 + 4] * inv, oacc[dt][8 * h2 + 5] * inv);
+          st.w = pack_bf16x2(oacc[dt][8 * h2 + 6] * inv, oacc[dt][8 * h2 + 7] * inv);
+          *(uint4*)(og + col) = st;
+        }
+      if (a.lse && hf == 0)
+        a.lse[(int64_t)bh * n + qi] = ltot > 0.f ? (m_run + __log2f(ltot)) * kLn2 : -INFINITY;
+    }
   }
-  }  // slots
 }
 
-// V [bh][n][D] -> V^T [bh][D][mb*BLK], zero beyond n. One 64x64 tile per workgroup.
-template <int D>
-__global__ __launch_bounds__(256) void transpose_v_kernel(const uint16_t* __restrict__ v, uint16_t* __restrict__ vt,
-                                                         int n, int64_t npad, int tiles_n) {
-  __shared__ uint16_t t[64][66];
-  const int tile = blockIdx.x % tiles_n;
-  const int dtile = (blockIdx.x / tiles_n) % (D / 64);
-  const int64_t bh = blockIdx.x / ((int64_t)tiles_n * (D / 64));
-  const int key0 = tile * 64, d0 = dtile * 64;
-  const uint16_t* src = v + bh * n * D;
-  uint16_t* dst = vt + bh * D * npad;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    const int key = key0 + r;
-    t[r][tx] = key < n ? src[(int64_t)key * D + d0 + tx] : (uint16_t)0;
+// Scheduler set-up: zero the queue counters and build, per queue, the prefix sums of its segment
+// lengths over the heads. One workgroup; thread x handles queue x.
+__global__ __launch_bounds__(64) void sched_kernel(int32_t* sched, const int32_t* seg, int bh, int mb, int n_xcd) {
+  const int x = threadIdx.x;
+  if (x >= n_xcd) return;
+  sched[x] = 0;
+  int32_t* px = sched + 64 + (int64_t)x * (bh + 1);
+  int acc = 0;
+  px[0] = 0;
+  for (int h = 0; h < bh; ++h) {
+    int s0, s1;
+    wa::xcd_segment(x, mb, n_xcd, seg ? seg + (int64_t)h * (n_xcd + 1) : nullptr, &s0, &s1);
+    acc += s1 - s0;
+    px[h + 1] = acc;
   }
-  __syncthreads();
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t col = key0 + tx;
-    if (col < npad) dst[(int64_t)(d0 + r) * npad + col] = t[tx][r];
+}
+
+int resident_cus() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
   }
+  return cached[dev];
 }
 
 template <int D, int BLK>
 hipError_t launch_t(const WaAttnLaunch& a, hipStream_t stream) {
-  const int64_t npad = (int64_t)a.mb * BLK;
-  const int tiles_n = (int)((npad + 63) / 64);
-  const int64_t tgrid = (int64_t)a.bh * (D / 64) * tiles_n;
-  hipLaunchKernelGGL((transpose_v_kernel<D>), dim3((unsigned)tgrid), dim3(256), 0, stream, (const uint16_t*)a.v,
-                     (uint16_t*)a.vt, a.seq_len, npad, tiles_n);
+  hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(64), 0, stream, a.sched, a.seg, a.bh, a.mb, a.n_xcd);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t grid = (int64_t)a.bh * wa::wg_per_head(a.mb, a.n_xcd);
-  if (grid <= 0) return hipSuccess;
+  const int64_t tasks = (int64_t)a.bh * a.mb;
+  if (tasks <= 0) return hipSuccess;
+  int occ = 0;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, attn_fwd_kernel<D, BLK>, BLK * 2, 0);
+  if (e != hipSuccess) return e;
+  const int64_t grid = std::min<int64_t>(tasks, (int64_t)resident_cus() * std::max(occ, 1));
   hipLaunchKernelGGL((attn_fwd_kernel<D, BLK>), dim3((unsigned)grid), dim3(BLK * 2), 0, stream, a);
   return hipGetLastError();
 }
@@ -411,10 +472,6 @@ hipError_t occ_t(int* n) {
 }
 
 }  // namespace
-
-size_t wa_vt_bytes(int64_t bh, int mb, int head_dim, int block) {
-  return (size_t)bh * head_dim * (size_t)mb * block * 2;
-}
 
 hipError_t wa_launch_attention(const WaAttnLaunch& a, hipStream_t stream) {
   if (a.head_dim == 128 && a.block == 128) return launch_t<128, 128>(a, stream);

@@ -109,7 +109,7 @@ def test_sparse_attn_validation():
     assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, None, FAKE, None, None, ctypes.byref(s), 0.0, 8, FAKE, None,
                                   ctypes.c_void_p(1 << 24), ws_n.value, None) == L.WA_ERR_INVALID_ARG
     assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, ctypes.byref(s), 0.0, 8, FAKE, None,
-                                  ctypes.c_void_p(1 << 24), 1024, None) == L.WA_ERR_WORKSPACE
+                                  ctypes.c_void_p(1 << 24), 256, None) == L.WA_ERR_WORKSPACE
 
 
 def test_build_permutation_validation():
