@@ -24,7 +24,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from workloads import CONFIGS, make_mask, make_qkv  # noqa: E402
+from workloads import ALL_CONFIGS, make_mask, make_qkv  # noqa: E402
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0
@@ -64,6 +64,13 @@ def _pmc_means(csv_path: str, kernel_substr: str):
     return {k: sum(v) / len(v) for k, v in vals.items()}, max((len(v) for v in vals.values()), default=0)
 
 
+PMC_PASSES = {
+    "A": "TCC_HIT_sum TCC_MISS_sum SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE",
+    "B": "FETCH_SIZE",
+    "C": "WRITE_SIZE TCC_EA0_RDREQ_DRAM_sum",
+}
+
+
 def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_note: str) -> None:
     """Turn rocprofv3 --pmc CSV passes into the traffic figure and a text summary.
 
@@ -83,7 +90,28 @@ def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_
             data = json.load(f)
     except (OSError, ValueError):
         data = {}
-    lines = [f"# attention kernel counters, workload {workload}", "", f"Command: {command_note}", "",
+    run = ("cd /tmp && export TMPDIR=/tmp && cd $GRAFT_REPO_ROOT && timeout -s KILL 240 rocprofv3 --pmc {ctr} "
+           "--kernel-include-regex {kre} --output-format csv -d {root}/{{variant}}_{p} -o run -- {cmd}")
+    bench_cmd = (f"python bench.py --config {workload} --steps 2 --warmup 1 --no-cpu-baseline "
+                 "--variants {variant}")
+    passes = [("A", PMC_PASSES["A"], "attn_fwd", bench_cmd), ("B", PMC_PASSES["B"], "attn_fwd", bench_cmd),
+              ("C", PMC_PASSES["C"], "attn_fwd", bench_cmd),
+              ("copy B", PMC_PASSES["B"], "'copyBuffer|elementwise|copy'", "python bench.py --copy-calibration 1024"),
+              ("copy C", PMC_PASSES["C"].split()[0], "'copyBuffer|elementwise|copy'",
+               "python bench.py --copy-calibration 1024")]
+    lines = [f"# attention kernel counters, workload {workload}", "", "Commands (one rocprofv3 run per pass; "
+             "{variant} is the row of the table, the copy passes write to copy_B and copy_C):", ""]
+    for p, ctr, kre, cmd in passes:
+        lines.append(f"* pass {p}: `" + run.format(ctr=ctr, kre=kre, root=root, p=p.split()[-1], cmd=cmd)
+                     .replace("{variant}_B", "copy_B" if p == "copy B" else "{variant}_B")
+                     .replace("{variant}_C", "copy_C" if p == "copy C" else "{variant}_C") + "`")
+    if command_note:
+        lines += ["", f"Driver: {command_note}"]
+    lines += ["",
+             "L2 hit % = TCC_HIT / (TCC_HIT + TCC_MISS). L2->fabric read bytes = FETCH_SIZE x the copy factor, "
+             "write bytes = WRITE_SIZE x its factor (both per launch). MFMA FLOP = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512. "
+             "MFMA busy % = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs), i.e. against the clock "
+             "the chip actually ran at.", "",
              f"Copy calibration (1 GiB device copy): FETCH_SIZE x {f_fetch:.3f}, WRITE_SIZE x {f_write:.3f}", "",
              "| variant | dispatches | L2 hit % | L2->fabric read GB/launch (scaled) | write GB/launch (scaled) | "
              "DRAM read req | MFMA FLOP (MOPS x 512) | MFMA busy % |",
@@ -107,6 +135,38 @@ def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_
                      f"{100 * busy:.1f} |")
     with open(out_json, "w") as f:
         json.dump(data, f, indent=1, sort_keys=True)
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_trace(stats_csv: str, bench_json: str, out_md: str, command_note: str) -> None:
+    """Turn a rocprofv3 --kernel-trace --stats kernel table (and the bench line of the same run) into a
+    text summary: per-kernel calls and durations, and the attention kernel's average next to the
+    duration bench.py measured with HIP events in the same run."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    with open(bench_json) as f:
+        line = json.loads([ln for ln in f.read().splitlines() if ln.startswith("{")][-1])
+    lines = [f"# kernel trace: {line['config']['workload']}, variant {line['config']['variant']}", "",
+             f"Command: `{command_note}`", "",
+             "| kernel | calls | average ms | min ms | max ms | share % |", "|---|---|---|---|---|---|"]
+    attn_avg = None
+    for r in rows:
+        name = r["Name"]
+        short = name.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        avg = float(r["AverageNs"]) / 1e6
+        if "attn_fwd_kernel" in name:
+            attn_avg = avg
+        lines.append(f"| {short} | {r['Calls']} | {avg:.3f} | {float(r['MinNs']) / 1e6:.3f} | "
+                     f"{float(r['MaxNs']) / 1e6:.3f} | {float(r['Percentage']):.2f} |")
+    v = line["variants"][line["config"]["variant"]]
+    lines += ["", f"bench.py (HIP events around the attention call, same run): {v['attn_ms']:.3f} ms per launch, "
+              f"{v['tflops_attn']:.1f} TFLOP/s over {line['config']['flop_per_step']:.4g} FLOP; "
+              f"step {v['ms_per_step']:.3f} ms."]
+    if attn_avg:
+        lines.append(f"rocprofv3 attention kernel average: {attn_avg:.3f} ms "
+                     f"({line['config']['flop_per_step'] / (attn_avg * 1e-3) / 1e12:.1f} TFLOP/s).")
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -150,17 +210,39 @@ def cpu_baseline(wl, q, k, v, mask, total_flop, budget_s: float):
     }
 
 
+# Row orders and queue layouts compared by the benchmark. "queues" is the kernel's n_xcd: 8 = one
+# task queue per XCD (segment x of every head runs on XCD x), 1 = one queue in slot order for the chip.
+VARIANTS = {
+    "reordered": dict(perm="two-stage", skip="never", n_xcd=8),
+    "natural": dict(perm=None, n_xcd=1),
+    "natural-xcd": dict(perm=None, n_xcd=8),
+    "reordered-1q": dict(perm="two-stage", skip="never", n_xcd=1, wave_mult=8),
+    "auto": dict(perm="two-stage", skip="auto", n_xcd=8),
+    "s1-only": dict(perm="stage1", skip="never", n_xcd=8),
+    "s2-only": dict(perm="s2-only", n_xcd=8),
+    "random": dict(perm="random", n_xcd=8),
+}
+VARIANT_HELP = {
+    "reordered": "two-stage order (Stage 1 polar sort + Stage 2 bucket sort), work-balanced XCD segments, "
+                 "one queue per XCD, skip never",
+    "natural": "identity order, one queue (plain slot order)",
+    "natural-xcd": "identity order, equal row-count XCD segments, one queue per XCD",
+    "reordered-1q": "two-stage order with one segment and chip-wide waves (8x the per-XCD wave), one queue",
+    "auto": "as reordered, with the adaptive skip rule",
+    "s1-only": "Stage-1 order only (no bucket sort), work-balanced XCD segments",
+    "s2-only": "identity order with the Stage-2 bucket sort only, equal row-count segments (built on the host)",
+    "random": "a seeded random order, equal row-count segments (built on the host)",
+}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="long-720p-401f", choices=sorted(CONFIGS))
+    ap.add_argument("--config", default="long-720p-401f", choices=sorted(ALL_CONFIGS))
     ap.add_argument("--variants", default="reordered,natural",
-                    help="comma list of: reordered (two-stage order, work-balanced XCD segments, skip never), "
-                         "natural (identity order, equal row-count XCD segments), auto (adaptive skip), "
-                         "naive (identity, plain dispatch order), reordered-rowseg (two-stage order, equal "
-                         "row-count segments), natural-balanced (identity order, work-balanced segments)")
+                    help="comma list of: " + "; ".join(f"{k}: {v}" for k, v in VARIANT_HELP.items()))
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -168,8 +250,18 @@ def main() -> int:
     ap.add_argument("--summarize-pmc", metavar="DIR", help="summarize rocprofv3 counter passes found in DIR "
                     "into profiles/attn_traffic.json and a markdown table (no GPU needed)")
     ap.add_argument("--pmc-command", default="", help="command line recorded in the counter summary")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("STATS_CSV", "BENCH_JSON"),
+                    help="summarize a rocprofv3 --kernel-trace --stats run of bench.py into profiles/ (no GPU needed)")
+    ap.add_argument("--trace-command", default="", help="command line recorded in the trace summary")
     args = ap.parse_args()
 
+    if args.summarize_trace:
+        stats_csv, bench_json = args.summarize_trace
+        with open(bench_json) as f:
+            cfg = json.loads([ln for ln in f.read().splitlines() if ln.startswith("{")][-1])["config"]
+        md = os.path.join(ROOT, "profiles", f"attn_fwd_{cfg['workload']}_{cfg['variant']}_kernel_trace.md")
+        summarize_trace(stats_csv, bench_json, md, args.trace_command)
+        return 0
     if args.summarize_pmc:
         md = os.path.join(ROOT, "profiles", f"attn_fwd_{args.config}_counters.md")
         summarize_pmc(args.summarize_pmc, args.config, TRAFFIC_FILE, md, args.pmc_command)
@@ -193,7 +285,7 @@ def main() -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
         return 0
-    wl = CONFIGS[args.config]
+    wl = ALL_CONFIGS[args.config]
     t0 = time.perf_counter()
     mask = make_mask(wl, threads=16)
     q, k, v = make_qkv(wl, threads=16)
@@ -214,31 +306,52 @@ def main() -> int:
     col_idx = torch.empty((b_ * h_ * mb * mb,), dtype=torch.int32, device="cuda")
     o = torch.empty_like(qd)
     flags = torch.empty((b_, h_), dtype=torch.uint8, device="cuda")
-    seg = torch.empty((b_, h_, 9), dtype=torch.int32, device="cuda")
     attn_ws = torch.empty(W.attn_workspace_size(shape), dtype=torch.uint8, device="cuda")
     wave = W.wave_size(wl.head_dim, wl.block)
     stream = torch.cuda.current_stream()
     log(f"uploaded; nnz={nnz} density={nnz / (b_ * h_ * mb * mb):.4f} wave_per_xcd={wave}")
 
+    rng = np.random.default_rng(12345)
+    row_nnz = mask.reshape(b_ * h_, mb, mb).sum(axis=2, dtype=np.int64)
+
+    def host_perm(kind):
+        """Ablation orders built once on the host (not part of the timed step)."""
+        out = np.empty((b_ * h_, mb), dtype=np.int32)
+        for hh in range(b_ * h_):
+            if kind == "random":
+                out[hh] = rng.permutation(mb)
+            else:  # s2-only: identity order, buckets of `wave` rows per XCD segment sorted by descending n_i
+                base, extra = divmod(mb, 8)
+                starts = [x * base + min(x, extra) for x in range(9)]
+                order = []
+                for x in range(8):
+                    for s0 in range(starts[x], starts[x + 1], wave):
+                        rows = np.arange(s0, min(s0 + wave, starts[x + 1]))
+                        order.extend(rows[np.argsort(-row_nnz[hh, rows], kind="stable")])
+                out[hh] = order
+        return torch.from_numpy(out).cuda().reshape(b_, h_, mb)
+
     def make_step(variant):
-        skip = {"reordered": "never", "auto": "auto", "reordered-rowseg": "never",
-                "natural-balanced": "always"}.get(variant)
-        n_xcd = 1 if variant == "naive" else 8
-        use_seg = variant in ("reordered", "auto", "natural-balanced")
+        spec = VARIANTS[variant]
+        fixed = host_perm(spec["perm"]) if spec["perm"] in ("random", "s2-only") else None
+        n_xcd = spec["n_xcd"]
+        s1 = torch.empty((b_, h_, mb), dtype=torch.int32, device="cuda") if spec["perm"] == "stage1" else None
+        seg_q = torch.empty((b_, h_, n_xcd + 1), dtype=torch.int32, device="cuda")
 
         def step(ev=None):
-            p = None
-            if skip is not None:
+            p, sg = fixed, None
+            if spec["perm"] in ("two-stage", "stage1"):
                 W.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
-                                    wave=wave, n_xcd=8, skip=skip, workspace=perm_ws, out=perm, flags_out=flags,
-                                    seg_out=seg)
-                p = perm
+                                    wave=wave * spec.get("wave_mult", 1), n_xcd=n_xcd, skip=spec["skip"],
+                                    workspace=perm_ws, out=perm, flags_out=flags, seg_out=seg_q,
+                                    stage1_out=s1)
+                p = s1 if s1 is not None else perm
+                sg = seg_q
             rp, ci = W.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
                                     row_ptr=row_ptr, col_idx=col_idx)
             if ev is not None:
                 ev[0].record(stream)
-            W.sparse_attn_csr(qd, kd, vd, rp, ci, p, seg if use_seg else None, block=wl.block, n_xcd=n_xcd,
-                              out=o, workspace=attn_ws)
+            W.sparse_attn_csr(qd, kd, vd, rp, ci, p, sg, block=wl.block, n_xcd=n_xcd, out=o, workspace=attn_ws)
             if ev is not None:
                 ev[1].record(stream)
         return step

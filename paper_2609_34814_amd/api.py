@@ -96,9 +96,10 @@ def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim:
                       n_xcd: int = 8, iters: int = 10, seed: int = 0, skip: str = "auto",
                       profile: Optional[L.WaSkipProfile] = None, workspace: Optional[torch.Tensor] = None,
                       return_info: bool = False, out: Optional[torch.Tensor] = None,
-                      flags_out: Optional[torch.Tensor] = None, seg_out: Optional[torch.Tensor] = None):
+                      flags_out: Optional[torch.Tensor] = None, seg_out: Optional[torch.Tensor] = None,
+                      stage1_out: Optional[torch.Tensor] = None):
     """(perm int32 [B][H][M_B], seg_start int32 [B][H][n_xcd+1], head flags uint8 [B][H])
-    (plus embedding and Stage-1 order if asked)."""
+    (plus embedding and Stage-1 order if asked; stage1_out, if given, receives the Stage-1 order)."""
     lib = L.load()
     mask = _mask_u8(mask)
     b, h, mb, nb = mask.shape
@@ -108,7 +109,7 @@ def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim:
     flags = torch.empty((b, h), dtype=torch.uint8, device=dev) if flags_out is None else flags_out
     seg = torch.empty((b, h, n_xcd + 1), dtype=torch.int32, device=dev) if seg_out is None else seg_out
     emb = torch.empty((b, h, mb, 2), dtype=torch.int32, device=dev) if return_info else None
-    s1 = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if return_info else None
+    s1 = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if return_info and stage1_out is None else stage1_out
     params = L.WaPermParams(0 if wave is None else int(wave), int(n_xcd), int(iters), _SKIP[skip],
                             int(seed) & ((1 << 64) - 1),
                             ctypes.pointer(profile) if profile is not None else None)

@@ -1,7 +1,7 @@
 """Seeded synthetic workloads (inputs only; no arithmetic of the method)."""
-from .gen import (CONFIGS, CONFIG_ORDER, Workload, custom, make_mask, make_mask_head, make_qkv,
+from .gen import (ALL_CONFIGS, CONFIGS, CONFIG_ORDER, EXTRA_CONFIGS, Workload, custom, make_mask, make_mask_head, make_qkv,
                   make_tensor, bf16_bits_to_f32, block_centres, with_seed,
                   STREAM_Q, STREAM_K, STREAM_V)
 
-__all__ = ["CONFIGS", "CONFIG_ORDER", "Workload", "custom", "make_mask", "make_mask_head", "make_qkv",
+__all__ = ["ALL_CONFIGS", "CONFIGS", "CONFIG_ORDER", "EXTRA_CONFIGS", "Workload", "custom", "make_mask", "make_mask_head", "make_qkv",
            "make_tensor", "bf16_bits_to_f32", "block_centres", "with_seed", "STREAM_Q", "STREAM_K", "STREAM_V"]

@@ -124,6 +124,17 @@ CONFIGS = {
 }
 CONFIG_ORDER = ["tiny", "wan1.3b-480p-81f", "wan14b-720p-81f", "long-720p-401f", "skip-d64"]
 
+# An additional workload with the shapes of the 401-frame one: half of the heads are "spatial"
+# (the count rule above), half are "temporal", keeping the blocks at (about) the same in-frame
+# position in every frame plus scattered globals. Temporal heads are where raster order puts rows
+# that share no K/V block next to each other (Sec. III-C, root cause 1).
+EXTRA_CONFIGS = {
+    "long-720p-401f-mixed": Workload("long-720p-401f-mixed", 1, 40, 128, 128, (101, 45, 80), 1006,
+                                     _rules((0, 20, dict(kind="count", rho_lo=0.05, rho_hi=0.05, sigma=0.8, g=8)),
+                                            (20, 40, dict(kind="radius", rt=101, rs=0.5, g=8)))),
+}
+ALL_CONFIGS = {**CONFIGS, **EXTRA_CONFIGS}
+
 
 def custom(name: str, *, batch=1, heads=2, head_dim=64, block=64, grid=(2, 16, 16), seed=7,
            rule=None, seq_len=None) -> Workload:
