@@ -159,9 +159,10 @@ wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* r
                           void* stream);
 
 /* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters
- * and per-queue prefix tables, (64 + 64 * (B*H + 1)) int32 rounded up to 256 bytes)
- * followed by the compacted lists. The scheduler part alone (the leading part)
- * suffices for wa_sparse_attn_csr. Calls that share a workspace must not overlap. */
+ * and per-queue prefix tables, (64 + 64 * (B*H + 1)) int32 rounded up to 256 bytes),
+ * a zero-padded transposed copy of V (bf16 [B][H][head_dim][M_B*block], rounded up
+ * to 256 bytes), then the compacted lists. The first two parts (the leading part)
+ * suffice for wa_sparse_attn_csr. Calls that share a workspace must not overlap. */
 wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Block-sparse attention forward: for every query block i and token q in it,
@@ -190,8 +191,7 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
 
 /* As wa_sparse_attn, from lists already built by wa_compact_mask (row i of head
  * (b,h) visits col_idx[(b*H+h)*M_B*N_B + row_ptr[b][h][i] ...] in list order).
- * workspace >= the scheduler part of wa_attn_workspace_size ((64 + 64 * (B*H + 1)) int32,
- * rounded up to 256 bytes), 256-byte aligned. */
+ * workspace >= the scheduler and V^T parts of wa_attn_workspace_size, 256-byte aligned. */
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                              const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
                              const wa_shape* shape,

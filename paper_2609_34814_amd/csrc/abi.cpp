@@ -88,12 +88,15 @@ PermWs perm_ws_layout(const Dims& d) {
   return w;
 }
 
-// Attention workspace: [scheduler state][row_ptr][col_idx]; the CSR entry point uses only the
-// scheduler part, sized for the largest n_xcd.
+// Attention workspace: [scheduler state][V^T copy][row_ptr][col_idx]; the CSR entry point uses the
+// first two parts. The scheduler part is sized for the largest n_xcd.
 constexpr int kMaxXcd = 64;
 size_t attn_sched_bytes(const Dims& d) { return align_up(wa::sched_ints(d.bh, kMaxXcd) * 4); }
+size_t attn_csr_ws_bytes(const Dims& d) {
+  return attn_sched_bytes(d) + align_up(wa_vt_bytes(d.bh, d.mb, d.d, d.blk));
+}
 size_t attn_ws_bytes(const Dims& d) {
-  return attn_sched_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4) + align_up((size_t)d.bh * d.mb * d.mb * 4);
+  return attn_csr_ws_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4) + align_up((size_t)d.bh * d.mb * d.mb * 4);
 }
 
 wa_status check_ws(void* ws, size_t have, size_t need) {
@@ -132,11 +135,13 @@ wa_status launch_compact(const uint8_t* mask, const Dims& d, int32_t* row_ptr, i
   return WA_OK;
 }
 
-wa_status launch_attn(const void* q, const void* k, const void* v, void* sched, const int32_t* row_ptr,
+wa_status launch_attn(const void* q, const void* k, const void* v, void* ws, const int32_t* row_ptr,
                       const int32_t* col_idx, const int32_t* perm, const int32_t* seg, const Dims& d, float scale,
                       int32_t n_xcd, void* o, float* lse, hipStream_t st) {
   WaAttnLaunch a{};
-  a.q = q; a.k = k; a.v = v; a.sched = (int32_t*)sched;
+  a.q = q; a.k = k; a.v = v;
+  a.sched = (int32_t*)ws;
+  a.vt = (char*)ws + attn_sched_bytes(d);
   a.row_ptr = row_ptr; a.col_idx = col_idx; a.perm = perm; a.seg = seg;
   a.o = o; a.lse = lse;
   a.bh = (int32_t)d.bh; a.seq_len = d.n; a.mb = d.mb; a.head_dim = d.d; a.block = d.blk; a.n_xcd = n_xcd;
@@ -315,8 +320,8 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
   if (s != WA_OK) return s;
   hipStream_t st = (hipStream_t)stream;
   char* base = (char*)workspace;
-  int32_t* row_ptr = (int32_t*)(base + attn_sched_bytes(d));
-  int32_t* col_idx = (int32_t*)(base + attn_sched_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4));
+  int32_t* row_ptr = (int32_t*)(base + attn_csr_ws_bytes(d));
+  int32_t* col_idx = (int32_t*)(base + attn_csr_ws_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4));
   s = launch_compact(mask, d, row_ptr, col_idx, st);
   if (s != WA_OK) return s;
   s = launch_attn(q, k, v, base, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, o, lse, st);
@@ -336,7 +341,7 @@ wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const 
   if (s != WA_OK) return s;
   if (!row_ptr || !col_idx) return fail(WA_ERR_INVALID_ARG, "row_ptr and col_idx must be non-null");
   if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
-  s = check_ws(workspace, workspace_bytes, attn_sched_bytes(d));
+  s = check_ws(workspace, workspace_bytes, attn_csr_ws_bytes(d));
   if (s != WA_OK) return s;
   s = launch_attn(q, k, v, workspace, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, o, lse,
                   (hipStream_t)stream);

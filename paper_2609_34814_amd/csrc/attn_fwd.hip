@@ -5,10 +5,10 @@
 // and partial O kept on chip). The workgroup has BLK/32 wavefronts; wavefront w
 // owns query rows [32w, 32w+32) of the block. Two workgroups share a CU.
 //
-// Data movement. K_j and V_j (both in their natural [token][d] layout) are
-// copied from global memory straight into LDS with global_load_lds_dwordx4 (no
-// register staging; rows past the end of the sequence are clamped to the last
-// row and masked). Only explicit vmcnt waits order these copies against LDS
+// Data movement. K_j (natural [token][d] layout) and V_j^T (from a transposed,
+// zero-padded [d][N_pad] copy of V made once per call) are copied from global
+// memory straight into LDS with global_load_lds_dwordx4 (no register staging;
+// K rows past the end of the sequence are clamped to the last row and masked). Only explicit vmcnt waits order these copies against LDS
 // reads, so the copy into one tile stays in flight while the other tile is read.
 // The LDS tiles are XOR-swizzled at 16-byte granularity so that the MFMA operand
 // reads are free of bank conflicts; the swizzle is applied by choosing each
@@ -24,8 +24,10 @@
 //     keys of one query (lane mod 32): the softmax max and sum are lane-local plus
 //     one exchange with lane^32, and
 //   * P^T in bf16 is the B operand of O^T += V^T P^T directly from those
-//     registers; the matching A operand (8 keys of one column of V) is gathered
-//     from the row-major V tile with two transposing LDS reads (ds_read_b64_tr_b16).
+//     registers; the matching A operand is one 16-byte row chunk of V^T (8 keys
+//     of one d), so every operand read is one ds_read_b128. (Reading V in its
+//     natural layout with ds_read_b64_tr_b16 moves half the bytes per LDS cycle,
+//     and LDS bandwidth, not the MFMA rate, bounds this kernel.)
 //   * O^T rows use the same permutation, so each lane finally holds 8 consecutive
 //     output columns and O is written with 16-byte stores at the block's original
 //     rows (the inverse permutation is fused into the store).
@@ -102,8 +104,9 @@ template <int D, int BLK>
 struct Cfg {
   static constexpr int NW = BLK / 32;
   static constexpr int NT = NW * 64;
-  static constexpr int RB = D * 2;        // K and V tile row bytes
-  static constexpr int TBYTES = BLK * RB;
+  static constexpr int RB = D * 2;        // K tile row bytes
+  static constexpr int VRB = BLK * 2;     // V^T tile row bytes (one row per d)
+  static constexpr int TBYTES = BLK * RB;  // K tile bytes = V^T tile bytes
   static constexpr int NK = TBYTES / (NT * 16);  // DMA instructions per thread and tile
   static constexpr int KT = BLK / 32;
   static constexpr int DT = D / 32;
@@ -138,11 +141,11 @@ struct Dma {
   // the swizzle's row period
   static constexpr bool kInvariant = (NW * RPI) % (V ? 4 : 16) == 0;
   __device__ static __forceinline__ int row(int i, int w, int lane) { return (i * NW + w) * RPI + lane / LPR; }
-  // per-lane source bytes relative to tile row (i*NW)*RPI
-  __device__ static __forceinline__ uint32_t lane_bytes(int i, int w, int lane) {
+  // per-lane source bytes relative to tile row (i*NW)*RPI, for source rows `stride` bytes apart
+  __device__ static __forceinline__ uint32_t lane_bytes(int i, int w, int lane, uint32_t stride = RB) {
     const int r0 = w * RPI + lane / LPR;
     const int rs = kInvariant ? r0 : row(i, w, lane);
-    return (uint32_t)r0 * RB + (uint32_t)(swz<RB, V>(rs, lane % LPR) * 16);
+    return (uint32_t)r0 * stride + (uint32_t)(swz<RB, V>(rs, lane % LPR) * 16);
   }
 };
 
@@ -170,12 +173,17 @@ __device__ __forceinline__ void issue_tile(unsigned char* tile, const unsigned c
   }
 }
 
-// Transposing LDS read (gfx950 ds_read_b64_tr_b16): within each group of 16 lanes, lane i receives
-// element (i mod 4) of the 8-byte chunks addressed by lanes 4e + i/4 of the group, e = 0..3.
-__device__ __forceinline__ uint2 lds_read_tr(const unsigned char* p) {
-  typedef short v4s __attribute__((ext_vector_type(4)));
-  const v4s r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(lds_void_t*)p);
-  return __builtin_bit_cast(uint2, r);
+// DMA of the V^T tile: rows d of the transposed copy (row stride row_bytes), keys [key0, key0 + BLK),
+// into a tile with the K-tile swizzle (rows of VRB bytes, read one row chunk per lane).
+template <int D, int BLK>
+__device__ __forceinline__ void issue_vt(unsigned char* tile, const unsigned char* vtg, uint32_t row_bytes, int key0,
+                                         int w, int lane) {
+  using C = Cfg<D, BLK>;
+  using G = Dma<C::VRB, C::NW, false>;
+#pragma unroll
+  for (int i = 0; i < C::NK; ++i)
+    dma16(vtg + (int64_t)key0 * 2 + (int64_t)(i * C::NW * G::RPI) * row_bytes, G::lane_bytes(i, w, lane, row_bytes),
+          tile + (i * C::NW + w) * 1024);
 }
 
 // Next task of this workgroup: slot of a head from the queue of its XCD, else from the others.
@@ -219,17 +227,6 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
   const int hf = lane >> 5;
   const int n = a.seq_len;
   const float c2 = a.scale * kLog2e;
-  const int krow_lane = 16 * (l32 >> 4) + perm16(l32 & 15);  // K tile row supplied by this lane in a 32-row group
-
-  // V tile addressing of the transposing reads (see lds_read_tr): lane (e, q) = ((lane mod 16) / 4,
-  // lane mod 4) of 16-lane group G = lane / 16 supplies row 8 (G / 2) + e (+ 32 kt + 16 k2 + 4 half)
-  // and columns 32 dt + 16 (G mod 2) + {0, 8, 4, 12}[q] .. +3, which are the O^T rows perm16 puts there.
-  const int ve = (lane & 15) >> 2, vq = lane & 3, vg = lane >> 4;
-  const unsigned char* v_lane = v_lds + (8 * (vg >> 1) + ve) * C::RB + 8 * (vq >> 1);
-  uint32_t v_chunk[C::DT];
-#pragma unroll
-  for (int dt = 0; dt < C::DT; ++dt)
-    v_chunk[dt] = 16u * (uint32_t)swz_v<C::RB>(ve, 4 * dt + 2 * (vg & 1) + (vq & 1));
 
   const int home = (int)(__builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 0xF) % a.n_xcd;
 
@@ -250,7 +247,9 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
 
     const uint16_t* qg = (const uint16_t*)a.q + (int64_t)bh * n * D;
     const unsigned char* kg = (const unsigned char*)a.k + (int64_t)bh * n * D * 2;
-    const unsigned char* vg_ = (const unsigned char*)a.v + (int64_t)bh * n * D * 2;
+    const int64_t npad = (int64_t)a.mb * BLK;
+    const unsigned char* vtg = (const unsigned char*)a.vt + (int64_t)bh * D * npad * 2;
+    const uint32_t vt_row_bytes = (uint32_t)(npad * 2);
 
     const int32_t* rp = a.row_ptr + (int64_t)bh * (a.mb + 1);
     const int beg = rp[row];
@@ -274,7 +273,7 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       j_cur = cols[beg];
       if ((unsigned)j_cur >= (unsigned)a.mb) j_cur = 0;
       issue_tile<D, BLK, false>(k_lds, kg, j_cur * BLK, n, w, lane);
-      issue_tile<D, BLK, true>(v_lds, vg_, j_cur * BLK, n, w, lane);
+      issue_vt<D, BLK>(v_lds, vtg, vt_row_bytes, j_cur * BLK, w, lane);
     }
     // the Q loads (issued first) are complete; the first tiles stay in flight
     WA_WAIT_VM(2 * C::NK);
@@ -294,6 +293,11 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     int e = beg;
     auto kv_block = [&](auto masked_tag) {
       constexpr bool MASKED = decltype(masked_tag)::value;
+      // Per-lane LDS and copy offsets are recomputed in every block from an opaque copy of the lane
+      // index: hoisted out of the loop they would hold ~36 registers that the operand reads need.
+      int lane_o = lane;
+      asm volatile("" : "+v"(lane_o));
+      const int krow_lane = 16 * ((lane_o & 31) >> 4) + perm16(lane_o & 15);
       const bool has_next = e + 1 < end;
       int j_next = 0;
       if (has_next) {
@@ -306,25 +310,39 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       WA_BARRIER();
 
       // ---- S^T = K_j Q^T ----
+      // consecutive MFMAs go to different accumulators (a chain on one accumulator would wait for
+      // each result), and the operand reads of k-step s+1 are in flight during the MFMAs of step s
       f32x16 sacc[C::KT];
 #pragma unroll
-      for (int kt = 0; kt < C::KT; ++kt) {
+      for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
         for (int v = 0; v < 16; ++v) sacc[kt][v] = 0.f;
-        const int krow = kt * 32 + krow_lane;
+      {
+        uint4 a_cur[C::KT], a_nxt[C::KT];
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = lds_chunk<C::RB>(k_lds, kt * 32 + krow_lane, hf);
 #pragma unroll
         for (int s = 0; s < C::KS; ++s) {
-          const bf16x8 av = as_bf16x8(lds_chunk<C::RB>(k_lds, krow, 2 * s + hf));
-          sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[s], sacc[kt], 0, 0, 0);
+          if (s + 1 < C::KS) {
+#pragma unroll
+            for (int kt = 0; kt < C::KT; ++kt)
+              a_nxt[kt] = lds_chunk<C::RB>(k_lds, kt * 32 + krow_lane, 2 * (s + 1) + hf);
+          }
+#pragma unroll
+          for (int kt = 0; kt < C::KT; ++kt)
+            sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a_cur[kt]), qf[s], sacc[kt], 0, 0, 0);
+#pragma unroll
+          for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = a_nxt[kt];
         }
       }
       // every wavefront is done with K_j: start K_{j+1}
       WA_BARRIER();
-      if (has_next) issue_tile<D, BLK, false>(k_lds, kg, j_next * BLK, n, w, lane);
+      if (has_next) issue_tile<D, BLK, false>(k_lds, kg, j_next * BLK, n, w, lane_o);
 
       // ---- online softmax (log2 domain) ----
       if constexpr (MASKED) {
         const int nvalid = n - j_cur * BLK;
+        const int hf = lane_o >> 5;  // from the opaque lane copy: no key table held across blocks
 #pragma unroll
         for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
@@ -375,24 +393,30 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       WA_BARRIER();
 
       // ---- O^T += V_j^T P^T ----
+      {
+        // k-step ks = 2 kt + k2 (16 keys); operand reads of step ks+1 in flight during step ks
+        uint4 a_cur[C::DT], a_nxt[C::DT];
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt) {
+        for (int dt = 0; dt < C::DT; ++dt) a_cur[dt] = lds_chunk<C::VRB>(v_lds, dt * 32 + krow_lane, hf);
 #pragma unroll
-        for (int kt = 0; kt < C::KT; ++kt)
+        for (int ks = 0; ks < 2 * C::KT; ++ks) {
+          if (ks + 1 < 2 * C::KT) {
 #pragma unroll
-          for (int k2 = 0; k2 < 2; ++k2) {
-            const unsigned char* vp = v_lane + (32 * kt + 16 * k2) * C::RB + v_chunk[dt];
-            const uint2 lo = lds_read_tr(vp);
-            const uint2 hi = lds_read_tr(vp + 4 * C::RB);
-            const bf16x8 av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-            const uint32_t* p = &pb[kt][4 * k2];
-            const bf16x8 bv = as_bf16x8(make_uint4(p[0], p[1], p[2], p[3]));
-            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, oacc[dt], 0, 0, 0);
+            for (int dt = 0; dt < C::DT; ++dt)
+              a_nxt[dt] = lds_chunk<C::VRB>(v_lds, dt * 32 + krow_lane, 2 * (ks + 1) + hf);
           }
+          const uint32_t* p = &pb[ks >> 1][4 * (ks & 1)];
+          const bf16x8 bv = as_bf16x8(make_uint4(p[0], p[1], p[2], p[3]));
+#pragma unroll
+          for (int dt = 0; dt < C::DT; ++dt)
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a_cur[dt]), bv, oacc[dt], 0, 0, 0);
+#pragma unroll
+          for (int dt = 0; dt < C::DT; ++dt) a_cur[dt] = a_nxt[dt];
+        }
       }
       // every wavefront is done with V_j: start V_{j+1}
       WA_BARRIER();
-      if (has_next) issue_tile<D, BLK, true>(v_lds, vg_, j_next * BLK, n, w, lane);
+      if (has_next) issue_vt<D, BLK>(v_lds, vtg, vt_row_bytes, j_next * BLK, w, lane_o);
       j_cur = j_next;
     };
     const bool ragged_last = end > beg && (n % BLK) != 0 && cols[end - 1] == a.mb - 1;
@@ -439,6 +463,42 @@ __global__ __launch_bounds__(64) void sched_kernel(int32_t* sched, const int32_t
   }
 }
 
+// V [bh][n][D] -> V^T [bh][D][npad], zero for keys >= n. One 64-key x 64-column tile per workgroup,
+// 16-byte loads and stores, transposed through LDS.
+template <int D>
+__global__ __launch_bounds__(256) void transpose_v_kernel(const uint16_t* __restrict__ v, uint16_t* __restrict__ vt,
+                                                         int n, int64_t npad, int tiles_n) {
+  __shared__ uint16_t t[64][64 + 8];
+  const int tile = blockIdx.x % tiles_n;
+  const int dtile = (blockIdx.x / tiles_n) % (D / 64);
+  const int64_t bh = blockIdx.x / ((int64_t)tiles_n * (D / 64));
+  const int key0 = tile * 64, d0 = dtile * 64;
+  const uint16_t* src = v + bh * n * D;
+  uint16_t* dst = vt + bh * D * npad;
+  const int tid = threadIdx.x;
+  // load: thread -> (key r, 8-column group c8), two passes of 32 keys
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int r = pass * 32 + tid / 8, c8 = tid % 8;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (key0 + r < n) val = *(const uint4*)(src + (int64_t)(key0 + r) * D + d0 + c8 * 8);
+    const uint32_t wv[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[r][c8 * 8 + e] = (uint16_t)(wv[e >> 1] >> ((e & 1) * 16));
+  }
+  __syncthreads();
+  // store: thread -> (column d, 8-key group k8), two passes of 32 columns
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int d = pass * 32 + tid / 8, k8 = tid % 8;
+    uint32_t wv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      wv[e] = (uint32_t)t[k8 * 8 + 2 * e][d] | ((uint32_t)t[k8 * 8 + 2 * e + 1][d] << 16);
+    *(uint4*)(dst + (int64_t)(d0 + d) * npad + key0 + k8 * 8) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+  }
+}
+
 int resident_cus() {
   static int cached[64];
   int dev = 0;
@@ -456,6 +516,15 @@ hipError_t launch_t(const WaAttnLaunch& a, hipStream_t stream) {
   hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(64), 0, stream, a.sched, a.seg, a.bh, a.mb, a.n_xcd);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int64_t npad = (int64_t)a.mb * BLK;
+  const int tiles_n = (int)((npad + 63) / 64);
+  const int64_t tgrid = (int64_t)a.bh * (D / 64) * tiles_n;
+  if (tgrid > 0) {
+    hipLaunchKernelGGL((transpose_v_kernel<D>), dim3((unsigned)tgrid), dim3(256), 0, stream, (const uint16_t*)a.v,
+                       (uint16_t*)a.vt, a.seq_len, npad, tiles_n);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const int64_t tasks = (int64_t)a.bh * a.mb;
   if (tasks <= 0) return hipSuccess;
   int occ = 0;
@@ -472,6 +541,10 @@ hipError_t occ_t(int* n) {
 }
 
 }  // namespace
+
+size_t wa_vt_bytes(int64_t bh, int mb, int head_dim, int block) {
+  return (size_t)bh * head_dim * (size_t)mb * block * 2;
+}
 
 hipError_t wa_launch_attention(const WaAttnLaunch& a, hipStream_t stream) {
   if (a.head_dim == 128 && a.block == 128) return launch_t<128, 128>(a, stream);

@@ -36,6 +36,7 @@ struct WaAttnLaunch {
   const void* q;
   const void* k;
   const void* v;
+  void* vt;          // workspace: V transposed to [bh][head_dim][mb*block], zero-padded
   int32_t* sched;    // workspace: sched_ints(bh, n_xcd) int32 (counters at [0, n_xcd), prefix table at 64)
   const int32_t* row_ptr;
   const int32_t* col_idx;
@@ -54,6 +55,7 @@ struct WaAttnLaunch {
 
 hipError_t wa_launch_attention(const WaAttnLaunch& a, hipStream_t stream);
 hipError_t wa_attention_occupancy(int head_dim, int block, int* wgs_per_cu);
+size_t wa_vt_bytes(int64_t bh, int mb, int head_dim, int block);
 
 hipError_t wa_launch_row_count(const uint8_t* mask, int64_t rows, int n, int32_t* counts, int64_t count_stride_rows,
                                int counts_offset, int mb, hipStream_t stream);
