@@ -67,14 +67,14 @@ typedef struct wa_shape {
 
 /* Offline-profile constants of the adaptive skip (Sec. IV-E). A head keeps the
  * identity order when any case fires (skip_mode = WA_SKIP_AUTO):
- *   1  distinct_kv_blocks * kv_block_bytes <= l2_bytes_per_xcd        (fits in L2)
+ *   1  distinct_kv_blocks * kv_block_bytes <= cache_bytes             (fits in cache)
  *   2  nnz * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row * M_B
  *                                 + ovh_ns_per_nnz * nnz                (too little work)
  *   3  sum_i |M_i & M_i+1| / sum_i |M_i | M_i+1| >= j_max              (already local)
  *   4  (lambda_1 + lambda_2) / ||M~||_F^2 < eta_min                      (no rank-2 structure)
  * Each comparison is one fixed sequence of IEEE fp64 operations. */
 typedef struct wa_skip_profile {
-  double l2_bytes_per_xcd;
+  double cache_bytes;
   double gain_ns_per_block;
   double ovh_ns_fixed;
   double ovh_ns_per_row;
@@ -87,7 +87,7 @@ enum { WA_SKIP_AUTO = 0, WA_SKIP_NEVER = 1, WA_SKIP_ALWAYS = 2 };
 
 /* head_flags bits written by wa_build_permutation */
 enum {
-  WA_FLAG_FITS_L2 = 1,
+  WA_FLAG_FITS_CACHE = 1,
   WA_FLAG_LITTLE_WORK = 2,
   WA_FLAG_LOCAL = 4,
   WA_FLAG_UNSTRUCTURED = 8,

@@ -15,7 +15,7 @@ WA_ERR_WORKSPACE = -4
 WA_ERR_HIP = -6
 
 WA_SKIP_AUTO, WA_SKIP_NEVER, WA_SKIP_ALWAYS = 0, 1, 2
-FLAG_FITS_L2, FLAG_LITTLE_WORK, FLAG_LOCAL, FLAG_UNSTRUCTURED, FLAG_DEGENERATE, FLAG_IDENTITY = 1, 2, 4, 8, 16, 64
+FLAG_FITS_CACHE, FLAG_LITTLE_WORK, FLAG_LOCAL, FLAG_UNSTRUCTURED, FLAG_DEGENERATE, FLAG_IDENTITY = 1, 2, 4, 8, 16, 64
 
 
 class WaShape(ctypes.Structure):
@@ -24,7 +24,7 @@ class WaShape(ctypes.Structure):
 
 
 class WaSkipProfile(ctypes.Structure):
-    _fields_ = [("l2_bytes_per_xcd", c_double), ("gain_ns_per_block", c_double), ("ovh_ns_fixed", c_double),
+    _fields_ = [("cache_bytes", c_double), ("gain_ns_per_block", c_double), ("ovh_ns_fixed", c_double),
                 ("ovh_ns_per_row", c_double), ("ovh_ns_per_nnz", c_double), ("j_max", c_double),
                 ("eta_min", c_double)]
 

@@ -108,13 +108,13 @@ wa_status check_ws(void* ws, size_t have, size_t need) {
 }
 
 const wa_skip_profile kDefaultProfile = {
-    4.0 * 1024.0 * 1024.0,  // l2_bytes_per_xcd: MI355X L2 per XCD
-    1.0,                    // gain_ns_per_block
-    2000.0,                 // ovh_ns_fixed
-    2.0,                    // ovh_ns_per_row
-    0.05,                   // ovh_ns_per_nnz
-    0.75,                   // j_max
-    0.05,                   // eta_min
+    256.0 * 1024.0 * 1024.0,  // cache_bytes: MI355X shared last-level cache (behind the per-XCD L2s)
+    1.0,                      // gain_ns_per_block
+    2000.0,                   // ovh_ns_fixed
+    2.0,                      // ovh_ns_per_row
+    0.05,                     // ovh_ns_per_nnz
+    0.75,                     // j_max
+    0.05,                     // eta_min
 };
 
 wa_status check_attn_common(const void* q, const void* k, const void* v, void* o, int32_t n_xcd) {

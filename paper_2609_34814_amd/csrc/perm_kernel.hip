@@ -34,7 +34,7 @@ constexpr int NT = 1024;
 constexpr int NWAVE = NT / 64;
 constexpr int MAXB = 4096;
 
-constexpr int FLAG_FITS_L2 = 1, FLAG_LITTLE_WORK = 2, FLAG_LOCAL = 4, FLAG_UNSTRUCTURED = 8, FLAG_DEGENERATE = 16,
+constexpr int FLAG_FITS_CACHE = 1, FLAG_LITTLE_WORK = 2, FLAG_LOCAL = 4, FLAG_UNSTRUCTURED = 8, FLAG_DEGENERATE = 16,
               FLAG_IDENTITY = 64;
 constexpr int SKIP_AUTO = 0, SKIP_ALWAYS = 2;
 
@@ -388,7 +388,7 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
   if (tid == 0) {
     int f = 0;
     const double kvb = (double)(2 * a.block * a.head_dim * 2);
-    if ((double)distinct * kvb <= a.prof.l2_bytes_per_xcd) f |= FLAG_FITS_L2;
+    if ((double)distinct * kvb <= a.prof.cache_bytes) f |= FLAG_FITS_CACHE;
     const double saving = (double)nnz * a.prof.gain_ns_per_block;
     const double cost = a.prof.ovh_ns_fixed + a.prof.ovh_ns_per_row * (double)m + a.prof.ovh_ns_per_nnz * (double)nnz;
     if (saving < cost) f |= FLAG_LITTLE_WORK;

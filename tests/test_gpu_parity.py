@@ -33,7 +33,7 @@ def _w():
 
 def _profile_np_to_c(p: S.SkipProfile):
     from paper_2609_34814_amd import _lib
-    return _lib.WaSkipProfile(p.l2_bytes_per_xcd, p.gain_ns_per_block, p.ovh_ns_fixed, p.ovh_ns_per_row,
+    return _lib.WaSkipProfile(p.cache_bytes, p.gain_ns_per_block, p.ovh_ns_fixed, p.ovh_ns_per_row,
                               p.ovh_ns_per_nnz, p.j_max, p.eta_min)
 
 
@@ -148,19 +148,25 @@ def _perm_case(wl, mask, *, wave, n_xcd, mode, iters=10, seed=0, profile=None):
     return perm, flags
 
 
+# A 4 MiB cache keeps skip case 1 quiet on these workloads, so the later cases decide.
+_SMALL_CACHE = S.SkipProfile(cache_bytes=4 * 1024 * 1024)
+
+
 @pytest.mark.parametrize("name", ["tiny", "wan1.3b-480p-81f", "skip-d64", "ragged", "dense", "single", "diag"])
-@pytest.mark.parametrize("mode", [S.SKIP_NEVER, S.SKIP_AUTO])
-def test_permutation_bit_exact(name, mode):
+@pytest.mark.parametrize("mode,profile", [(S.SKIP_NEVER, None), (S.SKIP_AUTO, None), (S.SKIP_AUTO, _SMALL_CACHE)],
+                         ids=["never", "auto", "auto-small-cache"])
+def test_permutation_bit_exact(name, mode, profile):
     wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
     mask = make_mask(wl)
-    _perm_case(wl, mask, wave=64, n_xcd=8, mode=mode)
+    _perm_case(wl, mask, wave=64, n_xcd=8, mode=mode, profile=profile)
 
 
-@pytest.mark.parametrize("name,mode", [("wan14b-720p-81f", S.SKIP_NEVER), ("wan14b-720p-81f", S.SKIP_AUTO),
-                                       ("long-720p-401f", S.SKIP_NEVER)])
-def test_permutation_bit_exact_full_size(name, mode):
+@pytest.mark.parametrize("name,mode,profile", [("wan14b-720p-81f", S.SKIP_NEVER, None),
+                                               ("wan14b-720p-81f", S.SKIP_AUTO, _SMALL_CACHE),
+                                               ("long-720p-401f", S.SKIP_NEVER, None)])
+def test_permutation_bit_exact_full_size(name, mode, profile):
     wl = CONFIGS[name]
-    _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=mode)
+    _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=mode, profile=profile)
 
 
 @pytest.mark.parametrize("n_xcd,wave,seed", [(1, 132, 5), (2, 7, 99), (8, 1, 3)])

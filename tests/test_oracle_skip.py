@@ -50,9 +50,11 @@ def test_tier1_cases():
     prof = S.SkipProfile()
     tiny = make_mask_head(CONFIGS["tiny"], 0, 0)
     f = S.tier1_flags(S.head_stats(tiny), prof, 64, 64)
-    assert f & S.FLAG_FITS_L2          # 64 KV blocks of 16 KiB = 1 MiB < 4 MiB
-    big = make_mask_head(CONFIGS["wan14b-720p-81f"], 0, 0)
-    assert S.tier1_flags(S.head_stats(big), prof, 128, 128) == 0
+    assert f & S.FLAG_FITS_CACHE          # 64 KV blocks of 16 KiB = 1 MiB < 256 MiB
+    big = S.head_stats(make_mask_head(CONFIGS["wan14b-720p-81f"], 0, 0))
+    # 591 KV blocks of 64 KiB = 37 MiB: inside the shared last-level cache, not inside one 4 MiB L2
+    assert S.tier1_flags(big, prof, 128, 128) == S.FLAG_FITS_CACHE
+    assert S.tier1_flags(big, S.SkipProfile(cache_bytes=4 * 1024 * 1024), 128, 128) == 0
     # already local: every row equal to its neighbour except one column
     band = np.zeros((100, 100), dtype=np.uint8)
     for i in range(100):
@@ -61,12 +63,12 @@ def test_tier1_cases():
     # little work: a nearly empty mask
     sparse = np.eye(300, dtype=np.uint8)
     assert S.tier1_flags(S.head_stats(sparse), prof, 128, 128) & S.FLAG_LITTLE_WORK
-    # boundary of case 1 is inclusive: exactly one L2 of distinct blocks fits
+    # boundary of case 1 is inclusive: exactly one cache of distinct blocks fits
     st = S.head_stats(np.eye(128, dtype=np.uint8))
-    exact = S.SkipProfile(l2_bytes_per_xcd=128 * S.kv_block_bytes(128, 128))
-    assert S.tier1_flags(st, exact, 128, 128) & S.FLAG_FITS_L2
-    below = S.SkipProfile(l2_bytes_per_xcd=128 * S.kv_block_bytes(128, 128) - 1)
-    assert not (S.tier1_flags(st, below, 128, 128) & S.FLAG_FITS_L2)
+    exact = S.SkipProfile(cache_bytes=128 * S.kv_block_bytes(128, 128))
+    assert S.tier1_flags(st, exact, 128, 128) & S.FLAG_FITS_CACHE
+    below = S.SkipProfile(cache_bytes=128 * S.kv_block_bytes(128, 128) - 1)
+    assert not (S.tier1_flags(st, below, 128, 128) & S.FLAG_FITS_CACHE)
 
 
 def test_driver_modes():
@@ -80,10 +82,15 @@ def test_driver_modes():
         ref, _ = P.two_stage_permutation(mask[0, h], seed=0, flat_head=h, wave=64, n_xcd=8, iters=10)
         assert np.array_equal(p_never[0, h], ref)
     assert not np.any(f_never & S.FLAG_IDENTITY)
-    p_auto, f_auto, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, **kw)
+    # a 4 MiB cache keeps case 1 quiet (11.6 MiB of K/V per head), so the later cases decide
+    small = S.SkipProfile(cache_bytes=4 * 1024 * 1024)
+    p_auto, f_auto, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, profile=small, **kw)
     # random heads: unstructured -> identity; locality heads: reordered
     assert f_auto[0, 0] & S.FLAG_UNSTRUCTURED and np.all(p_auto[0, 0] == np.arange(wl.mb))
     assert f_auto[0, 2] == 0 and np.array_equal(p_auto[0, 2], p_never[0, 2])
+    # default profile: every head's K/V fits the shared cache, so case 1 keeps the identity order
+    p_def, f_def, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, **kw)
+    assert np.all(f_def == S.FLAG_FITS_CACHE | S.FLAG_IDENTITY) and np.all(p_def == np.arange(wl.mb))
 
 
 def test_compaction_brute_force():
