@@ -49,7 +49,7 @@ def load_traffic(workload: str, variant: str):
     except (OSError, ValueError):
         return None
     entry = data.get(workload, {}).get(variant)
-    if not entry or entry.get("kernel_sha") != kernel_source_hash():
+    if not entry or entry.get("kernel_sha") != kernel_source_hash() or entry.get("variant_spec") != VARIANTS[variant]:
         return None
     return entry.get("hbm_bytes_per_launch")
 
@@ -127,7 +127,7 @@ def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_
         write = c["WRITE_SIZE"] * 1024.0 * f_write
         cycles = a["GRBM_GUI_ACTIVE"] / 8.0          # summed over the 8 XCDs
         busy = a["SQ_VALU_MFMA_BUSY_CYCLES"] / (256 * 4 * cycles)
-        entry[v] = {"kernel_sha": sha, "hbm_bytes_per_launch": fetch + write, "fetch_bytes": fetch,
+        entry[v] = {"kernel_sha": sha, "variant_spec": VARIANTS.get(v), "hbm_bytes_per_launch": fetch + write, "fetch_bytes": fetch,
                     "write_bytes": write, "l2_hit": hit, "dram_read_requests": c["TCC_EA0_RDREQ_DRAM_sum"],
                     "mfma_flop": a["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512, "mfma_busy": busy}
         lines.append(f"| {v} | {na} | {100 * hit:.2f} | {fetch / 1e9:.1f} | {write / 1e9:.2f} | "
@@ -210,29 +210,156 @@ def cpu_baseline(wl, q, k, v, mask, total_flop, budget_s: float):
     }
 
 
-# Row orders and queue layouts compared by the benchmark. "queues" is the kernel's n_xcd: 8 = one
-# task queue per XCD (segment x of every head runs on XCD x), 1 = one queue in slot order for the chip.
+# Row orders and queue layouts compared by the benchmark. n_xcd is the kernel's queue count and the
+# permutation's segment count: 1 = one queue in slot order for the whole chip, waves of W = resident
+# tasks per CU x CUs rows (Alg. 2 with the paper's W); 8 = one queue per XCD (segment x of every head
+# runs on XCD x), waves of W / 8 rows per segment.
 VARIANTS = {
-    "reordered": dict(perm="two-stage", skip="never", n_xcd=8),
+    "reordered": dict(perm="two-stage", skip="never", n_xcd=1, wave_mult=8),
     "natural": dict(perm=None, n_xcd=1),
+    "auto": dict(perm="two-stage", skip="auto", n_xcd=1, wave_mult=8),
+    "s1-only": dict(perm="stage1", skip="never", n_xcd=1, wave_mult=8),
+    "s2-only": dict(perm="s2-only", n_xcd=1, wave_mult=8),
+    "random": dict(perm="random", n_xcd=1),
+    "reordered-xcd": dict(perm="two-stage", skip="never", n_xcd=8),
     "natural-xcd": dict(perm=None, n_xcd=8),
-    "reordered-1q": dict(perm="two-stage", skip="never", n_xcd=1, wave_mult=8),
-    "auto": dict(perm="two-stage", skip="auto", n_xcd=8),
-    "s1-only": dict(perm="stage1", skip="never", n_xcd=8),
-    "s2-only": dict(perm="s2-only", n_xcd=8),
-    "random": dict(perm="random", n_xcd=8),
 }
 VARIANT_HELP = {
-    "reordered": "two-stage order (Stage 1 polar sort + Stage 2 bucket sort), work-balanced XCD segments, "
-                 "one queue per XCD, skip never",
+    "reordered": "two-stage order (Stage 1 polar sort + Stage 2 bucket sort), chip-wide waves, one queue, "
+                 "skip never",
     "natural": "identity order, one queue (plain slot order)",
+    "auto": "as reordered, with the adaptive skip rule deciding per head",
+    "s1-only": "Stage-1 order only (no bucket sort), one queue",
+    "s2-only": "identity order with the Stage-2 bucket sort over chip-wide waves only (built on the host)",
+    "random": "a seeded random order, one queue (built on the host)",
+    "reordered-xcd": "two-stage order, work-balanced XCD segments, one queue per XCD, skip never",
     "natural-xcd": "identity order, equal row-count XCD segments, one queue per XCD",
-    "reordered-1q": "two-stage order with one segment and chip-wide waves (8x the per-XCD wave), one queue",
-    "auto": "as reordered, with the adaptive skip rule",
-    "s1-only": "Stage-1 order only (no bucket sort), work-balanced XCD segments",
-    "s2-only": "identity order with the Stage-2 bucket sort only, equal row-count segments (built on the host)",
-    "random": "a seeded random order, equal row-count segments (built on the host)",
 }
+
+
+FLAG_NAMES = ((1, "fits_cache"), (2, "little_work"), (4, "local"), (8, "unstructured"), (16, "degenerate"))
+
+
+def _median(xs):
+    return float(np.median(np.asarray(xs, dtype=np.float64)))
+
+
+def run_skip_sweep(args) -> int:
+    """Kernel-level latency with and without reordering (overhead included) over sequence length and
+    density, each repetition starting from a flushed L2 and last-level cache, and the decision the
+    adaptive skip rule takes at each point. One JSON line per point on stdout."""
+    import torch
+    import paper_2609_34814_amd as W
+    from workloads import skip_sweep_workloads
+
+    points = skip_sweep_workloads()
+    if args.sweep_points:
+        keep = [s.strip() for s in args.sweep_points.split(",") if s.strip()]
+        points = [p for p in points if any(s in p.name for s in keep)]
+    # 1 GiB, larger than the L2s and the last-level cache together. Each repetition READS it: a write
+    # would leave dirty lines whose write-back the next kernel would pay for.
+    flush = torch.zeros(1 << 28, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for wl in points:
+        t0 = time.perf_counter()
+        mask = make_mask(wl, threads=16)
+        b_, h_, mb, n, d, blk = wl.batch, wl.heads, wl.mb, wl.seq_len, wl.head_dim, wl.block
+        nnz = int(mask.sum(dtype=np.int64))
+        distinct = mask.any(axis=2).sum(axis=-1)
+        kv_mib = float(distinct.mean()) * 2 * blk * d * 2 / 2 ** 20
+        md = torch.from_numpy(mask).cuda()
+        del mask
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(wl.seed)
+        q, k, v = (torch.randn((b_, h_, n, d), generator=gen, device="cuda", dtype=torch.bfloat16) for _ in range(3))
+        shape = W.shape_of(b_, h_, n, d, blk)
+        perm_ws = torch.empty(W.perm_workspace_size(shape), dtype=torch.uint8, device="cuda")
+        attn_ws = torch.empty(W.attn_workspace_size(shape), dtype=torch.uint8, device="cuda")
+        perm = torch.empty((b_, h_, mb), dtype=torch.int32, device="cuda")
+        seg = torch.empty((b_, h_, 2), dtype=torch.int32, device="cuda")
+        flags = torch.empty((b_, h_), dtype=torch.uint8, device="cuda")
+        row_ptr = torch.empty((b_, h_, mb + 1), dtype=torch.int32, device="cuda")
+        col_idx = torch.empty((b_ * h_ * mb * mb,), dtype=torch.int32, device="cuda")
+        o = torch.empty_like(q)
+        wave = W.wave_size(d, blk) * 8
+        log(f"{wl.name}: N={n} M_B={mb} nnz={nnz} K/V per head {kv_mib:.1f} MiB "
+            f"(inputs {time.perf_counter() - t0:.1f} s)")
+
+        def step(variant, ev):
+            ev[0].record(stream)
+            p = sg = None
+            if variant != "natural":
+                W.build_permutation(md, seq_len=n, block=blk, head_dim=d, wave=wave, n_xcd=1,
+                                    skip="never" if variant == "reordered" else "auto", workspace=perm_ws,
+                                    out=perm, flags_out=flags, seg_out=seg)
+                p, sg = perm, seg
+            ev[1].record(stream)
+            rp, ci = W.compact_mask(md, seq_len=n, block=blk, head_dim=d, row_ptr=row_ptr, col_idx=col_idx)
+            ev[2].record(stream)
+            W.sparse_attn_csr(q, k, v, rp, ci, p, sg, block=blk, n_xcd=1, out=o, workspace=attn_ws)
+            ev[3].record(stream)
+
+        rec = {"point": wl.name, "frames": wl.grid[0], "seq_len": n, "mb": mb, "heads": h_,
+               "kind": "mixed" if "mixed" in wl.name else "spatial",
+               "rho": float(wl.name.rsplit("rho", 1)[1]), "density": nnz / (b_ * h_ * mb * mb), "nnz": nnz,
+               "kv_mib_per_head": kv_mib, "reps": args.sweep_reps}
+        for variant in ("natural", "reordered", "auto"):
+            times = {"step": [], "perm": [], "compact": [], "attn": []}
+            for r in range(1 + args.sweep_reps):
+                flush.sum()
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                step(variant, ev)
+                torch.cuda.synchronize()
+                if r == 0:
+                    continue  # warm-up
+                times["step"].append(ev[0].elapsed_time(ev[3]))
+                times["perm"].append(ev[0].elapsed_time(ev[1]))
+                times["compact"].append(ev[1].elapsed_time(ev[2]))
+                times["attn"].append(ev[2].elapsed_time(ev[3]))
+            rec[variant] = {key: _median(val) for key, val in times.items()}
+            if variant != "natural":
+                f = flags.cpu().numpy().reshape(-1)
+                rec[variant]["identity_heads"] = int(np.count_nonzero(f & 64))
+                if variant == "reordered":
+                    rec["cases"] = {name: int(np.count_nonzero(f & bit)) for bit, name in FLAG_NAMES}
+        rec["gain_step"] = rec["natural"]["step"] / rec["reordered"]["step"]
+        rec["gain_attn"] = rec["natural"]["attn"] / rec["reordered"]["attn"]
+        rec["auto_vs_best"] = rec["auto"]["step"] / min(rec["natural"]["step"], rec["reordered"]["step"])
+        log(f"  natural {rec['natural']['step']:.2f} ms, reordered {rec['reordered']['step']:.2f} ms "
+            f"(perm {rec['reordered']['perm']:.2f}), auto {rec['auto']['step']:.2f} ms with "
+            f"{rec['auto']['identity_heads']}/{h_} heads skipped; gain step {rec['gain_step']:.3f} "
+            f"attention {rec['gain_attn']:.3f}")
+        print(json.dumps(rec), flush=True)
+        del md, q, k, v, perm_ws, attn_ws, perm, seg, flags, row_ptr, col_idx, o
+        torch.cuda.empty_cache()
+    return 0
+
+
+def summarize_sweep(jsonl: str, out_md: str, command_note: str) -> None:
+    recs = []
+    with open(jsonl) as f:
+        for ln in f:
+            if ln.startswith("{"):
+                recs.append(json.loads(ln))
+    lines = ["# Adaptive skip sweep: kernel-level latency with and without reordering", "",
+             "Each figure is the median over the repetitions of one step (permutation, when built, + mask",
+             "compaction + attention call); every repetition starts after a 1 GiB read that evicts the L2s",
+             "and the last-level cache. `gain` = natural / reordered (> 1: reordering pays).",
+             "`skip cases` counts heads per case of the rule under the built-in profile (one head can",
+             "hit several); `auto` runs with the rule deciding per head.", "",
+             f"Command: `{command_note}`", "",
+             "| point | tokens | density | K/V per head MiB | natural ms | reordered ms (perm) | gain step | "
+             "gain attention | auto ms (heads skipped) | auto / best | skip cases |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in recs:
+        cases = ", ".join(f"{k} {v}" for k, v in r.get("cases", {}).items() if v)
+        lines.append(f"| {r['point']} | {r['seq_len']} | {r['density'] * 100:.1f}% | {r['kv_mib_per_head']:.1f} | "
+                     f"{r['natural']['step']:.2f} | {r['reordered']['step']:.2f} ({r['reordered']['perm']:.2f}) | "
+                     f"{r['gain_step']:.3f} | {r['gain_attn']:.3f} | {r['auto']['step']:.2f} "
+                     f"({r['auto']['identity_heads']}/{r['heads']}) | {r['auto_vs_best']:.3f} | {cases or '-'} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(out_md)
 
 
 def main() -> int:
@@ -253,7 +380,17 @@ def main() -> int:
     ap.add_argument("--summarize-trace", nargs=2, metavar=("STATS_CSV", "BENCH_JSON"),
                     help="summarize a rocprofv3 --kernel-trace --stats run of bench.py into profiles/ (no GPU needed)")
     ap.add_argument("--trace-command", default="", help="command line recorded in the trace summary")
+    ap.add_argument("--skip-sweep", action="store_true",
+                    help="time natural / reordered / auto over the sequence-length and density sweep (JSON lines)")
+    ap.add_argument("--sweep-points", default="", help="comma list of substrings selecting sweep points")
+    ap.add_argument("--sweep-reps", type=int, default=5)
+    ap.add_argument("--summarize-sweep", metavar="JSONL", help="write profiles/skip_sweep.md from a sweep's output")
+    ap.add_argument("--sweep-command", default="", help="command line recorded in the sweep summary")
     args = ap.parse_args()
+
+    if args.summarize_sweep:
+        summarize_sweep(args.summarize_sweep, os.path.join(ROOT, "profiles", "skip_sweep.md"), args.sweep_command)
+        return 0
 
     if args.summarize_trace:
         stats_csv, bench_json = args.summarize_trace
@@ -276,6 +413,8 @@ def main() -> int:
     import paper_2609_34814_amd as W
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.skip_sweep:
+        return run_skip_sweep(args)
     if args.copy_calibration:
         n = args.copy_calibration * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -314,27 +453,28 @@ def main() -> int:
     rng = np.random.default_rng(12345)
     row_nnz = mask.reshape(b_ * h_, mb, mb).sum(axis=2, dtype=np.int64)
 
-    def host_perm(kind):
+    def host_perm(kind, n_seg, wave_rows):
         """Ablation orders built once on the host (not part of the timed step)."""
         out = np.empty((b_ * h_, mb), dtype=np.int32)
         for hh in range(b_ * h_):
             if kind == "random":
                 out[hh] = rng.permutation(mb)
-            else:  # s2-only: identity order, buckets of `wave` rows per XCD segment sorted by descending n_i
-                base, extra = divmod(mb, 8)
-                starts = [x * base + min(x, extra) for x in range(9)]
+            else:  # s2-only: identity order, buckets of `wave_rows` rows per segment sorted by descending n_i
+                base, extra = divmod(mb, n_seg)
+                starts = [x * base + min(x, extra) for x in range(n_seg + 1)]
                 order = []
-                for x in range(8):
-                    for s0 in range(starts[x], starts[x + 1], wave):
-                        rows = np.arange(s0, min(s0 + wave, starts[x + 1]))
+                for x in range(n_seg):
+                    for s0 in range(starts[x], starts[x + 1], wave_rows):
+                        rows = np.arange(s0, min(s0 + wave_rows, starts[x + 1]))
                         order.extend(rows[np.argsort(-row_nnz[hh, rows], kind="stable")])
                 out[hh] = order
         return torch.from_numpy(out).cuda().reshape(b_, h_, mb)
 
     def make_step(variant):
         spec = VARIANTS[variant]
-        fixed = host_perm(spec["perm"]) if spec["perm"] in ("random", "s2-only") else None
         n_xcd = spec["n_xcd"]
+        fixed = (host_perm(spec["perm"], n_xcd, wave * spec.get("wave_mult", 1))
+                 if spec["perm"] in ("random", "s2-only") else None)
         s1 = torch.empty((b_, h_, mb), dtype=torch.int32, device="cuda") if spec["perm"] == "stage1" else None
         seg_q = torch.empty((b_, h_, n_xcd + 1), dtype=torch.int32, device="cuda")
 

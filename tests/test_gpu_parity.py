@@ -283,3 +283,102 @@ def test_repeated_runs_identical():
     for _ in range(5):
         again, _ = _run_attn(wl, mask, q, k, v)
         assert torch.equal(again.view(torch.int16), first.view(torch.int16))
+
+
+# ------------------------------------------------------------------------------------------------
+# the benchmark's launch configuration at full size, and the largest supported head
+# ------------------------------------------------------------------------------------------------
+class _DeviceRows:
+    """O[b, h, lo:hi] pulled from the device as fp64 on demand (the full tensor is too big to copy)."""
+
+    def __init__(self, o):
+        self.o = o
+
+    def __getitem__(self, idx):
+        b, h, rows = idx
+        return self.o[b, h, rows].float().cpu().numpy().astype(np.float64)
+
+
+def _bench_launch(wl, md, qd, kd, vd, perm_kind):
+    """The path as the benchmark times it: CSR lists from compact_mask and one queue (n_xcd = 1);
+    perm_kind "reordered" uses the two-stage order over chip-wide waves, "natural" none."""
+    W_ = _w()
+    perm = seg = None
+    if perm_kind == "reordered":
+        wave = W_.wave_size(wl.head_dim, wl.block) * 8
+        perm, seg, _ = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
+                                            wave=wave, n_xcd=1, skip="never")
+    rp, ci = W_.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
+    o, lse = W_.sparse_attn_csr(qd, kd, vd, rp, ci, perm, seg, block=wl.block, n_xcd=1, return_lse=True)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def _few_blocks(mask, heads, extra, seed):
+    """First, last (ragged), heaviest and lightest rows of the given heads plus seeded random rows."""
+    b_, h_, mb, _ = mask.shape
+    n = mask.sum(-1)
+    picks = set()
+    for h in heads:
+        picks.update({(0, h, 0), (0, h, mb - 1), (0, h, int(n[0, h].argmax())), (0, h, int(n[0, h].argmin()))})
+    rng = np.random.default_rng(seed)
+    while len(picks) < 4 * len(heads) + extra:
+        picks.add((0, int(rng.integers(h_)), int(rng.integers(mb))))
+    return sorted(picks)
+
+
+def test_attention_bench_launch_full_size():
+    """363,600 tokens, 40 heads: sampled rows against the oracle, and O / LSE bit-identical to the
+    natural order in the same launch configuration."""
+    wl = CONFIGS["long-720p-401f"]
+    q, k, v = make_qkv(wl, threads=16)
+    mask = make_mask(wl, threads=16)
+    qd, kd, vd = bf16_dev(q), bf16_dev(k), bf16_dev(v)
+    md = u8_dev(mask)
+    o, lse = _bench_launch(wl, md, qd, kd, vd, "reordered")
+    o_nat, lse_nat = _bench_launch(wl, md, qd, kd, vd, "natural")
+    assert torch.equal(o.view(torch.int16), o_nat.view(torch.int16))
+    assert torch.equal(lse.view(torch.int32), lse_nat.view(torch.int32))
+    del o_nat, lse_nat
+    picks = _few_blocks(mask, (0, 19, 39), 12, seed=4)
+    ref = A.block_sparse_attention_rows(q, k, v, mask, wl.block, picks)
+    st = compare_blocks(_DeviceRows(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
+    print(wl.name, st)
+    _check(st)
+
+
+MAX_HEAD = custom("max-blocks", heads=2, head_dim=64, block=64, grid=(64, 64, 64), seq_len=4096 * 64 - 7, seed=15,
+                  rule=dict(kind="count", rho_lo=0.02, rho_hi=0.04, sigma=0.8, g=8))
+
+
+def test_max_blocks_compaction_and_permutation():
+    """M_B = 4096 (the largest supported head, last block 57 tokens): compaction and both
+    permutation layouts bit-exact."""
+    wl = MAX_HEAD
+    assert wl.mb == 4096
+    mask = make_mask(wl)
+    rp, ci = _w().compact_mask(u8_dev(mask), seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
+    torch.cuda.synchronize()
+    rp, ci = rp.cpu().numpy(), ci.cpu().numpy()
+    for h in range(wl.heads):
+        base = h * wl.mb * wl.mb
+        assert csr_matches_mask(mask[0, h], rp[0, h], ci[base: base + wl.mb * wl.mb])
+    _perm_case(wl, mask, wave=64, n_xcd=8, mode=S.SKIP_NEVER)
+    _perm_case(wl, mask, wave=_w().wave_size(wl.head_dim, wl.block) * 8, n_xcd=1, mode=S.SKIP_NEVER)
+
+
+def test_max_blocks_attention():
+    wl = MAX_HEAD
+    q, k, v = make_qkv(wl)
+    mask = make_mask(wl)
+    qd, kd, vd = bf16_dev(q), bf16_dev(k), bf16_dev(v)
+    md = u8_dev(mask)
+    o, lse = _bench_launch(wl, md, qd, kd, vd, "reordered")
+    o_nat, lse_nat = _run_attn(wl, mask, qd, kd, vd, perm=None, n_xcd=8)
+    assert torch.equal(o.view(torch.int16), o_nat.view(torch.int16))
+    assert torch.equal(lse.view(torch.int32), lse_nat.view(torch.int32))
+    picks = _few_blocks(mask, (0, 1), 16, seed=5)
+    ref = A.block_sparse_attention_rows(q, k, v, mask, wl.block, picks)
+    st = compare_blocks(_DeviceRows(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
+    print(wl.name, st)
+    _check(st)

@@ -136,6 +136,33 @@ EXTRA_CONFIGS = {
 ALL_CONFIGS = {**CONFIGS, **EXTRA_CONFIGS}
 
 
+def sweep_workload(frames: int, rho: float, kind: str, seed: int) -> Workload:
+    """One point of the skip-rule sweep: the 720p latent grid (45 x 80 tokens a frame) over ``frames``
+    frames, 40 heads, d = 128, 128-token blocks. ``kind`` "spatial": every head takes the count rule
+    at density ``rho``; "mixed": heads 20-39 take the temporal rule of the mixed workload instead."""
+    spatial = dict(kind="count", rho_lo=rho, rho_hi=rho, sigma=0.8, g=8)
+    if kind == "spatial":
+        groups = ((0, 40, spatial),)
+    elif kind == "mixed":
+        groups = ((0, 20, spatial), (20, 40, dict(kind="radius", rt=frames, rs=0.5, g=8)))
+    else:
+        raise ValueError(kind)
+    return Workload(f"sweep-{frames}f-{kind}-rho{rho:g}", 1, 40, 128, 128, (frames, 45, 80), seed, _rules(*groups))
+
+
+def skip_sweep_workloads():
+    """The sweep of the adaptive skip (Sec. VI-F): sequence length from 25,200 to 522,000 tokens
+    (7 to 145 latent frames; 145 frames are 4,079 blocks, just under the 4,096-block limit) at 5%
+    density, spatial and mixed heads; then density 1.7% to 25% at 363,600 tokens."""
+    out = []
+    for frames in (7, 14, 27, 55, 101, 145):
+        for kind in ("spatial", "mixed"):
+            out.append(sweep_workload(frames, 0.05, kind, 3000 + len(out)))
+    for rho in (0.017, 0.067, 0.145, 0.25):
+        out.append(sweep_workload(101, rho, "spatial", 3000 + len(out)))
+    return out
+
+
 def custom(name: str, *, batch=1, heads=2, head_dim=64, block=64, grid=(2, 16, 16), seed=7,
            rule=None, seq_len=None) -> Workload:
     """A small workload for tests; ``rule`` is one mask-rule dict applied to every head."""
