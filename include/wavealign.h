@@ -130,7 +130,11 @@ wa_status wa_wave_size(int32_t head_dim, int32_t block, int32_t* wave_per_xcd);
 wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row_nnz, int32_t* col_cnt,
                         int64_t* head_stats, void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes needed by wa_build_permutation and wa_mask_stats. */
+/* Workspace bytes needed by wa_build_permutation and wa_mask_stats: the bit-packed
+ * rows and columns of the mask, per-head statistics, and the state of the subspace
+ * iteration (X, the centred products and their per-slice partial sums, one slice
+ * per 256 columns), about B*H*M_B*(2*ceil(N_B/64)*8 + 40 + 16*ceil(N_B/256)) bytes.
+ * Calls that share a workspace must not overlap. */
 wa_status wa_perm_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Two-stage cache-aware row permutation per head (Alg. 2 with MFCSI, Alg. 1):

@@ -72,20 +72,39 @@ wa_status check_shape(const wa_shape* s, Dims* out) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 struct PermWs {
-  size_t rowbits, colbits, row_nnz, col_cnt, head_stats, total;
+  size_t rowbits, colbits, row_nnz, col_cnt, head_stats, xg, ym, part, psy, state, total;
+  int slices;
 };
 
 PermWs perm_ws_layout(const Dims& d) {
   PermWs w{};
   const int64_t words = (d.mb + 63) / 64;
+  w.slices = wa_perm_slices(d.mb);
   size_t off = 0;
   w.rowbits = off; off = align_up(off + (size_t)d.bh * d.mb * words * 8);
   w.colbits = off; off = align_up(off + (size_t)d.bh * d.mb * words * 8);
   w.row_nnz = off; off = align_up(off + (size_t)d.bh * d.mb * 4);
   w.col_cnt = off; off = align_up(off + (size_t)d.bh * d.mb * 4);
   w.head_stats = off; off = align_up(off + (size_t)d.bh * 6 * 8);
+  w.xg = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 4);
+  w.ym = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 8);
+  w.part = off; off = align_up(off + (size_t)d.bh * w.slices * d.mb * 2 * 8);
+  w.psy = off; off = align_up(off + (size_t)d.bh * w.slices * 2 * 8);
+  w.state = off; off = align_up(off + (size_t)d.bh * sizeof(PermState));
   w.total = off;
   return w;
+}
+
+void perm_ws_pointers(WaPermLaunch& a, const PermWs& L, char* base) {
+  a.rowbits = (const uint64_t*)(base + L.rowbits);
+  a.colbits = (const uint64_t*)(base + L.colbits);
+  a.cc = (int32_t*)(base + L.col_cnt);
+  a.xg = (int32_t*)(base + L.xg);
+  a.ym = (int64_t*)(base + L.ym);
+  a.part = (int64_t*)(base + L.part);
+  a.psy = (int64_t*)(base + L.psy);
+  a.state = (PermState*)(base + L.state);
+  a.slices = L.slices;
 }
 
 // Attention workspace: [scheduler state][V^T copy][row_ptr][col_idx]; the CSR entry point uses the
@@ -229,8 +248,7 @@ wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row
   s = perm_launch_common(mask, d, L, base, st, row_nnz);
   if (s != WA_OK) return s;
   WaPermLaunch a{};
-  a.rowbits = (const uint64_t*)(base + L.rowbits);
-  a.colbits = (const uint64_t*)(base + L.colbits);
+  perm_ws_pointers(a, L, base);
   a.row_nnz = row_nnz;
   a.col_cnt = col_cnt;
   a.head_stats = head_stats;
@@ -238,7 +256,7 @@ wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row
   a.wave = 1; a.n_xcd = 1; a.iters = 0; a.skip_mode = WA_SKIP_NEVER; a.stats_only = 1;
   a.block = d.blk; a.head_dim = d.d;
   a.prof = kDefaultProfile;
-  hipError_t e = wa_launch_perm_heads(a, st);
+  hipError_t e = wa_launch_perm(a, st);
   if (e != hipSuccess) return hip_fail(e, "mask stats launch");
   return ok();
 }
@@ -271,8 +289,7 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
   s = perm_launch_common(mask, d, L, base, st, nullptr);
   if (s != WA_OK) return s;
   WaPermLaunch a{};
-  a.rowbits = (const uint64_t*)(base + L.rowbits);
-  a.colbits = (const uint64_t*)(base + L.colbits);
+  perm_ws_pointers(a, L, base);
   a.row_nnz = (const int32_t*)(base + L.row_nnz);
   a.col_cnt = nullptr;
   a.head_stats = nullptr;
@@ -281,7 +298,7 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
   a.wave = wave; a.n_xcd = params->n_xcd; a.iters = params->iters; a.skip_mode = params->skip_mode;
   a.stats_only = 0; a.block = d.blk; a.head_dim = d.d; a.seed = params->seed;
   a.prof = params->profile ? *params->profile : kDefaultProfile;
-  hipError_t e = wa_launch_perm_heads(a, st);
+  hipError_t e = wa_launch_perm(a, st);
   if (e != hipSuccess) return hip_fail(e, "permutation launch");
   return ok();
 }

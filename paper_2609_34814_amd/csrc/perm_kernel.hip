@@ -1,12 +1,13 @@
-// Cache-aware query-row permutation for gfx950: one 1024-thread workgroup per head.
+// Cache-aware query-row permutation for gfx950.
 //
 // Phases (Sec. IV-C..IV-E, Alg. 1, Alg. 2):
 //   0  mask statistics from the bit-packed rows and columns (n_i, c_j, nnz,
 //      distinct columns, adjacent-row overlap, sum c_j^2);
-//   1  skip cases 1-3 (fits in L2, too little work, already local);
+//   1  skip cases 1-3 (fits in cache, too little work, already local);
 //   2  matrix-free centred subspace iteration in exact fixed point: the centred
 //      products are integer sums over the set bits of the packed mask plus the
-//      rank-one centring corrections scaled by m (Alg. 1); the 2-column QR is a
+//      rank-one centring corrections scaled by m (Alg. 1), spread over one
+//      workgroup per 256-column slice of every head; the 2-column QR is a
 //      Cholesky-QR of the exactly summed Gram matrix (one IEEE fp64 rounding per
 //      operation, no contraction); then Rayleigh-Ritz with one Jacobi rotation
 //      and a canonical column sign;
@@ -20,8 +21,13 @@
 //      (bucket, -n_i, position) keys sorts every bucket by descending n_i,
 //      stably. The segment table is an output: the attention kernel runs
 //      segment x on XCD x.
-// Every sum is an exact integer, so the order of parallel reductions does not
-// matter and the result is reproducible bit for bit. Supports m, n <= 4096.
+// Phases 0-1 and the first QR run in perm_init_kernel, each further QR in
+// orth_step_kernel and phases 3-5 in perm_finish_kernel (one 1024-thread
+// workgroup per head each); the centred products run in apply_gather_kernel and
+// apply_scatter_kernel. Per-head state between the kernels lives in the
+// workspace. Every sum is an exact integer, so neither the order of parallel
+// reductions nor the slicing matters and the result is reproducible bit for bit.
+// Supports m, n <= 4096.
 
 #pragma clang fp contract(off)
 
@@ -43,8 +49,7 @@ constexpr int PER = MAXB / NT;  // rows or columns per thread
 struct Shared {
   int32_t cc[MAXB];          // column counts; later the Stage-1 order
   int32_t xs[2 * MAXB];      // X (2^30 fixed point), later U
-  int32_t ys[2 * MAXB];      // Ys; later sort scratch (indices, then 64-bit keys)
-  int64_t za[2 * MAXB];      // M Ys accumulators
+  int32_t ys[2 * MAXB];      // sort scratch (indices, then 64-bit keys)
   int64_t red[NWAVE * 4];
   int32_t part[NT];          // scan partials
   int32_t seg[65];           // XCD segment starts of the current order
@@ -194,89 +199,168 @@ __device__ __forceinline__ void for_bits(const uint64_t* words, int nwords, int6
   }
 }
 
-// zr = m * M~ Ys for the thread's rows, with Ys = (m * M~^T X) >> sy, both exact; returns sy.
-// One lane per column: M^T X gathers X over the set bits of the column's 64-row words; M Ys
-// scatters Ys[j] into the rows of those bits with 64-bit LDS atomics (integer, so exact in any
-// order). Column counts are far more even than the heavy-tailed row counts, so both halves stay
-// balanced across the workgroup.
-__device__ int centred_apply(Shared& sh, const Head& H, int64_t (&zr)[PER][2]) {
-  const int tid = threadIdx.x;
-  const int64_t m = H.m;
-  int64_t ya[PER][2];
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    ya[k][0] = 0;
-    ya[k][1] = 0;
-    const int j = tid + k * NT;
-    if (j < H.n)
-      for_bits(H.colbits, H.mw, H.n, j, [&](int i) {
-        const int2 x = *(const int2*)&sh.xs[2 * i];
-        ya[k][0] += x.x;
-        ya[k][1] += x.y;
-      });
+// ---------------------------------------------------------------------------------------------
+// Centred products across many workgroups. One subspace step X -> Z = m * M~ Ys, with
+// Ys = (m * M~^T X) >> sy, runs as two slice kernels (one 256-thread workgroup per 256-column
+// slice of every head, one lane per column) and the per-head orth kernel:
+//   gather:  Ym[j] = m * sum_{i in column j} X[i] - c_j * sum_i X[i]; atomic max of |Ym| per head;
+//   scatter: Ys[j] = Ym[j] >> sy; the slice's share of M Ys, scattered into LDS with 64-bit LDS
+//            atomics, and of sum_j c_j Ys[j], both written out as partial sums;
+//   orth:    Z[i] = m * (sum of the partials of row i) - (sum of the partial c.Ys sums).
+// Column counts are far more even than the heavy-tailed row counts, so one lane per column keeps
+// the lanes of a wavefront balanced in both halves. Every sum is an exact integer, so the slicing
+// does not change any result.
+constexpr int GT = 256;
+constexpr int GW = GT / 64;
+
+__global__ __launch_bounds__(GT) void apply_gather_kernel(WaPermLaunch a) {
+  const int h = blockIdx.x / a.slices, s = blockIdx.x % a.slices;
+  if (!a.state[h].active) return;
+  __shared__ __attribute__((aligned(16))) int32_t xs[2 * MAXB];
+  __shared__ int64_t red[GW][2];
+  __shared__ uint64_t redm[GW];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int m = a.m, n = a.n, mw = (m + 63) / 64;
+  const int2* xg = reinterpret_cast<const int2*>(a.xg) + (int64_t)h * m;
+  int64_t sx0 = 0, sx1 = 0;
+  for (int i = tid; i < m; i += GT) {
+    const int2 x = xg[i];
+    xs[2 * i] = x.x;
+    xs[2 * i + 1] = x.y;
+    sx0 += x.x;
+    sx1 += x.y;
   }
-  int64_t sx[2] = {0, 0};
-  for (int i = tid; i < H.m; i += NT) {
-    sx[0] += sh.xs[2 * i];
-    sx[1] += sh.xs[2 * i + 1];
+  sx0 = wave_sum(sx0);
+  sx1 = wave_sum(sx1);
+  if (lane == 0) {
+    red[w][0] = sx0;
+    red[w][1] = sx1;
   }
-  block_sum<2>(sh, sx);
-  uint64_t mx = 0;
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int j = tid + k * NT;
-    if (j < H.n) {
-      const int64_t c = sh.cc[j];
-      ya[k][0] = m * ya[k][0] - c * sx[0];
-      ya[k][1] = m * ya[k][1] - c * sx[1];
-      const uint64_t a = uabs64(ya[k][0]), b = uabs64(ya[k][1]);
-      mx = a > mx ? a : mx;
-      mx = b > mx ? b : mx;
-    }
-  }
-  mx = block_max(sh, mx);
-  const int bl = bitlen_u64(mx);
-  const int sy = bl > 30 ? bl - 30 : 0;
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int j = tid + k * NT;
-    if (j < H.n) {
-      sh.ys[2 * j] = (int32_t)(ya[k][0] >> sy);
-      sh.ys[2 * j + 1] = (int32_t)(ya[k][1] >> sy);
-    }
-  }
-  for (int i = tid; i < 2 * H.m; i += NT) sh.za[i] = 0;
   __syncthreads();
+  sx0 = 0;
+  sx1 = 0;
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int j = tid + k * NT;
-    if (j < H.n) {
-      const int2 y = *(const int2*)&sh.ys[2 * j];
-      const unsigned long long y0 = (unsigned long long)(int64_t)y.x, y1 = (unsigned long long)(int64_t)y.y;
-      for_bits(H.colbits, H.mw, H.n, j, [&](int i) {
-        atomicAdd((unsigned long long*)&sh.za[2 * i], y0);
-        atomicAdd((unsigned long long*)&sh.za[2 * i + 1], y1);
-      });
+  for (int k = 0; k < GW; ++k) {
+    sx0 += red[k][0];
+    sx1 += red[k][1];
+  }
+  const int j = s * GT + tid;
+  uint64_t mx = 0;
+  if (j < n) {
+    int64_t y0 = 0, y1 = 0;
+    for_bits(a.colbits + (int64_t)h * n * mw, mw, n, j, [&](int i) {
+      const int2 x = *(const int2*)&xs[2 * i];
+      y0 += x.x;
+      y1 += x.y;
+    });
+    const int64_t c = a.cc[(int64_t)h * n + j];
+    y0 = (int64_t)m * y0 - c * sx0;
+    y1 = (int64_t)m * y1 - c * sx1;
+    int64_t* out = a.ym + ((int64_t)h * n + j) * 2;
+    out[0] = y0;
+    out[1] = y1;
+    const uint64_t p = uabs64(y0), q = uabs64(y1);
+    mx = p > q ? p : q;
+  }
+  mx = wave_max(mx);
+  if (lane == 0) redm[w] = mx;
+  __syncthreads();
+  if (tid == 0) {
+    for (int k = 1; k < GW; ++k) mx = redm[k] > mx ? redm[k] : mx;
+    if (mx) atomicMax((unsigned long long*)&a.state[h].maxy, (unsigned long long)mx);
+  }
+}
+
+__global__ __launch_bounds__(GT) void apply_scatter_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  unsigned long long* za = reinterpret_cast<unsigned long long*>(smem_raw);  // [2 m]
+  __shared__ int64_t red[GW][2];
+  const int h = blockIdx.x / a.slices, s = blockIdx.x % a.slices;
+  if (!a.state[h].active) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int m = a.m, n = a.n, mw = (m + 63) / 64;
+  const int bl = bitlen_u64(a.state[h].maxy);
+  const int sy = bl > 30 ? bl - 30 : 0;
+  for (int i = tid; i < 2 * m; i += GT) za[i] = 0ull;
+  __syncthreads();
+  const int j = s * GT + tid;
+  int64_t p0 = 0, p1 = 0;
+  if (j < n) {
+    const int64_t* yj = a.ym + ((int64_t)h * n + j) * 2;
+    const int32_t y0 = (int32_t)(yj[0] >> sy), y1 = (int32_t)(yj[1] >> sy);
+    const int64_t c = a.cc[(int64_t)h * n + j];
+    p0 = c * y0;
+    p1 = c * y1;
+    const unsigned long long u0 = (unsigned long long)(int64_t)y0, u1 = (unsigned long long)(int64_t)y1;
+    for_bits(a.colbits + (int64_t)h * n * mw, mw, n, j, [&](int i) {
+      atomicAdd(&za[2 * i], u0);
+      atomicAdd(&za[2 * i + 1], u1);
+    });
+  }
+  p0 = wave_sum(p0);
+  p1 = wave_sum(p1);
+  if (lane == 0) {
+    red[w][0] = p0;
+    red[w][1] = p1;
+  }
+  __syncthreads();  // also completes the scatter
+  const int64_t slot = (int64_t)h * a.slices + s;
+  if (tid == 0) {
+    int64_t q0 = 0, q1 = 0;
+    for (int k = 0; k < GW; ++k) {
+      q0 += red[k][0];
+      q1 += red[k][1];
     }
+    a.psy[slot * 2] = q0;
+    a.psy[slot * 2 + 1] = q1;
   }
-  int64_t syy[2] = {0, 0};
-  for (int j = tid; j < H.n; j += NT) {
-    syy[0] += (int64_t)sh.cc[j] * sh.ys[2 * j];
-    syy[1] += (int64_t)sh.cc[j] * sh.ys[2 * j + 1];
+  int64_t* part = a.part + slot * m * 2;
+  for (int i = tid; i < 2 * m; i += GT) part[i] = (int64_t)za[i];
+}
+
+// zr = m * (M Ys) - sum_j c_j Ys[j] for the thread's rows, from the scatter's partial sums.
+__device__ void gather_partials(const WaPermLaunch& a, int h, int64_t (&zr)[PER][2]) {
+  const int tid = threadIdx.x;
+  const int64_t m = a.m;
+  const int64_t* psy = a.psy + (int64_t)h * a.slices * 2;
+  int64_t sy0 = 0, sy1 = 0;
+  for (int s = 0; s < a.slices; ++s) {
+    sy0 += psy[2 * s];
+    sy1 += psy[2 * s + 1];
   }
-  block_sum<2>(sh, syy);  // its barriers also complete the scatter
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int i = tid + k * NT;
-    if (i < H.m) {
-      zr[k][0] = m * sh.za[2 * i] - syy[0];
-      zr[k][1] = m * sh.za[2 * i + 1] - syy[1];
-    } else {
-      zr[k][0] = 0;
-      zr[k][1] = 0;
+    zr[k][0] = 0;
+    zr[k][1] = 0;
+    if (i < a.m) {
+      int64_t z0 = 0, z1 = 0;
+      for (int s = 0; s < a.slices; ++s) {
+        const int64_t* p = a.part + (((int64_t)h * a.slices + s) * m + i) * 2;
+        z0 += p[0];
+        z1 += p[1];
+      }
+      zr[k][0] = m * z0 - sy0;
+      zr[k][1] = m * z1 - sy1;
     }
   }
-  return sy;
+}
+
+__device__ __forceinline__ Head head_of(const WaPermLaunch& a, int h) {
+  Head H;
+  H.m = a.m;
+  H.n = a.n;
+  H.nw = (a.n + 63) / 64;
+  H.mw = (a.m + 63) / 64;
+  H.rowbits = a.rowbits + (int64_t)h * a.m * H.nw;
+  H.colbits = a.colbits + (int64_t)h * a.n * H.mw;
+  H.row_nnz = a.row_nnz + (int64_t)h * a.m;
+  return H;
+}
+
+__device__ void store_x(const WaPermLaunch& a, const Shared& sh, int h) {
+  int2* xg = reinterpret_cast<int2*>(a.xg) + (int64_t)h * a.m;
+  for (int i = threadIdx.x; i < a.m; i += NT) xg[i] = make_int2(sh.xs[2 * i], sh.xs[2 * i + 1]);
 }
 
 __device__ __forceinline__ int angle_class(int64_t x, int64_t y) {
@@ -337,27 +421,40 @@ __device__ void compute_segments(Shared& sh, const int32_t* row_nnz, int m, int 
     for (int x = tid; x <= n_xcd; x += NT) seg_out[x] = sh.seg[x];
 }
 
-__global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
+// Writes the identity order for head h (and its segments and flags).
+__device__ void write_identity(const WaPermLaunch& a, Shared& sh, int h, int flags, bool zero_embedding) {
+  const int tid = threadIdx.x, m = a.m;
+  int32_t* perm = a.perm + (int64_t)h * m;
+  for (int i = tid; i < m; i += NT) {
+    perm[i] = i;
+    sh.cc[i] = i;
+    if (a.stage1) a.stage1[(int64_t)h * m + i] = i;
+    if (zero_embedding && a.embedding) {
+      a.embedding[((int64_t)h * m + i) * 2] = 0;
+      a.embedding[((int64_t)h * m + i) * 2 + 1] = 0;
+    }
+  }
+  __syncthreads();
+  compute_segments(sh, a.row_nnz + (int64_t)h * m, m, a.n_xcd,
+                   a.seg_start ? a.seg_start + (int64_t)h * (a.n_xcd + 1) : nullptr);
+  if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
+}
+
+// Statistics, skip cases 1-3, and the first QR of the seeded start block.
+__global__ __launch_bounds__(NT) void perm_init_kernel(WaPermLaunch a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
   Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
   const int tid = threadIdx.x;
   const int h = blockIdx.x;
   const int m = a.m, n = a.n;
-  Head H;
-  H.m = m;
-  H.n = n;
-  H.nw = (n + 63) / 64;
-  H.mw = (m + 63) / 64;
-  H.rowbits = a.rowbits + (int64_t)h * m * H.nw;
-  H.colbits = a.colbits + (int64_t)h * n * H.mw;
-  H.row_nnz = a.row_nnz + (int64_t)h * m;
+  const Head H = head_of(a, h);
 
   // ---- phase 0: statistics ----
   int64_t st[4] = {0, 0, 0, 0};  // nnz, distinct, sum c^2, (unused)
   for (int j = tid; j < n; j += NT) {
     int c = 0;
     for (int v = 0; v < H.mw; ++v) c += __popcll(H.colbits[(int64_t)v * n + j]);
-    sh.cc[j] = c;
+    a.cc[(int64_t)h * n + j] = c;
     if (a.col_cnt) a.col_cnt[(int64_t)h * n + j] = c;
     st[1] += c > 0;
     st[2] += (int64_t)c * c;
@@ -396,26 +493,21 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
     sh.i32[1] = f;
   }
   __syncthreads();
-  int flags = sh.i32[1];
-  int32_t* perm = a.perm + (int64_t)h * m;
-  int32_t* seg_out = a.seg_start ? a.seg_start + (int64_t)h * (a.n_xcd + 1) : nullptr;
+  const int flags = sh.i32[1];
+  PermState* S = a.state + h;
   if (a.skip_mode == SKIP_ALWAYS || (a.skip_mode == SKIP_AUTO && flags != 0)) {
-    for (int i = tid; i < m; i += NT) {
-      perm[i] = i;
-      sh.cc[i] = i;
-      if (a.stage1) a.stage1[(int64_t)h * m + i] = i;
-      if (a.embedding) {
-        a.embedding[((int64_t)h * m + i) * 2] = 0;
-        a.embedding[((int64_t)h * m + i) * 2 + 1] = 0;
-      }
+    write_identity(a, sh, h, flags, true);
+    if (tid == 0) {
+      S->maxy = 0;
+      S->active = 0;
+      S->degen = 0;
+      S->done = 1;
+      S->flags = flags;
     }
-    __syncthreads();
-    compute_segments(sh, H.row_nnz, m, a.n_xcd, seg_out);
-    if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
     return;
   }
 
-  // ---- phase 2: MFCSI ----
+  // ---- phase 2 starts: seeded start block and its QR ----
   int64_t zr[PER][2];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -424,15 +516,68 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
     zr[k][0] = i < m ? (int64_t)(splitmix64(base) >> 40) - (1ll << 23) : 0;
     zr[k][1] = i < m ? (int64_t)(splitmix64(base + 1ull) >> 40) - (1ll << 23) : 0;
   }
-  bool degen = orth(sh, H, zr);
-  for (int it = 0; it < a.iters && !degen; ++it) {
-    centred_apply(sh, H, zr);
-    degen = orth(sh, H, zr);
+  const bool degen = orth(sh, H, zr);
+  if (!degen) store_x(a, sh, h);
+  if (tid == 0) {
+    S->maxy = 0;
+    S->active = degen ? 0 : 1;
+    S->degen = degen ? 1 : 0;
+    S->done = 0;
+    S->flags = flags;
+    S->nnz = nnz;
+    S->sum_c2 = sum_c2;
   }
+}
+
+// One QR of the subspace iteration: Z from the partial sums, Cholesky-QR into the next X.
+__global__ __launch_bounds__(NT) void orth_step_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+  const int h = blockIdx.x;
+  PermState* S = a.state + h;
+  if (!S->active) return;
+  const Head H = head_of(a, h);
+  int64_t zr[PER][2];
+  gather_partials(a, h, zr);
+  const bool degen = orth(sh, H, zr);
+  if (!degen) store_x(a, sh, h);
+  if (threadIdx.x == 0) {
+    S->maxy = 0;
+    if (degen) {
+      S->active = 0;
+      S->degen = 1;
+    }
+  }
+}
+
+// Rayleigh-Ritz on the last product, canonical sign, skip case 4, Stage 1 and Stage 2.
+__global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+  const int tid = threadIdx.x;
+  const int h = blockIdx.x;
+  const int m = a.m;
+  const PermState* S = a.state + h;
+  if (S->done) return;
+  const Head H = head_of(a, h);
+  const bool degen = S->degen != 0;
+  const int64_t nnz = S->nnz, sum_c2 = S->sum_c2;
+  int flags = S->flags;
+  int32_t* perm = a.perm + (int64_t)h * m;
+  int32_t* seg_out = a.seg_start ? a.seg_start + (int64_t)h * (a.n_xcd + 1) : nullptr;
   int64_t trace = 0;
   int scale_exp = 0;
   if (!degen) {
-    const int sy = centred_apply(sh, H, zr);
+    const int2* xg = reinterpret_cast<const int2*>(a.xg) + (int64_t)h * m;
+    for (int i = tid; i < m; i += NT) {
+      const int2 x = xg[i];
+      sh.xs[2 * i] = x.x;
+      sh.xs[2 * i + 1] = x.y;
+    }
+    const int bly = bitlen_u64(S->maxy);
+    const int sy = bly > 30 ? bly - 30 : 0;
+    int64_t zr[PER][2];
+    gather_partials(a, h, zr);
     uint64_t mx = 0;
 #pragma unroll
     for (int k = 0; k < PER; ++k)
@@ -441,7 +586,7 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
         mx = p > mx ? p : mx;
         mx = q > mx ? q : mx;
       }
-    mx = block_max(sh, mx);
+    mx = block_max(sh, mx);  // its barriers also publish sh.xs
     const int bl = bitlen_u64(mx);
     const int s_r = bl > 24 ? bl - 24 : 0;
     int64_t b[4] = {0, 0, 0, 0};
@@ -524,14 +669,7 @@ __global__ __launch_bounds__(NT) void perm_head_kernel(WaPermLaunch a) {
     }
   if (a.skip_mode == SKIP_AUTO && (flags & FLAG_UNSTRUCTURED)) {
     __syncthreads();  // every thread has written its embedding rows (read from sh.xs)
-    for (int i = tid; i < m; i += NT) {
-      perm[i] = i;
-      sh.cc[i] = i;
-      if (a.stage1) a.stage1[(int64_t)h * m + i] = i;
-    }
-    __syncthreads();
-    compute_segments(sh, H.row_nnz, m, a.n_xcd, seg_out);
-    if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
+    write_identity(a, sh, h, flags, false);
     return;
   }
 
@@ -615,13 +753,37 @@ __global__ void fp64_probe_kernel(const double* a, const double* b, const int64_
 
 size_t wa_perm_shared_bytes() { return sizeof(Shared); }
 
-hipError_t wa_launch_perm_heads(const WaPermLaunch& a, hipStream_t stream) {
+int wa_perm_slices(int n) { return (n + GT - 1) / GT; }
+
+// Launch sequence on one stream: init; iters x (gather, scatter, orth); gather, scatter, finish.
+// The statistics-only form runs init alone.
+hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   if (a.bh <= 0) return hipSuccess;
+  if (a.slices != wa_perm_slices(a.n) || a.m > MAXB || a.n > MAXB) return hipErrorInvalidValue;
   const size_t smem = sizeof(Shared);
-  hipError_t e = hipFuncSetAttribute((const void*)perm_head_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)smem);
+  const size_t zsmem = (size_t)2 * a.m * sizeof(unsigned long long);
+  const void* big[] = {(const void*)perm_init_kernel, (const void*)orth_step_kernel, (const void*)perm_finish_kernel};
+  for (const void* f : big) {
+    hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = hipFuncSetAttribute((const void*)apply_scatter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)zsmem);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(perm_head_kernel, dim3(a.bh), dim3(NT), smem, stream, a);
+  hipLaunchKernelGGL(perm_init_kernel, dim3(a.bh), dim3(NT), smem, stream, a);
+  if ((e = hipGetLastError()) != hipSuccess || a.stats_only) return e;
+  const dim3 slices((unsigned)(a.bh * a.slices));
+  for (int it = 0; it <= a.iters; ++it) {
+    hipLaunchKernelGGL(apply_gather_kernel, slices, dim3(GT), 0, stream, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(apply_scatter_kernel, slices, dim3(GT), zsmem, stream, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (it < a.iters) {
+      hipLaunchKernelGGL(orth_step_kernel, dim3(a.bh), dim3(NT), smem, stream, a);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+  }
+  hipLaunchKernelGGL(perm_finish_kernel, dim3(a.bh), dim3(NT), smem, stream, a);
   return hipGetLastError();
 }
 
