@@ -128,10 +128,10 @@ wa_status check_ws(void* ws, size_t have, size_t need) {
 
 const wa_skip_profile kDefaultProfile = {
     256.0 * 1024.0 * 1024.0,  // cache_bytes: MI355X shared last-level cache (behind the per-XCD L2s)
-    1.0,                      // gain_ns_per_block
-    2000.0,                   // ovh_ns_fixed
-    2.0,                      // ovh_ns_per_row
-    0.05,                     // ovh_ns_per_nnz
+    0.1,                      // gain_ns_per_block: attention time saved per kept block, densest sweep points
+    5270.0,                   // ovh_ns_fixed    } permutation time per head, amortised over concurrent
+    7.6,                      // ovh_ns_per_row  } heads, least-squares fit over the sequence-length and
+    0.056,                    // ovh_ns_per_nnz  } density sweep
     0.75,                     // j_max
     0.05,                     // eta_min
 };

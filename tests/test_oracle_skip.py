@@ -46,15 +46,23 @@ def test_eta_separates_random_from_structured():
         assert lo <= S.eta(st, s1.trace, s1.scale_exp) < hi
 
 
+# A profile under which only the designed case fires on the inputs below: a 4 MiB cache and
+# a cheap reordering that saves 1 ns per kept block.
+PERMISSIVE = S.SkipProfile(cache_bytes=4 * 1024 * 1024, gain_ns_per_block=1.0, ovh_ns_fixed=2000.0,
+                           ovh_ns_per_row=2.0, ovh_ns_per_nnz=0.05)
+
+
 def test_tier1_cases():
     prof = S.SkipProfile()
     tiny = make_mask_head(CONFIGS["tiny"], 0, 0)
     f = S.tier1_flags(S.head_stats(tiny), prof, 64, 64)
     assert f & S.FLAG_FITS_CACHE          # 64 KV blocks of 16 KiB = 1 MiB < 256 MiB
     big = S.head_stats(make_mask_head(CONFIGS["wan14b-720p-81f"], 0, 0))
-    # 591 KV blocks of 64 KiB = 37 MiB: inside the shared last-level cache, not inside one 4 MiB L2
-    assert S.tier1_flags(big, prof, 128, 128) == S.FLAG_FITS_CACHE
-    assert S.tier1_flags(big, S.SkipProfile(cache_bytes=4 * 1024 * 1024), 128, 128) == 0
+    # 591 KV blocks of 64 KiB = 37 MiB: inside the shared last-level cache, not inside one 4 MiB L2;
+    # 52K kept blocks save 5 us at 0.1 ns each, less than the 13 us the permutation costs
+    assert S.tier1_flags(big, prof, 128, 128) == S.FLAG_FITS_CACHE | S.FLAG_LITTLE_WORK
+    assert S.tier1_flags(big, PERMISSIVE, 128, 128) == 0
+    prof = PERMISSIVE
     # already local: every row equal to its neighbour except one column
     band = np.zeros((100, 100), dtype=np.uint8)
     for i in range(100):
@@ -83,14 +91,14 @@ def test_driver_modes():
         assert np.array_equal(p_never[0, h], ref)
     assert not np.any(f_never & S.FLAG_IDENTITY)
     # a 4 MiB cache keeps case 1 quiet (11.6 MiB of K/V per head), so the later cases decide
-    small = S.SkipProfile(cache_bytes=4 * 1024 * 1024)
-    p_auto, f_auto, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, profile=small, **kw)
+    p_auto, f_auto, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, profile=PERMISSIVE, **kw)
     # random heads: unstructured -> identity; locality heads: reordered
     assert f_auto[0, 0] & S.FLAG_UNSTRUCTURED and np.all(p_auto[0, 0] == np.arange(wl.mb))
     assert f_auto[0, 2] == 0 and np.array_equal(p_auto[0, 2], p_never[0, 2])
     # default profile: every head's K/V fits the shared cache, so case 1 keeps the identity order
     p_def, f_def, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, **kw)
-    assert np.all(f_def == S.FLAG_FITS_CACHE | S.FLAG_IDENTITY) and np.all(p_def == np.arange(wl.mb))
+    assert np.all(f_def & S.FLAG_FITS_CACHE) and np.all(f_def & S.FLAG_IDENTITY)
+    assert np.all(p_def == np.arange(wl.mb))
 
 
 def test_compaction_brute_force():
