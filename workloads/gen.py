@@ -16,7 +16,14 @@ Sec. VI-F shows diagonal-dominated masks; Table I uses a random-mask floor).
 Random streams: every array is drawn from its own NumPy ``SeedSequence``
 ``[seed, stream, flat_head]`` so any head can be regenerated alone.
 Stream ids: 0 Q, 1 K, 2 V, 3 mask row counts / Bernoulli draws, 4 global
-columns, 5 tie-break hashes.
+columns, 5 tie-break hashes, 6 positional features.
+
+Workloads whose masks are to be produced from Q and K (the pooled-score mask
+producer) add a positional component to Q and K: per head, random Fourier
+features of the token's (frame, y, x) position, so that the expected product of
+two tokens' features is a Gaussian kernel of their distance. "spatial" heads
+decay with distance in time and space, "temporal" heads ignore the frame index,
+so that tokens at the same in-frame position match across all frames.
 """
 from __future__ import annotations
 
@@ -28,7 +35,7 @@ from typing import Optional, Sequence
 
 import numpy as np
 
-STREAM_Q, STREAM_K, STREAM_V, STREAM_COUNT, STREAM_GLOBAL, STREAM_TIE = 0, 1, 2, 3, 4, 5
+STREAM_Q, STREAM_K, STREAM_V, STREAM_COUNT, STREAM_GLOBAL, STREAM_TIE, STREAM_POS = 0, 1, 2, 3, 4, 5, 6
 
 
 # --------------------------------------------------------------------------------------
@@ -84,6 +91,8 @@ class Workload:
     # mask recipe, one entry per head group: list of (first_head, last_head_exclusive, rule dict)
     mask_rules: tuple = field(default_factory=tuple)
     seq_len_override: Optional[int] = None
+    # positional component of Q and K, one entry per head group: (first, last_exclusive, rule dict)
+    qk_rules: tuple = field(default_factory=tuple)
 
     @property
     def seq_len(self) -> int:
@@ -133,6 +142,19 @@ EXTRA_CONFIGS = {
                                      _rules((0, 20, dict(kind="count", rho_lo=0.05, rho_hi=0.05, sigma=0.8, g=8)),
                                             (20, 40, dict(kind="radius", rt=101, rs=0.5, g=8)))),
 }
+# Workloads for the pooled-score mask producer: Q and K carry the positional component above
+# (heads 0..H/2-1 spatial, the rest temporal); their masks are produced from Q and K, so
+# mask_rules is empty. The large one has the shapes of the 401-frame workload.
+_SPATIAL_QK = dict(amp=3.0, lt=1.5, ly=4.0, lx=6.0)
+_TEMPORAL_QK = dict(amp=3.0, lt=math.inf, ly=3.0, lx=4.0)
+PRODUCER_CONFIGS = {
+    "produced-tiny": Workload("produced-tiny", 1, 2, 64, 64, (4, 32, 32), 1101,
+                              qk_rules=_rules((0, 1, _SPATIAL_QK), (1, 2, _TEMPORAL_QK))),
+    "produced-ragged": Workload("produced-ragged", 2, 2, 128, 128, (5, 30, 52), 1102,
+                                qk_rules=_rules((0, 1, _SPATIAL_QK), (1, 2, _TEMPORAL_QK))),
+    "produced-long-720p-401f": Workload("produced-long-720p-401f", 1, 40, 128, 128, (101, 45, 80), 1103,
+                                        qk_rules=_rules((0, 20, _SPATIAL_QK), (20, 40, _TEMPORAL_QK))),
+}
 ALL_CONFIGS = {**CONFIGS, **EXTRA_CONFIGS}
 
 
@@ -175,6 +197,28 @@ def custom(name: str, *, batch=1, heads=2, head_dim=64, block=64, grid=(2, 16, 1
 # --------------------------------------------------------------------------------------
 # tensors
 # --------------------------------------------------------------------------------------
+def qk_rule_for_head(wl: Workload, h: int) -> Optional[dict]:
+    for a, b, r in wl.qk_rules:
+        if a <= h < b:
+            return dict(r)
+    return None
+
+
+def positional_features(wl: Workload, flat_head: int, rule: dict) -> np.ndarray:
+    """float64 [N][d]: sqrt(2/d) cos(w_c . p_t + phi_c) with p_t = (frame, y, x) of token t,
+    w_c ~ N(0, diag(1/lt^2, 1/ly^2, 1/lx^2)) (lt = inf: no time dependence), phi_c ~ U[0, 2 pi)."""
+    n, d = wl.seq_len, wl.head_dim
+    f_, hh, ww = wl.grid
+    rng = _rng(wl, STREAM_POS, flat_head)
+    g = rng.standard_normal((3, d))
+    inv_l = np.array([0.0 if math.isinf(rule["lt"]) else 1.0 / rule["lt"], 1.0 / rule["ly"], 1.0 / rule["lx"]])
+    w = g * inv_l[:, None]
+    phi = rng.uniform(0.0, 2.0 * math.pi, size=d)
+    t = np.arange(n, dtype=np.int64)
+    pos = np.stack([t // (hh * ww), (t // ww) % hh, t % ww], axis=1).astype(np.float64)
+    return math.sqrt(2.0 / d) * np.cos(pos @ w + phi)
+
+
 def make_tensor(wl: Workload, stream: int, heads: Optional[Sequence[int]] = None,
                 threads: int = 8) -> np.ndarray:
     """bf16 bit patterns, shape [B][H][N][d] (or [len(heads)] flat heads if ``heads`` given)."""
@@ -183,7 +227,12 @@ def make_tensor(wl: Workload, stream: int, heads: Optional[Sequence[int]] = None
     out = np.empty((len(flat), n, d), dtype=np.uint16)
 
     def one(k):
-        out[k] = bf16_normal(wl.seed, stream, flat[k], n * d).reshape(n, d)
+        bits = bf16_normal(wl.seed, stream, flat[k], n * d).reshape(n, d)
+        rule = qk_rule_for_head(wl, flat[k] % wl.heads) if stream in (STREAM_Q, STREAM_K) else None
+        if rule is not None:
+            x = bf16_bits_to_f32(bits).astype(np.float64) + rule["amp"] * positional_features(wl, flat[k], rule)
+            bits = _f64_to_bf16_bits(x)
+        out[k] = bits
 
     if len(flat) > 1 and threads > 1:
         with ThreadPoolExecutor(min(threads, len(flat))) as ex:
