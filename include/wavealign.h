@@ -162,6 +162,28 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
 wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* row_ptr, int32_t* col_idx,
                           void* stream);
 
+/* Pooled-score top-k block mask: a content-dependent producer of the mask the path
+ * consumes (Sec. II-B: dynamic sparse attention predicts block relevance from pooled
+ * Q/K features). Per head:
+ *   qbar_i = mean of the Q rows of block i (ascending float32 fold, then one
+ *            correctly rounded division by the block's token count); kbar_j alike;
+ *   codes  = rint(mean * fl32(127 / max_head |mean|)), clamped to [-127, 127]
+ *            (all zero when the maximum is 0), for Q and K separately;
+ *   s_ij   = sum_c qcode_i[c] * kcode_j[c] (exact integer);
+ *   row i keeps its `keep` largest s_ij (equal scores: smaller j first) and, if
+ *   `diagonal` is nonzero, block j = i.
+ *   q, k      bf16 [B][H][N][d], device
+ *   keep      >= 0; values >= N_B keep every block
+ *   mask      out uint8 [B][H][M_B][N_B], 1 = kept
+ *   codes     out int8 [2][B][H][M_B][d] (Q codes, then K codes), nullable
+ *   workspace >= wa_mask_producer_workspace_size(shape), 256-byte aligned. */
+wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* shape, int32_t keep, int32_t diagonal,
+                                uint8_t* mask, int8_t* codes, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by wa_produce_block_mask: float32 block means and per-head
+ * maxima of Q and K, and their int8 codes. */
+wa_status wa_mask_producer_workspace_size(const wa_shape* shape, size_t* bytes);
+
 /* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters
  * and per-queue prefix tables, (64 + 64 * (B*H + 1)) int32 rounded up to 256 bytes),
  * a zero-padded transposed copy of V (bf16 [B][H][head_dim][M_B*block], rounded up

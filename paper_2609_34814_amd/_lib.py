@@ -52,6 +52,9 @@ _SIGNATURES = {
     "wa_build_permutation": (c_int32, [c_void_p, POINTER(WaShape), POINTER(WaPermParams), c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "wa_compact_mask": (c_int32, [c_void_p, POINTER(WaShape), c_void_p, c_void_p, c_void_p]),
+    "wa_mask_producer_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
+    "wa_produce_block_mask": (c_int32, [c_void_p, c_void_p, POINTER(WaShape), c_int32, c_int32, c_void_p, c_void_p,
+                                        c_void_p, c_size_t, c_void_p]),
     "wa_attn_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
     "wa_sparse_attn": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(WaShape),
                                  c_float, c_int32, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),

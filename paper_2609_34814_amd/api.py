@@ -141,6 +141,40 @@ def compact_mask(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int 
     return row_ptr, col_idx
 
 
+def mask_producer_workspace_size(shape: L.WaShape) -> int:
+    lib = L.load()
+    n = ctypes.c_size_t(0)
+    L.check(lib.wa_mask_producer_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
+    return n.value
+
+
+def produce_block_mask(q: torch.Tensor, k: torch.Tensor, *, block: int, keep: int, diagonal: bool = True,
+                       out: Optional[torch.Tensor] = None, codes_out: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Pooled-score top-k block mask uint8 [B][H][M_B][M_B] from q, k bf16 [B][H][N][d]."""
+    lib = L.load()
+    for t, nm in ((q, "q"), (k, "k")):
+        _dev(t, nm)
+        if t.dtype != torch.bfloat16:
+            raise ValueError(f"{nm} must be bfloat16")
+    if q.shape != k.shape or q.dim() != 4:
+        raise ValueError("q and k must share one [B][H][N][d] shape")
+    b, h, n, d = q.shape
+    shape = shape_of(b, h, n, d, block)
+    mb = -(-n // block)
+    mask = torch.empty((b, h, mb, mb), dtype=torch.uint8, device=q.device) if out is None else out
+    if mask.dtype != torch.uint8 or mask.numel() < b * h * mb * mb:
+        raise ValueError("out must be a uint8 tensor of B*H*M_B*M_B elements")
+    if codes_out is not None and (codes_out.dtype != torch.int8 or codes_out.numel() < 2 * b * h * mb * d):
+        raise ValueError("codes_out must be an int8 tensor of 2*B*H*M_B*d elements")
+    need = mask_producer_workspace_size(shape)
+    if workspace is None or workspace.numel() < need:
+        workspace = _workspace(need, q.device)
+    L.check(lib.wa_produce_block_mask(_ptr(q), _ptr(k), ctypes.byref(shape), int(keep), 1 if diagonal else 0,
+                                      _ptr(mask), _ptr(codes_out), _ptr(workspace), workspace.numel(), _stream()))
+    return mask
+
+
 def _attn_args(q, k, v, block):
     for t, nm in ((q, "q"), (k, "k"), (v, "v")):
         _dev(t, nm)

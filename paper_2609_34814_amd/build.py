@@ -23,6 +23,8 @@ SOURCES = {
     "mask_kernels.hip": [],
     # the permutation must round exactly as specified: no fused multiply-add
     "perm_kernel.hip": ["-ffp-contract=off"],
+    # the mask producer's float32 folds, divisions and products must round as specified
+    "mask_producer.hip": ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt"],
     "abi.cpp": [],
 }
 

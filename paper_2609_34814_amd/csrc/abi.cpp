@@ -10,6 +10,7 @@
 
 #include "common.h"
 #include "perm_launch.h"
+#include "producer_launch.h"
 #include "wavealign.h"
 
 namespace {
@@ -70,6 +71,20 @@ wa_status check_shape(const wa_shape* s, Dims* out) {
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+struct ProducerWs {
+  size_t means, amax, codes, total;
+};
+
+ProducerWs producer_ws_layout(const Dims& d) {
+  ProducerWs w{};
+  size_t off = 0;
+  w.means = off; off = align_up(off + (size_t)2 * d.bh * d.mb * d.d * 4);
+  w.amax = off; off = align_up(off + (size_t)2 * d.bh * 4);
+  w.codes = off; off = align_up(off + (size_t)2 * d.bh * d.mb * d.d);
+  w.total = off;
+  return w;
+}
 
 struct PermWs {
   size_t rowbits, colbits, row_nnz, col_cnt, head_stats, xg, ym, part, psy, state, total;
@@ -300,6 +315,41 @@ wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const
   a.prof = params->profile ? *params->profile : kDefaultProfile;
   hipError_t e = wa_launch_perm(a, st);
   if (e != hipSuccess) return hip_fail(e, "permutation launch");
+  return ok();
+}
+
+wa_status wa_mask_producer_workspace_size(const wa_shape* shape, size_t* bytes) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!bytes) return fail(WA_ERR_INVALID_ARG, "bytes is null");
+  *bytes = producer_ws_layout(d).total;
+  return ok();
+}
+
+wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* shape, int32_t keep, int32_t diagonal,
+                                uint8_t* mask, int8_t* codes, void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!q || !k || !mask) return fail(WA_ERR_INVALID_ARG, "q, k and mask must be non-null");
+  if (keep < 0) return fail(WA_ERR_INVALID_ARG, "keep %d is negative", keep);
+  if (!aligned(q, 16) || !aligned(k, 16)) return fail(WA_ERR_ALIGNMENT, "q and k must be 16-byte aligned");
+  if (codes && !aligned(codes, 16)) return fail(WA_ERR_ALIGNMENT, "codes must be 16-byte aligned");
+  const ProducerWs L = producer_ws_layout(d);
+  s = check_ws(workspace, workspace_bytes, L.total);
+  if (s != WA_OK) return s;
+  char* base = (char*)workspace;
+  WaProducerLaunch a{};
+  a.q = q; a.k = k;
+  a.means = (float*)(base + L.means);
+  a.amax = (uint32_t*)(base + L.amax);
+  a.codes = codes ? codes : (int8_t*)(base + L.codes);
+  a.mask = mask;
+  a.bh = (int32_t)d.bh; a.mb = d.mb; a.seq_len = d.n; a.block = d.blk; a.head_dim = d.d;
+  a.keep = keep; a.diagonal = diagonal ? 1 : 0;
+  hipError_t e = wa_launch_producer(a, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "mask producer launch");
   return ok();
 }
 

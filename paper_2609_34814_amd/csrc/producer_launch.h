@@ -1,0 +1,18 @@
+// Internal launch interface of the mask-producer kernels (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+struct WaProducerLaunch {
+  const void* q;      // bf16 [bh][seq_len][head_dim]
+  const void* k;
+  float* means;       // workspace float32 [2][bh][mb][head_dim]: block means of Q, then K
+  uint32_t* amax;     // workspace [2][bh]: bits of the per-head maximum |mean|
+  int8_t* codes;      // [2][bh][mb][head_dim]: int8 codes of Q, then K
+  uint8_t* mask;      // out [bh][mb][mb]
+  int32_t bh, mb, seq_len, block, head_dim, keep, diagonal;
+};
+
+hipError_t wa_launch_producer(const WaProducerLaunch& a, hipStream_t stream);
+size_t wa_producer_select_smem(int mb);

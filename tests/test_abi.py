@@ -112,6 +112,34 @@ def test_sparse_attn_validation():
                                   ctypes.c_void_p(1 << 24), 256, None) == L.WA_ERR_WORKSPACE
 
 
+def test_produce_block_mask_validation():
+    lib = _lib()
+    s = _shape()
+    ws_n = ctypes.c_size_t(0)
+    assert lib.wa_mask_producer_workspace_size(ctypes.byref(s), ctypes.byref(ws_n)) == 0
+    b, h, mb, d = s.batch, s.heads, -(-s.seq_len // s.block), s.head_dim
+    assert ws_n.value >= 2 * b * h * mb * d * 5
+    args = dict(q=FAKE, k=FAKE, keep=8, mask=FAKE, codes=None, ws=ctypes.c_void_p(1 << 24), ws_bytes=ws_n.value)
+
+    def call(**kw):
+        a = dict(args)
+        a.update(kw)
+        return lib.wa_produce_block_mask(a["q"], a["k"], ctypes.byref(s), a["keep"], 1, a["mask"], a["codes"],
+                                         a["ws"], a["ws_bytes"], None)
+
+    assert call(q=None) == L.WA_ERR_INVALID_ARG
+    assert call(k=None) == L.WA_ERR_INVALID_ARG
+    assert call(mask=None) == L.WA_ERR_INVALID_ARG
+    assert call(keep=-1) == L.WA_ERR_INVALID_ARG
+    assert call(q=ctypes.c_void_p((1 << 20) + 2)) == L.WA_ERR_ALIGNMENT
+    assert call(codes=ctypes.c_void_p((1 << 20) + 8)) == L.WA_ERR_ALIGNMENT
+    assert call(ws=None) == L.WA_ERR_INVALID_ARG
+    assert call(ws_bytes=ws_n.value - 1) == L.WA_ERR_WORKSPACE
+    bad = L.WaShape(1, 1, 100, 96, 64)
+    assert lib.wa_produce_block_mask(FAKE, FAKE, ctypes.byref(bad), 4, 1, FAKE, None, ctypes.c_void_p(1 << 24),
+                                     1 << 30, None) == L.WA_ERR_UNSUPPORTED
+
+
 def test_build_permutation_validation():
     lib = _lib()
     s = _shape()

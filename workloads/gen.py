@@ -145,8 +145,8 @@ EXTRA_CONFIGS = {
 # Workloads for the pooled-score mask producer: Q and K carry the positional component above
 # (heads 0..H/2-1 spatial, the rest temporal); their masks are produced from Q and K, so
 # mask_rules is empty. The large one has the shapes of the 401-frame workload.
-_SPATIAL_QK = dict(amp=3.0, lt=1.5, ly=4.0, lx=6.0)
-_TEMPORAL_QK = dict(amp=3.0, lt=math.inf, ly=3.0, lx=4.0)
+_SPATIAL_QK = dict(amp=3.0, lt=2.0, ly=6.0, lx=40.0)
+_TEMPORAL_QK = dict(amp=3.0, lt=math.inf, ly=4.0, lx=30.0)
 PRODUCER_CONFIGS = {
     "produced-tiny": Workload("produced-tiny", 1, 2, 64, 64, (4, 32, 32), 1101,
                               qk_rules=_rules((0, 1, _SPATIAL_QK), (1, 2, _TEMPORAL_QK))),
