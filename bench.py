@@ -148,6 +148,8 @@ def summarize_trace(stats_csv: str, bench_json: str, out_md: str, command_note: 
     rows = list(csv.DictReader(open(stats_csv)))
     with open(bench_json) as f:
         line = json.loads([ln for ln in f.read().splitlines() if ln.startswith("{")][-1])
+    if line.get("mode") == "producer":
+        return summarize_producer_trace(rows, line, out_md, command_note)
     lines = [f"# kernel trace: {line['config']['workload']}, variant {line['config']['variant']}", "",
              f"Command: `{command_note}`", "",
              "| kernel | calls | average ms | min ms | max ms | share % |", "|---|---|---|---|---|---|"]
@@ -167,6 +169,38 @@ def summarize_trace(stats_csv: str, bench_json: str, out_md: str, command_note: 
     if attn_avg:
         lines.append(f"rocprofv3 attention kernel average: {attn_avg:.3f} ms "
                      f"({line['config']['flop_per_step'] / (attn_avg * 1e-3) / 1e12:.1f} TFLOP/s).")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_producer_trace(rows, line, out_md: str, command_note: str) -> None:
+    """Kernel table of a `bench.py --producer` run: the producer's kernels against the HBM roofline
+    of reading Q and K once and writing the mask, and the path on the produced mask."""
+    lines = [f"# kernel trace: pooled-score top-k mask producer, {line['workload']}", "",
+             f"Command: `{command_note}`", "",
+             "| kernel | calls | average ms | min ms | max ms | share % |", "|---|---|---|---|---|---|"]
+    prod_ms = 0.0
+    for r in rows:
+        short = r["Name"].replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        avg = float(r["AverageNs"]) / 1e6
+        if any(s in r["Name"] for s in ("pool_kernel", "quant_kernel", "score_select_kernel", "zero_amax_kernel")):
+            prod_ms += avg
+        if short.startswith("at::") or "elementwise" in short or "reduce_kernel" in short:
+            continue
+        lines.append(f"| {short} | {r['Calls']} | {avg:.3f} | {float(r['MinNs']) / 1e6:.3f} | "
+                     f"{float(r['MaxNs']) / 1e6:.3f} | {float(r['Percentage']):.2f} |")
+    rf = line["producer_roofline"]
+    lines += ["", f"keep {line['keep']} blocks per row + the diagonal (density {100 * line['density']:.2f}%).",
+              f"bench.py (HIP events around wa_produce_block_mask, same run): {line['producer_ms']:.3f} ms; "
+              f"{rf['achieved']:.0f} GB/s of {rf['algorithmic_bytes'] / 1e9:.2f} GB algorithmic bytes "
+              f"(Q and K read once, mask written) = {100 * rf['frac']:.1f}% of 8 TB/s.",
+              f"rocprofv3, sum of the producer kernels' averages: {prod_ms:.3f} ms.", "",
+              "Path on the produced mask (step = permutation if built + compaction + attention):", ""]
+    for v, r in line["path"].items():
+        extra = f", {r['identity_heads']} heads kept the identity order" if "identity_heads" in r else ""
+        lines.append(f"* {v}: step {r['step_ms']:.2f} ms, attention {r['attn_ms']:.2f} ms, "
+                     f"{r['tflops_step']:.1f} TFLOP/s{extra}")
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -335,6 +369,87 @@ def run_skip_sweep(args) -> int:
     return 0
 
 
+def run_producer(args) -> int:
+    """The pooled-score top-k mask producer on the 363,600-token shape with positional Q/K: its time
+    and HBM roofline, then the path (natural / reordered / auto) on the mask it produced."""
+    import torch
+    import paper_2609_34814_amd as W
+    from workloads.gen import PRODUCER_CONFIGS
+
+    wl = PRODUCER_CONFIGS["produced-long-720p-401f"]
+    t0 = time.perf_counter()
+    q, k, v = make_qkv(wl, threads=16)
+    log(f"generated {wl.name} in {time.perf_counter() - t0:.1f} s")
+
+    def dev(bits):
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+
+    qd, kd, vd = dev(q), dev(k), dev(v)
+    del q, k, v
+    b_, h_, mb, n, d, blk = wl.batch, wl.heads, wl.mb, wl.seq_len, wl.head_dim, wl.block
+    keep = round(args.producer_density * mb)
+    shape = W.shape_of(b_, h_, n, d, blk)
+    pws = torch.empty(W.mask_producer_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    md = torch.empty((b_, h_, mb, mb), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    times = []
+    for r in range(args.warmup + args.steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        W.produce_block_mask(qd, kd, block=blk, keep=keep, diagonal=True, out=md, workspace=pws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if r >= args.warmup:
+            times.append(e0.elapsed_time(e1))
+    prod_ms = float(np.mean(times))
+    hbm_bytes = 2.0 * b_ * h_ * n * d * 2 + float(b_ * h_ * mb * mb)
+    nnz = int(md.sum(dtype=torch.int64).item())
+    log(f"producer: {prod_ms:.3f} ms, keep {keep} + diagonal, nnz {nnz} ({nnz / (b_ * h_ * mb * mb):.4f})")
+
+    perm_ws = torch.empty(W.perm_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    attn_ws = torch.empty(W.attn_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    perm = torch.empty((b_, h_, mb), dtype=torch.int32, device="cuda")
+    seg = torch.empty((b_, h_, 2), dtype=torch.int32, device="cuda")
+    flags = torch.empty((b_, h_), dtype=torch.uint8, device="cuda")
+    row_ptr = torch.empty((b_, h_, mb + 1), dtype=torch.int32, device="cuda")
+    col_idx = torch.empty((b_ * h_ * mb * mb,), dtype=torch.int32, device="cuda")
+    o = torch.empty_like(qd)
+    wave = W.wave_size(d, blk) * 8
+    flop = 4.0 * blk * blk * d * nnz
+    res = {}
+    for variant in ("natural", "reordered", "auto"):
+        st = []
+        for r in range(args.warmup + args.steps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            ev[0].record(stream)
+            p = sg = None
+            if variant != "natural":
+                W.build_permutation(md, seq_len=n, block=blk, head_dim=d, wave=wave, n_xcd=1,
+                                    skip="never" if variant == "reordered" else "auto", workspace=perm_ws,
+                                    out=perm, flags_out=flags, seg_out=seg)
+                p, sg = perm, seg
+            rp, ci = W.compact_mask(md, seq_len=n, block=blk, head_dim=d, row_ptr=row_ptr, col_idx=col_idx)
+            ev[1].record(stream)
+            W.sparse_attn_csr(qd, kd, vd, rp, ci, p, sg, block=blk, n_xcd=1, out=o, workspace=attn_ws)
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            if r >= args.warmup:
+                st.append((ev[0].elapsed_time(ev[2]), ev[1].elapsed_time(ev[2])))
+        step_ms, attn_ms = (float(np.mean([x[i] for x in st])) for i in range(2))
+        res[variant] = {"step_ms": step_ms, "attn_ms": attn_ms, "tflops_step": flop / (step_ms * 1e-3) / 1e12}
+        if variant != "natural":
+            res[variant]["identity_heads"] = int(((flags & 64) != 0).sum().item())
+        log(f"{variant}: step {step_ms:.2f} ms, attention {attn_ms:.2f} ms")
+    print(json.dumps({
+        "mode": "producer", "workload": wl.name, "keep": keep, "diagonal": True, "density": nnz / (b_ * h_ * mb * mb),
+        "producer_ms": prod_ms,
+        "producer_roofline": {"bound": "hbm", "achieved": hbm_bytes / (prod_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "frac": hbm_bytes / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                              "algorithmic_bytes": hbm_bytes},
+        "path": res}), flush=True)
+    return 0
+
+
 def summarize_sweep(jsonl: str, out_md: str, command_note: str) -> None:
     recs = []
     with open(jsonl) as f:
@@ -403,6 +518,9 @@ def main() -> int:
     ap.add_argument("--sweep-points", default="", help="comma list of substrings selecting sweep points")
     ap.add_argument("--sweep-reps", type=int, default=5)
     ap.add_argument("--summarize-sweep", metavar="JSONL", help="write profiles/skip_sweep.md from a sweep's output")
+    ap.add_argument("--producer", action="store_true",
+                    help="time the pooled-score top-k mask producer and the path on its mask (JSON line)")
+    ap.add_argument("--producer-density", type=float, default=0.05, help="kept blocks per row / M_B")
     ap.add_argument("--sweep-command", default="", help="command line recorded in the sweep summary")
     args = ap.parse_args()
 
@@ -413,8 +531,11 @@ def main() -> int:
     if args.summarize_trace:
         stats_csv, bench_json = args.summarize_trace
         with open(bench_json) as f:
-            cfg = json.loads([ln for ln in f.read().splitlines() if ln.startswith("{")][-1])["config"]
-        md = os.path.join(ROOT, "profiles", f"attn_fwd_{cfg['workload']}_{cfg['variant']}_kernel_trace.md")
+            cfg = json.loads([ln for ln in f.read().splitlines() if ln.startswith("{")][-1]).get("config")
+        if cfg is None:
+            md = os.path.join(ROOT, "profiles", "mask_producer_produced-long-720p-401f_kernel_trace.md")
+        else:
+            md = os.path.join(ROOT, "profiles", f"attn_fwd_{cfg['workload']}_{cfg['variant']}_kernel_trace.md")
         summarize_trace(stats_csv, bench_json, md, args.trace_command)
         return 0
     if args.summarize_pmc:
@@ -433,6 +554,8 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.skip_sweep:
         return run_skip_sweep(args)
+    if args.producer:
+        return run_producer(args)
     if args.copy_calibration:
         n = args.copy_calibration * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")

@@ -9,8 +9,8 @@
 //   quant_kernel        int8 codes rint(mean * fl32(127 / max)), clamped to [-127, 127];
 //   score_select_kernel one workgroup per ROWS query blocks of a head: exact int32 scores
 //                       s_ij = sum_c qcode_i[c] kcode_j[c] (v_dot4_i32_i8) for every KV block j
-//                       into LDS, then one wavefront per row finds the k-th largest score by
-//                       bisection over the integer range, keeps every larger score, the first
+//                       into LDS, then one wavefront per row, holding the row in registers,
+//                       finds the k-th largest score by bisection over the integer range, keeps every larger score, the first
 //                       equal scores in ascending j up to k, and the diagonal if asked, and
 //                       writes the mask row.
 // Every step is exact or a single float32 rounding in a fixed order, so the mask is the same bit
@@ -20,12 +20,13 @@
 
 #include "common.h"
 #include "producer_launch.h"
+#include "wavealign.h"
 
 namespace {
 
 constexpr int kPoolThreads = 256;
-constexpr int kRows = 8;          // query blocks per score_select workgroup
-constexpr int kSelThreads = 256;  // 4 wavefronts, 2 rows each
+constexpr int kRows = 4;          // query blocks per score_select workgroup
+constexpr int kSelThreads = 256;  // 4 wavefronts, one row each
 
 __global__ __launch_bounds__(64) void zero_amax_kernel(uint32_t* amax, int n) {
   for (int i = threadIdx.x; i < n; i += 64) amax[i] = 0u;
@@ -55,12 +56,12 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(WaProducerLaunch a) 
     const uint16_t* p = x + ((int64_t)bh * a.seq_len + t0) * D + 8 * g;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     int t = 0;
-    for (; t + 4 <= cnt; t += 4) {
-      uint4 v[4];
+    for (; t + 8 <= cnt; t += 8) {
+      uint4 v[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = *(const uint4*)(p + (int64_t)(t + u) * D);
+      for (int u = 0; u < 8; ++u) v[u] = *(const uint4*)(p + (int64_t)(t + u) * D);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 8; ++u) {
         acc[0] += bf16_lo(v[u].x);
         acc[1] += bf16_hi(v[u].x);
         acc[2] += bf16_lo(v[u].y);
@@ -124,6 +125,7 @@ __global__ __launch_bounds__(256) void quant_kernel(WaProducerLaunch a) {
 template <int D>
 __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLaunch a) {
   constexpr int W4 = D / 4;  // 32-bit words of one code row
+  constexpr int JT = WA_MAX_BLOCKS / 64;  // scores of one row per lane
   extern __shared__ __attribute__((aligned(16))) int32_t sc[];  // [kRows][mb] scores
   __shared__ int32_t qs[kRows][W4];
   const int tiles = (a.mb + kRows - 1) / kRows;
@@ -158,49 +160,60 @@ __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLau
     for (int r = 0; r < kRows; ++r) sc[r * mb + j] = s[r];
   }
   __syncthreads();
-  // selection: wavefront w handles rows w and w + 4
-  const int lane = tid & 63, wv = tid >> 6;
+  // selection: wavefront w handles row w, with the row's scores in registers (entry t of lane l is
+  // block 64 t + l; entries past the row hold INT32_MIN and are never counted)
+  const int lane = tid & 63, r = tid >> 6;
+  if (r >= nr) return;
   const int keep = a.keep < mb ? a.keep : mb;
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-  for (int r = wv; r < nr; r += kSelThreads / 64) {
-    const int32_t* row = sc + r * mb;
-    const int i = r0 + r;
-    // k-th largest value v: the largest v with #{s >= v} >= keep
-    int lo = INT32_MAX, hi = INT32_MIN;
-    for (int j = lane; j < mb; j += 64) {
-      lo = min(lo, row[j]);
-      hi = max(hi, row[j]);
+  const int32_t* row = sc + r * mb;
+  const int i = r0 + r;
+  int32_t val[JT];
+#pragma unroll
+  for (int t = 0; t < JT; ++t) {
+    const int j = 64 * t + lane;
+    val[t] = j < mb ? row[j] : INT32_MIN;
+  }
+  // k-th largest value v: the largest v with #{s >= v} >= keep
+  int lo = INT32_MAX, hi = INT32_MIN;
+#pragma unroll
+  for (int t = 0; t < JT; ++t)
+    if (64 * t + lane < mb) {
+      lo = min(lo, val[t]);
+      hi = max(hi, val[t]);
     }
-    for (int o = 32; o > 0; o >>= 1) {
-      lo = min(lo, __shfl_xor(lo, o));
-      hi = max(hi, __shfl_xor(hi, o));
-    }
-    // invariant: #{s >= lo} >= keep (lo = min counts every entry), #{s >= hi + 1} < keep
-    while (keep > 0 && lo < hi) {
-      const int mid = lo + (int)(((int64_t)hi - lo + 1) / 2);
-      int c = 0;
-      for (int j = lane; j < mb; j += 64) c += row[j] >= mid;
-      for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
-      if (c >= keep) lo = mid; else hi = mid - 1;
-    }
-    const int v = lo;
-    int greater = 0;
-    for (int j = lane; j < mb; j += 64) greater += row[j] > v;
-    for (int o = 32; o > 0; o >>= 1) greater += __shfl_xor(greater, o);
-    const int ties = keep - greater;  // equal scores to keep, in ascending j
-    uint8_t* out = a.mask + ((int64_t)bh * mb + i) * mb;
-    int seen = 0;
-    for (int j0 = 0; j0 < mb; j0 += 64) {
-      const int j = j0 + lane;
-      const int sv = j < mb ? row[j] : INT32_MIN;
-      const bool eq = j < mb && keep > 0 && sv == v;
-      const uint64_t eqw = __ballot(eq);
-      const int rank = seen + __popcll(eqw & below);
-      const bool kept = keep > 0 && (sv > v || (eq && rank < ties));
-      const bool diag = a.diagonal && j == i;
-      if (j < mb) out[j] = (kept || diag) ? 1 : 0;
-      seen += __popcll(eqw);
-    }
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = min(lo, __shfl_xor(lo, o));
+    hi = max(hi, __shfl_xor(hi, o));
+  }
+  // invariant: #{s >= lo} >= keep (lo = the minimum counts every entry), #{s >= hi + 1} < keep
+  while (keep > 0 && lo < hi) {
+    const int mid = lo + (int)(((int64_t)hi - lo + 1) / 2);
+    int c = 0;
+#pragma unroll
+    for (int t = 0; t < JT; ++t) c += val[t] >= mid;
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+    if (c >= keep) lo = mid; else hi = mid - 1;
+  }
+  const int v = lo;
+  int greater = 0;
+#pragma unroll
+  for (int t = 0; t < JT; ++t) greater += val[t] > v;
+  for (int o = 32; o > 0; o >>= 1) greater += __shfl_xor(greater, o);
+  const int ties = keep - greater;  // equal scores to keep, in ascending j
+  uint8_t* out = a.mask + ((int64_t)bh * mb + i) * mb;
+  int seen = 0;
+#pragma unroll
+  for (int t = 0; t < JT; ++t) {
+    const int j = 64 * t + lane;
+    const bool in = j < mb;
+    const bool eq = in && keep > 0 && val[t] == v;
+    const uint64_t eqw = __ballot(eq);
+    const int rank = seen + __popcll(eqw & below);
+    const bool kept = keep > 0 && in && (val[t] > v || (eq && rank < ties));
+    const bool diag = a.diagonal && j == i;
+    if (in) out[j] = (kept || diag) ? 1 : 0;
+    seen += __popcll(eqw);
   }
 }
 
