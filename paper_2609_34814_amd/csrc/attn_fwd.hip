@@ -63,6 +63,11 @@ constexpr float kRescale = 8.0f;  // log2 headroom of the lazily rescaled runnin
 // memory accesses across it
 #define WA_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
+// Scheduling fence: no instruction moves across it. Placed between the operand reads of k-step s+1
+// and the MFMAs of k-step s, it keeps those reads in flight while the MFMAs run (left alone, the
+// scheduler sinks every read to just before its MFMA, and each MFMA then waits out an LDS latency).
+#define WA_SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -328,9 +333,11 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
             for (int kt = 0; kt < C::KT; ++kt)
               a_nxt[kt] = lds_chunk<C::RB>(k_lds, kt * 32 + krow_lane, 2 * (s + 1) + hf);
           }
+          WA_SCHED_FENCE();
 #pragma unroll
           for (int kt = 0; kt < C::KT; ++kt)
             sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a_cur[kt]), qf[s], sacc[kt], 0, 0, 0);
+          WA_SCHED_FENCE();
 #pragma unroll
           for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = a_nxt[kt];
         }
