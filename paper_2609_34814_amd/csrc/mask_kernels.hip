@@ -1,11 +1,15 @@
 // Mask scans for gfx950: row counts, per-row KV-index lists, and the bit-packed
 // row and column masks that the permutation builder iterates over.
 //
-// A wavefront scans one mask row 64 columns at a time: lane l tests column
-// 64t + l, a ballot gives the 64-bit word of kept columns, and the popcount of
-// the word below lane l is the lane's rank among the kept columns. Indices are
-// therefore written in ascending column order (the order in which the attention
-// kernel visits KV blocks) and the result is independent of scheduling.
+// A wavefront scans one mask row 1024 columns at a time: lane l takes columns
+// [1024t + 16l, +16) with 16-byte loads (mask rows start at any byte, so a lane
+// reads the aligned 16-byte chunk holding its first column and, when its columns
+// cross into the next chunk, that one too, and byte-aligns the pair). Each load
+// covers at least one byte of the row, so it never leaves the pages that hold
+// the mask. Kept-column counts are popcounts; the lanes' exclusive prefix sum
+// ranks their columns, so indices are written in ascending column order (the
+// order in which the attention kernel visits KV blocks) and the result is
+// independent of scheduling.
 
 #include "common.h"
 #include "perm_launch.h"
@@ -16,6 +20,52 @@ constexpr int kWavesPerWG = 4;
 
 __device__ __forceinline__ uint64_t ballot64(bool p) { return __ballot(p); }
 
+// One bit per byte of w (bit i = byte i is nonzero).
+__device__ __forceinline__ uint32_t nz_nibble(uint32_t w) {
+  uint32_t t = ((w & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | w;
+  t = (t >> 7) & 0x01010101u;
+  return (t | (t >> 7) | (t >> 14) | (t >> 21)) & 0xFu;
+}
+
+// Nonzero mask of the bytes p[0 .. valid), valid in 1..16 (bit b = byte b). The byte offset of p
+// within its 16-byte chunk must be the same in every lane of the wavefront.
+__device__ __forceinline__ uint32_t nz16(const uint8_t* p, int valid) {
+  const uintptr_t addr = (uintptr_t)p;
+  const uint8_t* a = p - (addr & 15);
+  const int d = (int)(addr & 15);
+  const uint4 c0 = *(const uint4*)a;
+  uint4 c1 = make_uint4(0u, 0u, 0u, 0u);
+  if (d + valid > 16) c1 = *(const uint4*)(a + 16);
+  const uint32_t w[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+  const uint32_t r = (uint32_t)(d & 3);
+  uint32_t o[4];
+  switch (d >> 2) {  // uniform
+    case 0:
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 1], w[i], r);
+      break;
+    case 1:
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 2], w[i + 1], r);
+      break;
+    case 2:
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 3], w[i + 2], r);
+      break;
+    default:
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 4], w[i + 3], r);
+      break;
+  }
+  const uint32_t bits = nz_nibble(o[0]) | (nz_nibble(o[1]) << 4) | (nz_nibble(o[2]) << 8) | (nz_nibble(o[3]) << 12);
+  return valid >= 16 ? bits : bits & ((1u << valid) - 1u);
+}
+
+// Kept-column mask of columns [col0, col0 + 16) of a row of n bytes (0 past the end).
+__device__ __forceinline__ uint32_t row_bits16(const uint8_t* rowp, int n, int col0) {
+  return col0 < n ? nz16(rowp + col0, min(16, n - col0)) : 0u;
+}
+
 // counts[(row / mb) * count_stride_rows + counts_offset + row % mb] = n_row
 __global__ __launch_bounds__(256) void row_count_kernel(const uint8_t* __restrict__ mask, int64_t rows, int n,
                                                          int32_t* __restrict__ counts, int64_t stride, int offset,
@@ -25,7 +75,7 @@ __global__ __launch_bounds__(256) void row_count_kernel(const uint8_t* __restric
   const int lane = threadIdx.x & 63;
   const uint8_t* p = mask + row * n;
   int cnt = 0;
-  for (int j = lane; j < n; j += 64) cnt += p[j] != 0;
+  for (int c0 = 0; c0 < n; c0 += 1024) cnt += __popc(row_bits16(p, n, c0 + 16 * lane));
   for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
   if (lane == 0) counts[(row / mb) * stride + offset + row % mb] = cnt;
 }
@@ -67,14 +117,23 @@ __global__ __launch_bounds__(256) void row_write_kernel(const uint8_t* __restric
   const int i = (int)(row % mb);
   const uint8_t* p = mask + row * n;
   int32_t* out = col_idx + h * (int64_t)mb * n + row_ptr[h * (mb + 1) + i];
-  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int base = 0;
-  for (int j0 = 0; j0 < n; j0 += 64) {
-    const int j = j0 + lane;
-    const bool keep = j < n && p[j] != 0;
-    const uint64_t word = ballot64(keep);
-    if (keep) out[base + __popcll(word & below)] = j;
-    base += __popcll(word);
+  for (int c0 = 0; c0 < n; c0 += 1024) {
+    const int col = c0 + 16 * lane;
+    uint32_t bits = row_bits16(p, n, col);
+    const int cnt = __popc(bits);
+    int incl = cnt;  // inclusive prefix sum over the lanes
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(incl, o);
+      if (lane >= o) incl += u;
+    }
+    int pos = base + incl - cnt;
+    while (bits) {
+      out[pos++] = col + __ffs((int)bits) - 1;
+      bits &= bits - 1u;
+    }
+    base += __shfl(incl, 63);
   }
 }
 
@@ -90,12 +149,16 @@ __global__ __launch_bounds__(256) void pack_rows_kernel(const uint8_t* __restric
   const int i = (int)(row % m);
   const uint8_t* p = mask + row * n;
   int cnt = 0;
-  for (int w = 0; w < nw; ++w) {
-    const int j = w * 64 + lane;
-    const uint64_t word = ballot64(j < n && p[j] != 0);
-    if (lane == 0) rowbits[(h * nw + w) * m + i] = word;
-    cnt += __popcll(word);
+  for (int c0 = 0; c0 < n; c0 += 1024) {
+    const uint32_t b = row_bits16(p, n, c0 + 16 * lane);
+    cnt += __popc(b);
+    // lanes 4k .. 4k+3 hold the 64 columns of word c0 / 64 + k
+    const uint64_t word = (uint64_t)b | ((uint64_t)__shfl_down(b, 1) << 16) | ((uint64_t)__shfl_down(b, 2) << 32) |
+                          ((uint64_t)__shfl_down(b, 3) << 48);
+    const int w = c0 / 64 + (lane >> 2);
+    if ((lane & 3) == 0 && w < nw) rowbits[(h * nw + w) * m + i] = word;
   }
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
   if (lane == 0) row_nnz[row] = cnt;
 }
 
