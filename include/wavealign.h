@@ -14,8 +14,8 @@
  *   - Tensor and mask pointers are DEVICE pointers owned by the caller.
  *     Scalar parameter structs are HOST pointers, read during the call only.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
- *     and is asynchronous: no entry point synchronises, allocates device
- *     memory or frees caller memory. Scratch memory comes from the caller's
+ *     and is asynchronous: no entry point synchronises (except the debugging
+ *     check wa_check_perm), allocates device memory or frees caller memory. Scratch memory comes from the caller's
  *     `workspace` (device memory, 256-byte aligned, of at least the size the
  *     matching *_workspace_size call reports).
  *   - Every argument is validated before anything is enqueued; on error the
@@ -54,6 +54,7 @@ typedef enum wa_status {
   WA_ERR_UNSUPPORTED = -2,  /* head_dim / block / size outside the supported set */
   WA_ERR_ALIGNMENT = -3,    /* tensor not 16-byte aligned, workspace not 256-byte aligned */
   WA_ERR_WORKSPACE = -4,    /* workspace smaller than required */
+  WA_ERR_INVALID_PERM = -5, /* wa_check_perm: some perm[b][h] is not a permutation of 0..M_B-1 */
   WA_ERR_HIP = -6           /* a HIP runtime call or kernel launch failed */
 } wa_status;
 
@@ -154,6 +155,19 @@ wa_status wa_perm_workspace_size(const wa_shape* shape, size_t* bytes);
 wa_status wa_build_permutation(const uint8_t* mask, const wa_shape* shape, const wa_perm_params* params,
                                int32_t* perm, int32_t* seg_start, uint8_t* head_flags, int32_t* embedding,
                                int32_t* stage1_order, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Debugging check of a permutation argument (Sec. IV-B: P_h is a permutation
+ * matrix): every perm[b][h] must hold each of 0..M_B-1 exactly once.
+ *   perm       int32 [B][H][M_B], device
+ *   head_ok    out int32 [B][H], device, nullable: 1 where the head's order is a
+ *              permutation, else 0
+ *   workspace  >= wa_check_perm_workspace_size(shape), 256-byte aligned
+ * Unlike every other entry point this call SYNCHRONISES `stream` (it copies the
+ * count of bad heads to the host) and returns WA_ERR_INVALID_PERM when any head
+ * fails, WA_OK otherwise. */
+wa_status wa_check_perm(const int32_t* perm, const wa_shape* shape, int32_t* head_ok, void* workspace,
+                        size_t workspace_bytes, void* stream);
+wa_status wa_check_perm_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Compacted per-row KV-block index lists (the mask-selected inner loop of Sec. II-C):
  *   row_ptr out int32 [B][H][M_B+1]: exclusive prefix sum of n_i, local to the head

@@ -12,6 +12,7 @@ WA_ERR_INVALID_ARG = -1
 WA_ERR_UNSUPPORTED = -2
 WA_ERR_ALIGNMENT = -3
 WA_ERR_WORKSPACE = -4
+WA_ERR_INVALID_PERM = -5
 WA_ERR_HIP = -6
 
 WA_SKIP_AUTO, WA_SKIP_NEVER, WA_SKIP_ALWAYS = 0, 1, 2
@@ -53,6 +54,8 @@ _SIGNATURES = {
                                        c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "wa_compact_mask": (c_int32, [c_void_p, POINTER(WaShape), c_void_p, c_void_p, c_void_p]),
     "wa_mask_producer_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
+    "wa_check_perm_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
+    "wa_check_perm": (c_int32, [c_void_p, POINTER(WaShape), c_void_p, c_void_p, c_size_t, c_void_p]),
     "wa_produce_block_mask": (c_int32, [c_void_p, c_void_p, POINTER(WaShape), c_int32, c_int32, c_void_p, c_void_p,
                                         c_void_p, c_size_t, c_void_p]),
     "wa_attn_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),

@@ -175,6 +175,28 @@ def produce_block_mask(q: torch.Tensor, k: torch.Tensor, *, block: int, keep: in
     return mask
 
 
+def check_perm(perm: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 128,
+               head_ok: Optional[torch.Tensor] = None) -> bool:
+    """True if every perm[b][h] is a permutation of 0..M_B-1 (synchronises the current stream)."""
+    lib = L.load()
+    _dev(perm, "perm")
+    if perm.dtype != torch.int32 or perm.dim() != 3:
+        raise ValueError("perm must be an int32 [B][H][M_B] tensor")
+    b, h, mb = perm.shape
+    shape = shape_of(b, h, seq_len, head_dim, block)
+    if -(-seq_len // block) != mb:
+        raise ValueError("perm's last dimension must be ceil(seq_len / block)")
+    n = ctypes.c_size_t(0)
+    L.check(lib.wa_check_perm_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
+    ws = _workspace(n.value, perm.device)
+    st = lib.wa_check_perm(_ptr(perm.contiguous()), ctypes.byref(shape), _ptr(head_ok), _ptr(ws), ws.numel(),
+                           _stream())
+    if st == L.WA_ERR_INVALID_PERM:
+        return False
+    L.check(st)
+    return True
+
+
 def _attn_args(q, k, v, block):
     for t, nm in ((q, "q"), (k, "k"), (v, "v")):
         _dev(t, nm)

@@ -209,6 +209,7 @@ const char* wa_status_string(wa_status s) {
     case WA_ERR_UNSUPPORTED: return "unsupported shape or parameter";
     case WA_ERR_ALIGNMENT: return "misaligned pointer";
     case WA_ERR_WORKSPACE: return "workspace too small";
+    case WA_ERR_INVALID_PERM: return "not a permutation";
     case WA_ERR_HIP: return "HIP runtime error";
   }
   return "unknown status";
@@ -350,6 +351,38 @@ wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* sh
   a.keep = keep; a.diagonal = diagonal ? 1 : 0;
   hipError_t e = wa_launch_producer(a, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "mask producer launch");
+  return ok();
+}
+
+wa_status wa_check_perm_workspace_size(const wa_shape* shape, size_t* bytes) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!bytes) return fail(WA_ERR_INVALID_ARG, "bytes is null");
+  *bytes = kAlign;
+  return ok();
+}
+
+wa_status wa_check_perm(const int32_t* perm, const wa_shape* shape, int32_t* head_ok, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!perm) return fail(WA_ERR_INVALID_ARG, "perm is null");
+  s = check_ws(workspace, workspace_bytes, kAlign);
+  if (s != WA_OK) return s;
+  hipStream_t st = (hipStream_t)stream;
+  int32_t* bad = (int32_t*)workspace;
+  hipError_t e = wa_launch_check_perm(perm, (int)d.bh, d.mb, bad, head_ok, st);
+  if (e != hipSuccess) return hip_fail(e, "check_perm launch");
+  int32_t host_bad = 0;
+  e = hipMemcpyAsync(&host_bad, bad, sizeof(host_bad), hipMemcpyDeviceToHost, st);
+  if (e != hipSuccess) return hip_fail(e, "check_perm copy");
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "check_perm synchronize");
+  if (host_bad != 0)
+    return fail(WA_ERR_INVALID_PERM, "%d of %lld heads hold no permutation of 0..%d", host_bad, (long long)d.bh,
+                d.mb - 1);
   return ok();
 }
 

@@ -13,6 +13,7 @@
 
 #include "common.h"
 #include "perm_launch.h"
+#include "wavealign.h"
 
 namespace {
 
@@ -186,6 +187,39 @@ __global__ __launch_bounds__(256) void transpose_bits_kernel(const uint64_t* __r
   if (j < n) colbits[(h * mw + v) * n + j] = out;
 }
 
+// Permutation check: one workgroup per head marks each entry in an LDS bitmap; an entry out of
+// range or already marked, or a bitmap with fewer than m marks, makes the head bad. bad[0] counts
+// bad heads (zeroed by the first workgroup's predecessor kernel); head_ok (nullable) gets 1 / 0.
+__global__ __launch_bounds__(64) void zero_counter_kernel(int32_t* c) {
+  if (threadIdx.x == 0) c[0] = 0;
+}
+
+__global__ __launch_bounds__(256) void check_perm_kernel(const int32_t* __restrict__ perm, int m,
+                                                         int32_t* __restrict__ bad, int32_t* __restrict__ head_ok) {
+  __shared__ uint32_t seen[WA_MAX_BLOCKS / 32];
+  __shared__ int fault;
+  const int64_t h = blockIdx.x;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < (m + 31) / 32; i += 256) seen[i] = 0u;
+  if (tid == 0) fault = 0;
+  __syncthreads();
+  const int32_t* p = perm + h * m;
+  for (int s = tid; s < m; s += 256) {
+    const int32_t r = p[s];
+    if (r < 0 || r >= m) {
+      fault = 1;
+    } else {
+      const uint32_t bit = 1u << (r & 31);
+      if (atomicOr(&seen[r >> 5], bit) & bit) fault = 1;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    if (head_ok) head_ok[h] = fault ? 0 : 1;
+    if (fault) atomicAdd(bad, 1);
+  }
+}
+
 // Each workgroup records the XCD it runs on (hardware register XCC_ID, bits [3:0]).
 __global__ void xcc_probe_kernel(int32_t* out, int n) {
   if (threadIdx.x == 0 && (int)blockIdx.x < n)
@@ -193,6 +227,15 @@ __global__ void xcc_probe_kernel(int32_t* out, int n) {
 }
 
 }  // namespace
+
+hipError_t wa_launch_check_perm(const int32_t* perm, int bh, int m, int32_t* bad, int32_t* head_ok,
+                                hipStream_t stream) {
+  hipLaunchKernelGGL(zero_counter_kernel, dim3(1), dim3(64), 0, stream, bad);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || bh <= 0) return e;
+  hipLaunchKernelGGL(check_perm_kernel, dim3(bh), dim3(256), 0, stream, perm, m, bad, head_ok);
+  return hipGetLastError();
+}
 
 hipError_t wa_launch_xcc_probe(int32_t* out, int n_wg, hipStream_t stream) {
   if (n_wg <= 0) return hipSuccess;

@@ -52,3 +52,5 @@ hipError_t wa_launch_pack_rows(const uint8_t* mask, int64_t rows, int m, int n, 
 hipError_t wa_launch_transpose_bits(const uint64_t* rowbits, int bh, int m, int n, uint64_t* colbits,
                                     hipStream_t stream);
 hipError_t wa_launch_xcc_probe(int32_t* out, int n_wg, hipStream_t stream);
+hipError_t wa_launch_check_perm(const int32_t* perm, int bh, int m, int32_t* bad, int32_t* head_ok,
+                                hipStream_t stream);

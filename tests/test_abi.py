@@ -140,6 +140,18 @@ def test_produce_block_mask_validation():
                                      1 << 30, None) == L.WA_ERR_UNSUPPORTED
 
 
+def test_check_perm_validation():
+    lib = _lib()
+    s = _shape()
+    n = ctypes.c_size_t(0)
+    assert lib.wa_check_perm_workspace_size(ctypes.byref(s), ctypes.byref(n)) == 0 and n.value >= 4
+    ws = ctypes.c_void_p(1 << 24)
+    assert lib.wa_check_perm(None, ctypes.byref(s), None, ws, n.value, None) == L.WA_ERR_INVALID_ARG
+    assert lib.wa_check_perm(FAKE, ctypes.byref(s), None, ws, 0, None) == L.WA_ERR_WORKSPACE
+    assert lib.wa_check_perm(FAKE, ctypes.byref(s), None, None, n.value, None) == L.WA_ERR_INVALID_ARG
+    assert lib.wa_status_string(L.WA_ERR_INVALID_PERM) == b"not a permutation"
+
+
 def test_build_permutation_validation():
     lib = _lib()
     s = _shape()

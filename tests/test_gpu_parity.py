@@ -384,3 +384,26 @@ def test_max_blocks_attention():
     st = compare_blocks(_DeviceRows(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
     print(wl.name, st)
     _check(st)
+
+
+# ------------------------------------------------------------------------------------------------
+# the permutation check (debugging entry point)
+# ------------------------------------------------------------------------------------------------
+def test_check_perm():
+    wl = CONFIGS["wan1.3b-480p-81f"]
+    W_ = _w()
+    md = u8_dev(make_mask(wl))
+    perm, _, _ = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim, skip="never")
+    ok = torch.empty((wl.batch, wl.heads), dtype=torch.int32, device="cuda")
+    assert W_.check_perm(perm, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim, head_ok=ok)
+    assert bool((ok == 1).all())
+    bad = perm.clone()
+    bad[0, 3, 10] = bad[0, 3, 11]          # a duplicate (and a missing row)
+    bad[0, 7, 0] = wl.mb                   # out of range
+    bad[0, 9, 5] = -1
+    assert not W_.check_perm(bad, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim, head_ok=ok)
+    want = np.ones((wl.batch, wl.heads), dtype=np.int32)
+    want[0, [3, 7, 9]] = 0
+    assert np.array_equal(ok.cpu().numpy(), want)
+    one = torch.zeros((1, 2, 1), dtype=torch.int32, device="cuda")   # M_B = 1
+    assert W_.check_perm(one, seq_len=50, block=64, head_dim=64)
