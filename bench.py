@@ -578,6 +578,15 @@ def main() -> int:
     md = torch.from_numpy(mask).cuda()
     nnz = int(mask.sum(dtype=np.int64))
     flop = 4.0 * wl.block * wl.block * wl.head_dim * nnz
+    # compulsory bytes of one attention call: Q read and O written once, every distinct K/V block of a
+    # head read once (the ragged last block at its true size), and the KV index lists
+    blk_tokens = np.full(wl.mb, wl.block, dtype=np.int64)
+    blk_tokens[-1] = wl.seq_len - (wl.mb - 1) * wl.block
+    used = mask.any(axis=2)                              # [B][H][N_B]
+    kv_bytes = int((used * blk_tokens).sum()) * wl.head_dim * 2 * 2
+    qo_bytes = 2 * wl.batch * wl.heads * wl.seq_len * wl.head_dim * 2
+    list_bytes = 4 * nnz
+    algo_bytes = kv_bytes + qo_bytes + list_bytes
     b_, h_, mb = wl.batch, wl.heads, wl.mb
     shape = W.shape_of(b_, h_, wl.seq_len, wl.head_dim, wl.block)
     perm_ws = torch.empty(W.perm_workspace_size(shape), dtype=torch.uint8, device="cuda")
@@ -621,6 +630,8 @@ def main() -> int:
 
         def step(ev=None):
             p, sg = fixed, None
+            if ev is not None:
+                ev[2].record(stream)
             if spec["perm"] in ("two-stage", "stage1"):
                 W.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
                                     wave=wave * spec.get("wave_mult", 1), n_xcd=n_xcd, skip=spec["skip"],
@@ -628,6 +639,8 @@ def main() -> int:
                                     stage1_out=s1)
                 p = s1 if s1 is not None else perm
                 sg = seg_q
+            if ev is not None:
+                ev[3].record(stream)
             rp, ci = W.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
                                     row_ptr=row_ptr, col_idx=col_idx)
             if ev is not None:
@@ -643,7 +656,8 @@ def main() -> int:
         for _ in range(args.warmup):
             step()
         torch.cuda.synchronize()
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        # per step: [0] attention start, [1] attention end, [2] step start, [3] permutation end
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         w0 = time.perf_counter()
@@ -654,8 +668,11 @@ def main() -> int:
         torch.cuda.synchronize()
         wall = time.perf_counter() - w0
         ms_step = start.elapsed_time(end) / args.steps
-        attn_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+        attn_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+        perm_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+        compact_ms = float(np.mean([e[3].elapsed_time(e[0]) for e in evs]))
         results[variant] = dict(ms_per_step=ms_step, wall_ms_per_step=wall * 1e3 / args.steps, attn_ms=attn_ms,
+                                perm_ms=perm_ms, compact_ms=compact_ms,
                                 tflops_step=flop / (ms_step * 1e-3) / 1e12,
                                 tflops_attn=flop / (attn_ms * 1e-3) / 1e12)
         log(f"{variant}: step {ms_step:.2f} ms, attention kernel {attn_ms:.2f} ms "
@@ -689,6 +706,8 @@ def main() -> int:
                    "block": wl.block, "kept_blocks": nnz, "density": nnz / (b_ * h_ * mb * mb),
                    "flop_per_step": flop, "variant": head, "wave_per_xcd": wave},
         "roofline": roof,
+        "algorithmic_bytes": {"kv_compulsory": kv_bytes, "q_and_o": qo_bytes, "kv_lists": list_bytes,
+                              "total": algo_bytes, "flop_per_byte": flop / algo_bytes},
         "variants": results,
     }
     if "natural" in results and "reordered" in results:
