@@ -234,6 +234,21 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
   const float c2 = a.scale * kLog2e;
 
   const int home = (int)(__builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 0xF) % a.n_xcd;
+  // byte offsets of this lane's K-operand chunk of k-step s in the K tile (key tile kt adds kt 32 RB)
+  uint32_t kofs[C::KS];
+  {
+    const int kr = 16 * ((lane & 31) >> 4) + perm16(lane & 15);
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s) kofs[s] = (uint32_t)(kr * C::RB + swz_k<C::RB>(kr, 2 * s + hf) * 16);
+  }
+  // the same for the V^T operand of k-step ks (16 keys; d tile dt adds dt 32 VRB)
+  uint32_t vofs[2 * C::KT];
+  {
+    const int kr = 16 * ((lane & 31) >> 4) + perm16(lane & 15);
+#pragma unroll
+    for (int ks = 0; ks < 2 * C::KT; ++ks)
+      vofs[ks] = (uint32_t)(kr * C::VRB + swz_k<C::VRB>(kr, 2 * ks + hf) * 16);
+  }
 
   for (;;) {
     if (tid == 0) {
@@ -298,11 +313,11 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     int e = beg;
     auto kv_block = [&](auto masked_tag) {
       constexpr bool MASKED = decltype(masked_tag)::value;
-      // Per-lane LDS and copy offsets are recomputed in every block from an opaque copy of the lane
-      // index: hoisted out of the loop they would hold ~36 registers that the operand reads need.
+      // The per-lane copy offsets are recomputed in every block from an opaque copy of the lane index
+      // (hoisted out of the loop they would hold registers that the operand reads need); the operand
+      // read offsets, one per k-step, are computed once per kernel (kofs, vofs).
       int lane_o = lane;
       asm volatile("" : "+v"(lane_o));
-      const int krow_lane = 16 * ((lane_o & 31) >> 4) + perm16(lane_o & 15);
       const bool has_next = e + 1 < end;
       int j_next = 0;
       if (has_next) {
@@ -325,13 +340,13 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       {
         uint4 a_cur[C::KT], a_nxt[C::KT];
 #pragma unroll
-        for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = lds_chunk<C::RB>(k_lds, kt * 32 + krow_lane, hf);
+        for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = *(const uint4*)(k_lds + kofs[0] + kt * 32 * C::RB);
 #pragma unroll
         for (int s = 0; s < C::KS; ++s) {
           if (s + 1 < C::KS) {
 #pragma unroll
             for (int kt = 0; kt < C::KT; ++kt)
-              a_nxt[kt] = lds_chunk<C::RB>(k_lds, kt * 32 + krow_lane, 2 * (s + 1) + hf);
+              a_nxt[kt] = *(const uint4*)(k_lds + kofs[s + 1] + kt * 32 * C::RB);
           }
           WA_SCHED_FENCE();
 #pragma unroll
@@ -404,13 +419,13 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
         // k-step ks = 2 kt + k2 (16 keys); operand reads of step ks+1 in flight during step ks
         uint4 a_cur[C::DT], a_nxt[C::DT];
 #pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt) a_cur[dt] = lds_chunk<C::VRB>(v_lds, dt * 32 + krow_lane, hf);
+        for (int dt = 0; dt < C::DT; ++dt) a_cur[dt] = *(const uint4*)(v_lds + vofs[0] + dt * 32 * C::VRB);
 #pragma unroll
         for (int ks = 0; ks < 2 * C::KT; ++ks) {
           if (ks + 1 < 2 * C::KT) {
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt)
-              a_nxt[dt] = lds_chunk<C::VRB>(v_lds, dt * 32 + krow_lane, 2 * (ks + 1) + hf);
+              a_nxt[dt] = *(const uint4*)(v_lds + vofs[ks + 1] + dt * 32 * C::VRB);
           }
           const uint32_t* p = &pb[ks >> 1][4 * (ks & 1)];
           const bf16x8 bv = as_bf16x8(make_uint4(p[0], p[1], p[2], p[3]));
