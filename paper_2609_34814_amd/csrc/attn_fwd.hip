@@ -55,7 +55,9 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr float kRescale = 8.0f;  // log2 headroom of the lazily rescaled running maximum
+// Probabilities are taken against the first block's row maximum; a row in which one reaches this
+// bound is recomputed against its exact maximum (fp32 and bf16 hold values up to it exactly scaled).
+constexpr float kProbLimit = 4294967296.0f;  // 2^32
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
 #define WA_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14))
@@ -224,6 +226,7 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
   __shared__ __attribute__((aligned(1024))) unsigned char k_lds[C::TBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char v_lds[C::TBYTES];
   __shared__ int task[2];
+  __shared__ int redo;  // the current row is recomputed against its exact maximum
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -256,6 +259,7 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       if (!fetch_task(a, home, &tb, &ts)) tb = -1;
       task[0] = tb;
       task[1] = ts;
+      redo = 0;
     }
     __syncthreads();
     const int bh = __builtin_amdgcn_readfirstlane(task[0]);
@@ -288,31 +292,67 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       qf[s] = as_bf16x8(val);
     }
 
-    int j_cur = 0;
-    if (beg < end) {
-      j_cur = cols[beg];
-      if ((unsigned)j_cur >= (unsigned)a.mb) j_cur = 0;
-      issue_tile<D, BLK, false>(k_lds, kg, j_cur * BLK, n, w, lane);
-      issue_vt<D, BLK>(v_lds, vtg, vt_row_bytes, j_cur * BLK, w, lane);
-    }
-    // the Q loads (issued first) are complete; the first tiles stay in flight
-    WA_WAIT_VM(2 * C::NK);
-
     f32x16 oacc[C::DT];
-#pragma unroll
-    for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
-
-    float m_run = -INFINITY;
+    float m_run = -INFINITY;  // reference maximum (log2 units), set by the row's first block
     float l_run = 0.f;
+    int j_cur = 0;
 
-    // One KV block: wait for its tiles, S^T = K_j Q^T, online softmax, O^T += V_j^T P^T, and keep the
-    // copies of the next block in flight. MASKED handles the ragged last block (keys past the end of
-    // the sequence score -inf); the lists are ascending, so it can only be a row's last block.
+    // S^T = K_j Q^T from the K tile in LDS. Consecutive MFMAs go to different accumulators (a chain on
+    // one accumulator would wait for each result), and the operand reads of k-step s+1 are in flight
+    // during the MFMAs of step s.
+    auto scores = [&](f32x16 (&sacc)[C::KT]) {
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[kt][v] = 0.f;
+      uint4 a_cur[C::KT], a_nxt[C::KT];
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = *(const uint4*)(k_lds + kofs[0] + kt * 32 * C::RB);
+#pragma unroll
+      for (int s = 0; s < C::KS; ++s) {
+        if (s + 1 < C::KS) {
+#pragma unroll
+          for (int kt = 0; kt < C::KT; ++kt) a_nxt[kt] = *(const uint4*)(k_lds + kofs[s + 1] + kt * 32 * C::RB);
+        }
+        WA_SCHED_FENCE();
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt)
+          sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a_cur[kt]), qf[s], sacc[kt], 0, 0, 0);
+        WA_SCHED_FENCE();
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = a_nxt[kt];
+      }
+    };
+    // keys past the end of the sequence (ragged last block) score -inf
+    auto mask_tail = [&](f32x16 (&sacc)[C::KT], int nvalid, int lane_o) {
+      const int hf_o = lane_o >> 5;  // from the opaque lane copy: no key table held across blocks
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kt * 32 + 16 * (v >> 3) + 8 * hf_o + (v & 7);
+          if (key >= nvalid) sacc[kt][v] = -INFINITY;
+        }
+    };
+    // row maximum of a score tile, in log2 units (shared by the two lanes of a query)
+    auto tile_max = [&](const f32x16 (&sacc)[C::KT]) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kt][v]);
+      return fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+    };
+
+    // One KV block: wait for its tiles, S^T = K_j Q^T, softmax numerators, O^T += V_j^T P^T, and keep
+    // the copies of the next block in flight. MASKED handles the ragged last block; the lists are
+    // ascending, so it can only be a row's last block. FIRST takes the block's row maximum as the
+    // softmax reference of the row: every later probability is taken against it, so O and l are never
+    // rescaled (a row whose probabilities outgrow the reference is recomputed, below).
     int e = beg;
-    auto kv_block = [&](auto masked_tag) {
+    auto kv_block = [&](auto masked_tag, auto first_tag) {
       constexpr bool MASKED = decltype(masked_tag)::value;
+      constexpr bool FIRST = decltype(first_tag)::value;
       // The per-lane copy offsets are recomputed in every block from an opaque copy of the lane index
       // (hoisted out of the loop they would hold registers that the operand reads need); the operand
       // read offsets, one per k-step, are computed once per kernel (kofs, vofs).
@@ -328,71 +368,15 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       // K_j resident (V_j may still be in flight)
       WA_WAIT_VM(C::NK);
       WA_BARRIER();
-
-      // ---- S^T = K_j Q^T ----
-      // consecutive MFMAs go to different accumulators (a chain on one accumulator would wait for
-      // each result), and the operand reads of k-step s+1 are in flight during the MFMAs of step s
       f32x16 sacc[C::KT];
-#pragma unroll
-      for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[kt][v] = 0.f;
-      {
-        uint4 a_cur[C::KT], a_nxt[C::KT];
-#pragma unroll
-        for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = *(const uint4*)(k_lds + kofs[0] + kt * 32 * C::RB);
-#pragma unroll
-        for (int s = 0; s < C::KS; ++s) {
-          if (s + 1 < C::KS) {
-#pragma unroll
-            for (int kt = 0; kt < C::KT; ++kt)
-              a_nxt[kt] = *(const uint4*)(k_lds + kofs[s + 1] + kt * 32 * C::RB);
-          }
-          WA_SCHED_FENCE();
-#pragma unroll
-          for (int kt = 0; kt < C::KT; ++kt)
-            sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a_cur[kt]), qf[s], sacc[kt], 0, 0, 0);
-          WA_SCHED_FENCE();
-#pragma unroll
-          for (int kt = 0; kt < C::KT; ++kt) a_cur[kt] = a_nxt[kt];
-        }
-      }
+      scores(sacc);
       // every wavefront is done with K_j: start K_{j+1}
       WA_BARRIER();
       if (has_next) issue_tile<D, BLK, false>(k_lds, kg, j_next * BLK, n, w, lane_o);
 
-      // ---- online softmax (log2 domain) ----
-      if constexpr (MASKED) {
-        const int nvalid = n - j_cur * BLK;
-        const int hf = lane_o >> 5;  // from the opaque lane copy: no key table held across blocks
-#pragma unroll
-        for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int key = kt * 32 + 16 * (v >> 3) + 8 * hf + (v & 7);
-            if (key >= nvalid) sacc[kt][v] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kt][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
-      // Lazy rescaling: the running maximum is raised (and O, l rescaled) only when some query of the
-      // wavefront sees a score above it by more than kRescale; otherwise the probabilities are taken
-      // against the old maximum and stay below 2^kRescale.
-      if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescale)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) oacc[t][v] *= alpha;
-      }
-
+      // ---- softmax numerators (log2 domain) ----
+      if constexpr (MASKED) mask_tail(sacc, n - j_cur * BLK, lane_o);
+      if constexpr (FIRST) m_run = tile_max(sacc);
       float lsum = 0.f;
       uint32_t pb[C::KT][8];
 #pragma unroll
@@ -442,8 +426,65 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       j_cur = j_next;
     };
     const bool ragged_last = end > beg && (n % BLK) != 0 && cols[end - 1] == a.mb - 1;
-    for (; e < end - (ragged_last ? 1 : 0); ++e) kv_block(std::false_type{});
-    if (ragged_last) kv_block(std::true_type{});
+    const int e_plain = end - (ragged_last ? 1 : 0);
+
+    // Pass 0 takes the first block's maximum as the reference. If some probability reached
+    // kProbLimit (a later score above the reference by log2(kProbLimit) or more, in log2 units), the
+    // whole workgroup recomputes the row: the exact row maximum over all its blocks first, then
+    // pass 1 against it (every probability <= 1). The decision is per workgroup, since its wavefronts
+    // share the tile copies.
+    for (int pass = 0;; ++pass) {
+      if (beg < end) {
+        j_cur = cols[beg];
+        if ((unsigned)j_cur >= (unsigned)a.mb) j_cur = 0;
+        issue_tile<D, BLK, false>(k_lds, kg, j_cur * BLK, n, w, lane);
+        issue_vt<D, BLK>(v_lds, vtg, vt_row_bytes, j_cur * BLK, w, lane);
+      }
+      // the Q loads (issued first) are complete; the first tiles stay in flight
+      WA_WAIT_VM(2 * C::NK);
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
+      l_run = 0.f;
+      e = beg;
+      if (e < e_plain) {
+        if (pass == 0) {
+          kv_block(std::false_type{}, std::true_type{});
+        } else {
+          kv_block(std::false_type{}, std::false_type{});
+        }
+        for (++e; e < e_plain; ++e) kv_block(std::false_type{}, std::false_type{});
+        if (ragged_last) kv_block(std::true_type{}, std::false_type{});
+      } else if (ragged_last) {
+        if (pass == 0) {
+          kv_block(std::true_type{}, std::true_type{});
+        } else {
+          kv_block(std::true_type{}, std::false_type{});
+        }
+      }
+      if (pass > 0) break;
+      if (__builtin_amdgcn_ballot_w64(!(l_run < kProbLimit)) && lane == 0) redo = 1;  // also inf / NaN
+      __syncthreads();
+      const int again = __builtin_amdgcn_readfirstlane(redo);
+      __syncthreads();  // every wavefront has read the flag before the next row clears it
+      if (!again) break;
+      // exact row maximum: K tiles one at a time, scores only
+      float mx = -INFINITY;
+      for (int e2 = beg; e2 < end; ++e2) {
+        int j = cols[e2];
+        if ((unsigned)j >= (unsigned)a.mb) j = 0;
+        issue_tile<D, BLK, false>(k_lds, kg, j * BLK, n, w, lane);
+        WA_WAIT_VM(0);
+        WA_BARRIER();
+        f32x16 sacc[C::KT];
+        scores(sacc);
+        if (j * BLK + BLK > n) mask_tail(sacc, n - j * BLK, lane);
+        mx = fmaxf(mx, tile_max(sacc));
+        WA_BARRIER();  // every wavefront is done with the tile before the next copy
+      }
+      m_run = mx;
+    }
 
     // ---- epilogue: normalise and store at the original rows ----
     const float ltot = l_run + __shfl_xor(l_run, 32);

@@ -237,6 +237,43 @@ def test_attention_sharp_logits():
     assert st["rel_rms"] <= 1e-2 and st["lse"] <= 1e-3, st
 
 
+def test_attention_scores_far_above_first_block():
+    """Rows whose later blocks score far above their first block take the exact-maximum recomputation.
+
+    The kernel takes each row's first kept block's maximum as the softmax reference; K of the upper
+    half of the blocks is scaled by 32 (exact in bf16), so rows that start in the lower half and reach
+    the upper half see probabilities far beyond 2^32 against it and must be recomputed. Rows that start
+    in the upper half keep the fast pass. Both must match the oracle, and O must not depend on the
+    row order.
+    """
+    wl = CONFIGS["tiny"]
+    q, k, v = make_qkv(wl)
+    mask = make_mask(wl)
+    kd = bf16_dev(k).float()
+    kd[:, :, wl.mb // 2 * wl.block:] *= 32
+    kd = kd.to(torch.bfloat16)
+    k_bits = kd.view(torch.int16).cpu().numpy().view(np.uint16)
+    first = np.argmax(mask != 0, axis=-1)
+    reaches_up = (mask[..., wl.mb // 2:] != 0).any(-1)
+    assert ((first < wl.mb // 2) & reaches_up).any() and (first >= wl.mb // 2).any()
+    o, lse = _run_attn(wl, mask, bf16_dev(q), kd, bf16_dev(v))
+    ref_o, ref_lse = A.block_sparse_attention(q, k_bits, v, mask, wl.block)
+    picks = [(0, h, i) for h in range(wl.heads) for i in range(wl.mb)]
+    ref = {p: (ref_o[0, p[1], slice(*A.block_token_range(p[2], wl.block, wl.seq_len))],
+               ref_lse[0, p[1], slice(*A.block_token_range(p[2], wl.block, wl.seq_len))]) for p in picks}
+    st = compare_blocks(dev_f64(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
+    print("far above first block", st)
+    assert np.isfinite(dev_f64(o)).all()
+    # one key dominates most rows: the bar of the sharp-logit case
+    vmax = float(np.abs(A.bf16_to_f64(v)).max())
+    assert st["max_abs"] <= 4 * 2.0 ** -9 * vmax, st
+    assert st["rel_rms"] <= 1e-2 and st["lse"] <= 1e-3, st
+    perm = torch.from_numpy(np.stack([np.random.default_rng(h).permutation(wl.mb) for h in range(wl.heads)])
+                            .astype(np.int32)[None]).cuda()
+    o2, lse2 = _run_attn(wl, mask, bf16_dev(q), kd, bf16_dev(v), perm=perm)
+    assert torch.equal(o.view(torch.int16), o2.view(torch.int16)) and torch.equal(lse, lse2)
+
+
 @pytest.mark.parametrize("name,count", [("wan1.3b-480p-81f", 48), ("skip-d64", 48), ("wan14b-720p-81f", 64)])
 def test_attention_sampled_vs_oracle(name, count):
     wl = CONFIGS[name]
