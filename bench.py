@@ -55,29 +55,35 @@ def load_traffic(workload: str, variant: str):
 
 
 def _pmc_means(csv_path: str, kernel_substr: str):
+    """Mean of every counter over the matching dispatches (and the mean dispatch duration in ns)."""
     import csv
     vals = {}
+    durs = {}
     with open(csv_path) as f:
         for r in csv.DictReader(f):
             if kernel_substr in r["Kernel_Name"]:
                 vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
-    return {k: sum(v) / len(v) for k, v in vals.items()}, max((len(v) for v in vals.values()), default=0)
+                durs[r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    out = {k: sum(v) / len(v) for k, v in vals.items()}
+    if durs:
+        out["duration_ns"] = sum(durs.values()) / len(durs)
+    return out, max((len(v) for v in vals.values()), default=0)
 
 
 PMC_PASSES = {
     "A": "TCC_HIT_sum TCC_MISS_sum SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE",
     "B": "FETCH_SIZE",
     "C": "WRITE_SIZE TCC_EA0_RDREQ_DRAM_sum",
+    "D": "TCP_TCC_READ_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_LEVEL_sum",
 }
 
 
 def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_note: str) -> None:
     """Turn rocprofv3 --pmc CSV passes into the traffic figure and a text summary.
 
-    Expects <root>/<variant>_{A,B,C}/run_counter_collection.csv for the attention kernel
-    (A: TCC_HIT_sum TCC_MISS_sum SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES
-    GRBM_GUI_ACTIVE; B: FETCH_SIZE; C: WRITE_SIZE TCC_EA0_RDREQ_DRAM_sum) and copy_{B,C} for a plain
-    1 GiB device copy, whose FETCH_SIZE / WRITE_SIZE give the byte-scaling factors.
+    Expects <root>/<variant>_{A,B,C,D}/run_counter_collection.csv for the attention kernel (the
+    counters of PMC_PASSES; pass D is optional) and copy_{B,C} for a plain 1 GiB device copy, whose
+    FETCH_SIZE / WRITE_SIZE give the byte-scaling factors.
     """
     cb, _ = _pmc_means(os.path.join(root, "copy_B", "run_counter_collection.csv"), "copyBuffer")
     cc, _ = _pmc_means(os.path.join(root, "copy_C", "run_counter_collection.csv"), "copyBuffer")
@@ -95,7 +101,7 @@ def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_
     bench_cmd = (f"python bench.py --config {workload} --steps 2 --warmup 1 --no-cpu-baseline "
                  "--variants {variant}")
     passes = [("A", PMC_PASSES["A"], "attn_fwd", bench_cmd), ("B", PMC_PASSES["B"], "attn_fwd", bench_cmd),
-              ("C", PMC_PASSES["C"], "attn_fwd", bench_cmd),
+              ("C", PMC_PASSES["C"], "attn_fwd", bench_cmd), ("D", PMC_PASSES["D"], "attn_fwd", bench_cmd),
               ("copy B", PMC_PASSES["B"], "'copyBuffer|elementwise|copy'", "python bench.py --copy-calibration 1024"),
               ("copy C", PMC_PASSES["C"].split()[0], "'copyBuffer|elementwise|copy'",
                "python bench.py --copy-calibration 1024")]
@@ -111,11 +117,14 @@ def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_
              "L2 hit % = TCC_HIT / (TCC_HIT + TCC_MISS). L2->fabric read bytes = FETCH_SIZE x the copy factor, "
              "write bytes = WRITE_SIZE x its factor (both per launch). MFMA FLOP = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512. "
              "MFMA busy % = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs), i.e. against the clock "
-             "the chip actually ran at.", "",
+             "the chip actually ran at; that clock = GRBM_GUI_ACTIVE / 8 XCDs / the dispatch's duration. "
+             "L2 latency = TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ (cycles per request from a CU); fabric "
+             "latency = TCC_EA0_RDREQ_LEVEL / TCC_EA0_RDREQ (cycles a read to the fabric is outstanding).", "",
              f"Copy calibration (1 GiB device copy): FETCH_SIZE x {f_fetch:.3f}, WRITE_SIZE x {f_write:.3f}", "",
-             "| variant | dispatches | L2 hit % | L2->fabric read GB/launch (scaled) | write GB/launch (scaled) | "
-             "DRAM read req | MFMA FLOP (MOPS x 512) | MFMA busy % |",
-             "|---|---|---|---|---|---|---|---|"]
+             "| variant | dispatches | kernel ms | clock GHz | L2 hit % | L2->fabric read GB/launch (scaled) | "
+             "write GB/launch (scaled) | DRAM read req | MFMA FLOP (MOPS x 512) | MFMA busy % | L2 latency | "
+             "fabric latency |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     entry = data.setdefault(workload, {})
     variants = sorted({d.rsplit("_", 1)[0] for d in os.listdir(root) if d.endswith("_A")})
     for v in variants:
@@ -130,9 +139,16 @@ def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_
         entry[v] = {"kernel_sha": sha, "variant_spec": VARIANTS.get(v), "hbm_bytes_per_launch": fetch + write, "fetch_bytes": fetch,
                     "write_bytes": write, "l2_hit": hit, "dram_read_requests": c["TCC_EA0_RDREQ_DRAM_sum"],
                     "mfma_flop": a["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512, "mfma_busy": busy}
-        lines.append(f"| {v} | {na} | {100 * hit:.2f} | {fetch / 1e9:.1f} | {write / 1e9:.2f} | "
-                     f"{c['TCC_EA0_RDREQ_DRAM_sum']:.4g} | {a['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.4g} | "
-                     f"{100 * busy:.1f} |")
+        dpath = os.path.join(root, f"{v}_D", "run_counter_collection.csv")
+        dd = _pmc_means(dpath, "attn_fwd")[0] if os.path.exists(dpath) else {}
+        l2_lat = (f"{dd['TCP_TCC_READ_REQ_LATENCY_sum'] / dd['TCP_TCC_READ_REQ_sum']:.0f}"
+                  if dd.get("TCP_TCC_READ_REQ_sum") else "-")
+        fab_lat = f"{dd['TCC_EA0_RDREQ_LEVEL_sum'] / dd['TCC_EA0_RDREQ_sum']:.0f}" if dd.get("TCC_EA0_RDREQ_sum") else "-"
+        clock = cycles / a["duration_ns"] if a.get("duration_ns") else float("nan")
+        entry[v]["clock_ghz"] = clock
+        lines.append(f"| {v} | {na} | {a.get('duration_ns', float('nan')) / 1e6:.2f} | {clock:.3f} | {100 * hit:.2f} | "
+                     f"{fetch / 1e9:.1f} | {write / 1e9:.2f} | {c['TCC_EA0_RDREQ_DRAM_sum']:.4g} | "
+                     f"{a['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.4g} | {100 * busy:.1f} | {l2_lat} | {fab_lat} |")
     with open(out_json, "w") as f:
         json.dump(data, f, indent=1, sort_keys=True)
     with open(out_md, "w") as f:
