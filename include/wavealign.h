@@ -211,7 +211,10 @@ wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
  * accumulation, bf16 output. Query block i runs at the slot s with perm[s] = i
  * and is read and written at its original rows (the inverse permutation of
  * Sec. IV-A is fused into the store), so O is identical for every perm.
- * A query block with no kept KV block gets O = 0 and LSE = -inf.
+ * A query block with no kept KV block gets O = 0 and LSE = -inf. The softmax
+ * takes the scores of each row's first kept block as its reference maximum; a
+ * row whose later scores exceed it by 32 or more (log2 units) is recomputed
+ * against its exact maximum within the same call. Inputs must be finite.
  *   q, k, v      bf16 [B][H][N][d], 16-byte aligned
  *   perm         int32 [B][H][M_B], NULL = identity (not checked for bijectivity)
  *   seg_start    int32 [B][H][n_xcd+1] XCD segment table from wa_build_permutation,
