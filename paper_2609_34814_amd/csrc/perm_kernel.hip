@@ -68,18 +68,39 @@ __device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
 __device__ __forceinline__ int bitlen_u64(uint64_t v) { return v ? 64 - __clzll((long long)v) : 0; }
 __device__ __forceinline__ uint64_t uabs64(int64_t v) { return v < 0 ? (uint64_t)(-v) : (uint64_t)v; }
 
-__device__ __forceinline__ int64_t wave_sum(int64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+// Wavefront reductions with DPP lane moves (a few cycles each, where a lane shuffle goes through
+// LDS): xor 1 and xor 2 within quads, then the half-row and row mirrors, then the row broadcasts of
+// lane 15 and lane 31, which leave the total in lane 63; it is read back to every lane.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROW_MASK, 0xf, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROW_MASK, 0xf, false);
+  return ((uint64_t)hi << 32) | lo;
 }
+__device__ __forceinline__ uint64_t lane63(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ int64_t wave_sum(int64_t v) {
+  uint64_t u = (uint64_t)v;  // two's complement: the sum modulo 2^64 is the exact sum
+  u += dpp64<0xB1, 0xf>(u);   // quad_perm [1,0,3,2]
+  u += dpp64<0x4E, 0xf>(u);   // quad_perm [2,3,0,1]
+  u += dpp64<0x141, 0xf>(u);  // row_half_mirror
+  u += dpp64<0x140, 0xf>(u);  // row_mirror
+  u += dpp64<0x142, 0xa>(u);  // row_bcast15 into rows 1 and 3
+  u += dpp64<0x143, 0xc>(u);  // row_bcast31 into rows 2 and 3
+  return (int64_t)lane63(u);
+}
+__device__ __forceinline__ uint64_t max64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 __device__ __forceinline__ uint64_t wave_max(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    uint64_t u = __shfl_xor(v, o);
-    v = u > v ? u : v;
-  }
-  return v;
+  v = max64(v, dpp64<0xB1, 0xf>(v));
+  v = max64(v, dpp64<0x4E, 0xf>(v));
+  v = max64(v, dpp64<0x141, 0xf>(v));
+  v = max64(v, dpp64<0x140, 0xf>(v));
+  v = max64(v, dpp64<0x142, 0xa>(v));
+  v = max64(v, dpp64<0x143, 0xc>(v));
+  return lane63(v);
 }
 
 // Sum of up to 4 int64 values over the workgroup; the result is returned to every thread.
@@ -440,12 +461,18 @@ __device__ void write_identity(const WaPermLaunch& a, Shared& sh, int h, int fla
   if (a.flags && tid == 0) a.flags[h] = (uint8_t)(flags | FLAG_IDENTITY);
 }
 
-// Statistics, skip cases 1-3, and the first QR of the seeded start block.
-__global__ __launch_bounds__(NT) void perm_init_kernel(WaPermLaunch a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+// What the set-up of a head leaves for the subspace iteration (uniform over the workgroup).
+struct HeadInit {
+  int status;  // 0: iterate; 1: done (statistics only, or a skipped head with its identity order written);
+               // 2: the start block is degenerate
+  int flags;   // skip-rule flags of cases 1-3
+  int64_t nnz, sum_c2;
+};
+constexpr int HEAD_ITERATE = 0, HEAD_DONE = 1, HEAD_DEGENERATE = 2;
+
+// Statistics, skip cases 1-3, and the first QR of the seeded start block (into sh.xs and a.xg).
+__device__ HeadInit init_head(const WaPermLaunch& a, Shared& sh, int h) {
   const int tid = threadIdx.x;
-  const int h = blockIdx.x;
   const int m = a.m, n = a.n;
   const Head H = head_of(a, h);
 
@@ -479,7 +506,7 @@ __global__ __launch_bounds__(NT) void perm_init_kernel(WaPermLaunch a) {
     hs[4] = sum_c2;
     hs[5] = 0;
   }
-  if (a.stats_only) return;
+  if (a.stats_only) return {HEAD_DONE, 0, nnz, sum_c2};
 
   // ---- phase 1: skip cases 1-3 ----
   if (tid == 0) {
@@ -504,7 +531,7 @@ __global__ __launch_bounds__(NT) void perm_init_kernel(WaPermLaunch a) {
       S->done = 1;
       S->flags = flags;
     }
-    return;
+    return {HEAD_DONE, flags, nnz, sum_c2};
   }
 
   // ---- phase 2 starts: seeded start block and its QR ----
@@ -527,6 +554,13 @@ __global__ __launch_bounds__(NT) void perm_init_kernel(WaPermLaunch a) {
     S->nnz = nnz;
     S->sum_c2 = sum_c2;
   }
+  return {degen ? HEAD_DEGENERATE : HEAD_ITERATE, flags, nnz, sum_c2};
+}
+
+__global__ __launch_bounds__(NT) void perm_init_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+  init_head(a, sh, blockIdx.x);
 }
 
 // One QR of the subspace iteration: Z from the partial sums, Cholesky-QR into the next X.
@@ -550,34 +584,20 @@ __global__ __launch_bounds__(NT) void orth_step_kernel(WaPermLaunch a) {
   }
 }
 
-// Rayleigh-Ritz on the last product, canonical sign, skip case 4, Stage 1 and Stage 2.
-__global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+// Rayleigh-Ritz on the last product Z (thread-owned rows, zr) of X (in sh.xs), canonical sign, skip
+// case 4, Stage 1 and Stage 2. maxy is the max |Ym| of that product's first half (it fixes sy).
+__device__ void finish_head(const WaPermLaunch& a, Shared& sh, int h, bool degen, int64_t nnz, int64_t sum_c2,
+                            int flags, uint64_t maxy, const int64_t (&zr)[PER][2]) {
   const int tid = threadIdx.x;
-  const int h = blockIdx.x;
   const int m = a.m;
-  const PermState* S = a.state + h;
-  if (S->done) return;
   const Head H = head_of(a, h);
-  const bool degen = S->degen != 0;
-  const int64_t nnz = S->nnz, sum_c2 = S->sum_c2;
-  int flags = S->flags;
   int32_t* perm = a.perm + (int64_t)h * m;
   int32_t* seg_out = a.seg_start ? a.seg_start + (int64_t)h * (a.n_xcd + 1) : nullptr;
   int64_t trace = 0;
   int scale_exp = 0;
   if (!degen) {
-    const int2* xg = reinterpret_cast<const int2*>(a.xg) + (int64_t)h * m;
-    for (int i = tid; i < m; i += NT) {
-      const int2 x = xg[i];
-      sh.xs[2 * i] = x.x;
-      sh.xs[2 * i + 1] = x.y;
-    }
-    const int bly = bitlen_u64(S->maxy);
+    const int bly = bitlen_u64(maxy);
     const int sy = bly > 30 ? bly - 30 : 0;
-    int64_t zr[PER][2];
-    gather_partials(a, h, zr);
     uint64_t mx = 0;
 #pragma unroll
     for (int k = 0; k < PER; ++k)
@@ -736,6 +756,125 @@ __global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
   if (a.flags && tid == 0) a.flags[h] = (uint8_t)flags;
 }
 
+__global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+  const int h = blockIdx.x;
+  const PermState* S = a.state + h;
+  if (S->done) return;
+  const bool degen = S->degen != 0;
+  int64_t zr[PER][2] = {};
+  if (!degen) {
+    const int2* xg = reinterpret_cast<const int2*>(a.xg) + (int64_t)h * a.m;
+    for (int i = threadIdx.x; i < a.m; i += NT) {
+      const int2 x = xg[i];
+      sh.xs[2 * i] = x.x;
+      sh.xs[2 * i + 1] = x.y;
+    }
+    gather_partials(a, h, zr);
+  }
+  finish_head(a, sh, h, degen, S->nnz, S->sum_c2, S->flags, S->maxy, zr);
+}
+
+// The whole permutation of a head in one workgroup, for heads too small to fill the chip with column
+// slices: the same exact integer products as the slice kernels (so the same result), with Ym kept
+// in registers and M Ys scattered into LDS, and X kept in LDS between the steps.
+//   apply: Z = m * M~ Ys, Ys = (m * M~^T X) >> sy, for X in sh.xs; maxy = max |m * M~^T X|.
+//   colbits: the head's column bitmask (held in LDS by the caller); cc: its column counts.
+__device__ void apply_head(const WaPermLaunch& a, Shared& sh, unsigned long long* za, const uint64_t* colbits,
+                           const int32_t (&cc)[PER], int64_t (&zr)[PER][2], uint64_t& maxy) {
+  const int tid = threadIdx.x;
+  const int m = a.m, n = a.n, mw = (m + 63) / 64;
+  int64_t sx[2] = {0, 0};
+  for (int i = tid; i < m; i += NT) {
+    sx[0] += sh.xs[2 * i];
+    sx[1] += sh.xs[2 * i + 1];
+  }
+  block_sum<2>(sh, sx);
+  int64_t ym[PER][2];
+  uint64_t mx = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int j = tid + k * NT;
+    ym[k][0] = 0;
+    ym[k][1] = 0;
+    if (j < n) {
+      int64_t y0 = 0, y1 = 0;
+      for_bits(colbits, mw, n, j, [&](int i) {
+        y0 += sh.xs[2 * i];
+        y1 += sh.xs[2 * i + 1];
+      });
+      const int64_t c = cc[k];
+      ym[k][0] = (int64_t)m * y0 - c * sx[0];
+      ym[k][1] = (int64_t)m * y1 - c * sx[1];
+      const uint64_t p = uabs64(ym[k][0]), q = uabs64(ym[k][1]);
+      mx = p > mx ? p : mx;
+      mx = q > mx ? q : mx;
+    }
+  }
+  maxy = block_max(sh, mx);
+  const int bl = bitlen_u64(maxy);
+  const int sy = bl > 30 ? bl - 30 : 0;
+  for (int i = tid; i < 2 * m; i += NT) za[i] = 0ull;
+  __syncthreads();
+  int64_t py[2] = {0, 0};
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int j = tid + k * NT;
+    if (j < n) {
+      const int32_t y0 = (int32_t)(ym[k][0] >> sy), y1 = (int32_t)(ym[k][1] >> sy);
+      const int64_t c = cc[k];
+      py[0] += c * y0;
+      py[1] += c * y1;
+      const unsigned long long u0 = (unsigned long long)(int64_t)y0, u1 = (unsigned long long)(int64_t)y1;
+      for_bits(colbits, mw, n, j, [&](int i) {
+        atomicAdd(&za[2 * i], u0);
+        atomicAdd(&za[2 * i + 1], u1);
+      });
+    }
+  }
+  block_sum<2>(sh, py);  // its barriers also complete the scatter
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = tid + k * NT;
+    zr[k][0] = i < m ? (int64_t)m * (int64_t)za[2 * i] - py[0] : 0;
+    zr[k][1] = i < m ? (int64_t)m * (int64_t)za[2 * i + 1] - py[1] : 0;
+  }
+  __syncthreads();  // every thread has read za before the next step clears it
+}
+
+__global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+  unsigned long long* za = reinterpret_cast<unsigned long long*>(smem_raw + sizeof(Shared));  // [2 m]
+  uint64_t* cb = reinterpret_cast<uint64_t*>(za + 2 * a.m);  // the head's column bitmask [mw][n]
+  const int h = blockIdx.x;
+  const HeadInit hi = init_head(a, sh, h);
+  if (hi.status == HEAD_DONE) return;
+  bool degen = hi.status == HEAD_DEGENERATE;
+  int64_t zr[PER][2] = {};
+  uint64_t maxy = 0;
+  if (!degen) {
+    const Head H = head_of(a, h);
+    for (int t = threadIdx.x; t < H.mw * a.n; t += NT) cb[t] = H.colbits[t];
+    int32_t cc[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int j = threadIdx.x + k * NT;
+      cc[k] = j < a.n ? a.cc[(int64_t)h * a.n + j] : 0;
+    }
+    __syncthreads();
+    for (int it = 0; it <= a.iters; ++it) {
+      apply_head(a, sh, za, cb, cc, zr, maxy);
+      if (it < a.iters && orth(sh, H, zr)) {
+        degen = true;
+        break;
+      }
+    }
+  }
+  finish_head(a, sh, h, degen, hi.nnz, hi.sum_c2, hi.flags, maxy, zr);
+}
+
 // Arithmetic self-check: the fp64 operations the permutation relies on, evaluated on the GPU.
 __global__ void fp64_probe_kernel(const double* a, const double* b, const int64_t* c, double* out, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -755,8 +894,17 @@ size_t wa_perm_shared_bytes() { return sizeof(Shared); }
 
 int wa_perm_slices(int n) { return (n + GT - 1) / GT; }
 
-// Launch sequence on one stream: init; iters x (gather, scatter, orth); gather, scatter, finish.
-// The statistics-only form runs init alone.
+// Heads of at most this many 256-column slices run as one workgroup each (perm_fused_kernel), which
+// replaces the 3 + 3 T launches of the slice kernels (0.21 -> 0.18 ms for 2 heads of 64 blocks,
+// 0.34 -> 0.28 ms for 12 heads of 256); from three slices on, the slices' parallelism wins.
+#ifndef WA_PERM_FUSED_MAX_SLICES
+#define WA_PERM_FUSED_MAX_SLICES 2
+#endif
+constexpr int kFusedMaxSlices = WA_PERM_FUSED_MAX_SLICES;
+constexpr size_t kLdsBytes = 160 * 1024;  // LDS of one gfx950 workgroup
+
+// Launch sequence on one stream: init; iters x (gather, scatter, orth); gather, scatter, finish; or
+// the fused kernel alone. The statistics-only form runs init alone.
 hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   if (a.bh <= 0) return hipSuccess;
   if (a.slices != wa_perm_slices(a.n) || a.m > MAXB || a.n > MAXB) return hipErrorInvalidValue;
@@ -770,6 +918,14 @@ hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   hipError_t e = hipFuncSetAttribute((const void*)apply_scatter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)zsmem);
   if (e != hipSuccess) return e;
+  const size_t fsmem = smem + (size_t)2 * a.m * sizeof(unsigned long long) +
+                       (size_t)((a.m + 63) / 64) * a.n * sizeof(uint64_t);
+  if (!a.stats_only && a.slices <= kFusedMaxSlices && fsmem <= kLdsBytes) {
+    e = hipFuncSetAttribute((const void*)perm_fused_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fsmem);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(perm_fused_kernel, dim3(a.bh), dim3(NT), fsmem, stream, a);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(perm_init_kernel, dim3(a.bh), dim3(NT), smem, stream, a);
   if ((e = hipGetLastError()) != hipSuccess || a.stats_only) return e;
   const dim3 slices((unsigned)(a.bh * a.slices));
