@@ -24,7 +24,10 @@ very sparse masks. The paper gives no formula, so the reading here is:
 The default constants are offline profiles of the target, taken by timing each
 step with and without reordering over sequence length and density (the sweep of
 Sec. VI-F): the overhead terms are a least-squares fit of the permutation's time
-per head, the gain the attention time saved per kept block at the densest points.
+per head; the gain is the attention time saved per kept block where reordering
+paid; cache_bytes is the K/V per head below which it did not pay (the shared
+last-level cache holds that much next to the streamed Q, O and V^T); j_max lies
+below the adjacent-row overlap of heads whose raster order is already local.
 
 Each floating-point expression below is evaluated in fp64 with one IEEE
 rounding per operation in the order written, so that an independent
@@ -49,12 +52,12 @@ SKIP_AUTO, SKIP_NEVER, SKIP_ALWAYS = 0, 1, 2
 
 @dataclass(frozen=True)
 class SkipProfile:
-    cache_bytes: float = 256.0 * 1024 * 1024
-    gain_ns_per_block: float = 0.1
-    ovh_ns_fixed: float = 5270.0
-    ovh_ns_per_row: float = 7.6
-    ovh_ns_per_nnz: float = 0.056
-    j_max: float = 0.75
+    cache_bytes: float = 96.0 * 1024 * 1024
+    gain_ns_per_block: float = 0.5
+    ovh_ns_fixed: float = 6122.0
+    ovh_ns_per_row: float = 4.55
+    ovh_ns_per_nnz: float = 0.0567
+    j_max: float = 0.2
     eta_min: float = 0.05
 
 

@@ -141,14 +141,16 @@ wa_status check_ws(void* ws, size_t have, size_t need) {
   return WA_OK;
 }
 
+// MI355X offline profiles from the sequence-length and density sweep of the attention step.
 const wa_skip_profile kDefaultProfile = {
-    256.0 * 1024.0 * 1024.0,  // cache_bytes: MI355X shared last-level cache (behind the per-XCD L2s)
-    0.1,                      // gain_ns_per_block: attention time saved per kept block, densest sweep points
-    5270.0,                   // ovh_ns_fixed    } permutation time per head, amortised over concurrent
-    7.6,                      // ovh_ns_per_row  } heads, least-squares fit over the sequence-length and
-    0.056,                    // ovh_ns_per_nnz  } density sweep
-    0.75,                     // j_max
-    0.05,                     // eta_min
+    96.0 * 1024.0 * 1024.0,  // cache_bytes: K/V per head below which reordering did not pay (the shared
+                             // 256 MiB last-level cache holds it next to the streamed Q, O and V^T)
+    0.5,                     // gain_ns_per_block: attention time saved per kept block where it paid
+    6122.0,                  // ovh_ns_fixed    } permutation time per head, amortised over concurrent
+    4.55,                    // ovh_ns_per_row  } heads, least-squares fit over the sweep
+    0.0567,                  // ovh_ns_per_nnz  }
+    0.2,                     // j_max: adjacent rows of raster-local heads share 23-40% of their blocks
+    0.05,                    // eta_min
 };
 
 wa_status check_attn_common(const void* q, const void* k, const void* v, void* o, int32_t n_xcd) {

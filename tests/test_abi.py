@@ -42,7 +42,7 @@ def test_version_and_strings():
         assert lib.wa_status_string(code)
     p = L.WaSkipProfile()
     assert lib.wa_default_skip_profile(ctypes.byref(p)) == 0
-    assert p.cache_bytes == 256 * 1024 * 1024 and p.eta_min == 0.05
+    assert p.cache_bytes == 96 * 1024 * 1024 and p.j_max == 0.2 and p.eta_min == 0.05
     assert lib.wa_default_skip_profile(None) == L.WA_ERR_INVALID_ARG
 
 

@@ -151,7 +151,7 @@ def _perm_case(wl, mask, *, wave, n_xcd, mode, iters=10, seed=0, profile=None):
 # A 4 MiB cache and a cheap, profitable reordering keep skip cases 1 and 2 quiet on these
 # workloads, so the later cases decide.
 _SMALL_CACHE = S.SkipProfile(cache_bytes=4 * 1024 * 1024, gain_ns_per_block=1.0, ovh_ns_fixed=2000.0,
-                             ovh_ns_per_row=2.0, ovh_ns_per_nnz=0.05)
+                             ovh_ns_per_row=2.0, ovh_ns_per_nnz=0.05, j_max=0.75)
 
 
 @pytest.mark.parametrize("name", ["tiny", "wan1.3b-480p-81f", "skip-d64", "ragged", "dense", "single", "diag"])

@@ -49,18 +49,19 @@ def test_eta_separates_random_from_structured():
 # A profile under which only the designed case fires on the inputs below: a 4 MiB cache and
 # a cheap reordering that saves 1 ns per kept block.
 PERMISSIVE = S.SkipProfile(cache_bytes=4 * 1024 * 1024, gain_ns_per_block=1.0, ovh_ns_fixed=2000.0,
-                           ovh_ns_per_row=2.0, ovh_ns_per_nnz=0.05)
+                           ovh_ns_per_row=2.0, ovh_ns_per_nnz=0.05, j_max=0.75)
 
 
 def test_tier1_cases():
     prof = S.SkipProfile()
     tiny = make_mask_head(CONFIGS["tiny"], 0, 0)
     f = S.tier1_flags(S.head_stats(tiny), prof, 64, 64)
-    assert f & S.FLAG_FITS_CACHE          # 64 KV blocks of 16 KiB = 1 MiB < 256 MiB
+    assert f & S.FLAG_FITS_CACHE          # 64 KV blocks of 16 KiB = 1 MiB < 96 MiB
     big = S.head_stats(make_mask_head(CONFIGS["wan14b-720p-81f"], 0, 0))
-    # 591 KV blocks of 64 KiB = 37 MiB: inside the shared last-level cache, not inside one 4 MiB L2;
-    # 52K kept blocks save 5 us at 0.1 ns each, less than the 13 us the permutation costs
-    assert S.tier1_flags(big, prof, 128, 128) == S.FLAG_FITS_CACHE | S.FLAG_LITTLE_WORK
+    # 591 KV blocks of 64 KiB = 37 MiB: below the 96 MiB break-even, not inside one 4 MiB L2;
+    # 84K kept blocks save 42 us at 0.5 ns each, more than the 14 us the permutation costs;
+    # adjacent rows share 36% of their blocks (raster order is already local)
+    assert S.tier1_flags(big, prof, 128, 128) == S.FLAG_FITS_CACHE | S.FLAG_LOCAL
     assert S.tier1_flags(big, PERMISSIVE, 128, 128) == 0
     prof = PERMISSIVE
     # already local: every row equal to its neighbour except one column
@@ -77,6 +78,19 @@ def test_tier1_cases():
     assert S.tier1_flags(st, exact, 128, 128) & S.FLAG_FITS_CACHE
     below = S.SkipProfile(cache_bytes=128 * S.kv_block_bytes(128, 128) - 1)
     assert not (S.tier1_flags(st, below, 128, 128) & S.FLAG_FITS_CACHE)
+
+
+def test_default_rule_decides_per_head_on_mixed_heads():
+    """Default profile on the 401-frame workload with spatial and temporal heads: the spatial heads are
+    already local in raster order (adjacent rows share ~33% of their blocks) and keep it; the temporal
+    heads (~6%) are reordered; 178 MiB of K/V per head is above the cache break-even."""
+    from workloads.gen import ALL_CONFIGS
+    wl = ALL_CONFIGS["long-720p-401f-mixed"]
+    prof = S.SkipProfile()
+    spatial = S.head_stats(make_mask_head(wl, 0, 0))
+    temporal = S.head_stats(make_mask_head(wl, 0, 20))
+    assert S.tier1_flags(spatial, prof, wl.block, wl.head_dim) == S.FLAG_LOCAL
+    assert S.tier1_flags(temporal, prof, wl.block, wl.head_dim) == 0
 
 
 def test_driver_modes():
