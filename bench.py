@@ -4,7 +4,12 @@ A step is one pass of the whole path over the workload, inputs resident in HBM:
   build_permutation (mask scans, subspace iteration, polar sort, wave buckets, Stage 2)
   -> compact_mask (per-row KV-block lists) -> sparse attention (bf16 MFMA).
 The headline value is effective TFLOP/s = 4 * block^2 * d * sum(nnz) / step time,
-i.e. the FLOPs of the kept blocks over the whole step (reordering overhead included).
+i.e. the FLOPs of the kept blocks over the whole step (reordering overhead included), of the
+method as the paper defines it: the adaptive skip rule decides per head whether the two-stage
+order is built or the identity order kept (variant `auto`). The same line reports every timed
+variant (by default also `reordered`, the two-stage order on every head, and `natural`), their
+speedups over natural order, and the L2 hit ratio and L2-to-fabric read bytes of each from the
+committed counter summary while it matches the kernel source.
 
 Prints one JSON line. Default workload: the 720p / 401-frame long-video shape
 (40 heads, d = 128, 363,600 tokens, 128-token blocks, ~5% mean density).
@@ -52,6 +57,21 @@ def load_traffic(workload: str, variant: str):
     if not entry or entry.get("kernel_sha") != kernel_source_hash() or entry.get("variant_spec") != VARIANTS[variant]:
         return None
     return entry.get("hbm_bytes_per_launch")
+
+
+def load_counters(workload: str, variant: str):
+    """L2 hit ratio, L2-to-fabric read bytes, MFMA busy and clock of one variant's attention launch, from
+    the committed rocprofv3 counter summary while it matches the kernel source (else None)."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            entry = json.load(f).get(workload, {}).get(variant)
+    except (OSError, ValueError):
+        return None
+    if not entry or entry.get("kernel_sha") != kernel_source_hash() or entry.get("variant_spec") != VARIANTS[variant]:
+        return None
+    return {"l2_hit": entry.get("l2_hit"), "l2_fabric_read_bytes": entry.get("fetch_bytes"),
+            "mfma_busy": entry.get("mfma_busy"), "clock_ghz": entry.get("clock_ghz"),
+            "source": "profiles/attn_traffic.json"}
 
 
 def _pmc_means(csv_path: str, kernel_substr: str):
@@ -517,7 +537,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="long-720p-401f", choices=sorted(ALL_CONFIGS))
-    ap.add_argument("--variants", default="reordered,natural",
+    ap.add_argument("--variants", default="auto,reordered,natural",
                     help="comma list of: " + "; ".join(f"{k}: {v}" for k, v in VARIANT_HELP.items()))
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -694,7 +714,7 @@ def main() -> int:
         log(f"{variant}: step {ms_step:.2f} ms, attention kernel {attn_ms:.2f} ms "
             f"({results[variant]['tflops_attn']:.1f} TFLOP/s)")
 
-    head = "reordered" if "reordered" in results else next(iter(results))
+    head = next((v for v in ("auto", "reordered") if v in results), next(iter(results)))
     r = results[head]
     traffic = load_traffic(wl.name, head)
     roof = {
@@ -706,7 +726,7 @@ def main() -> int:
         "traffic": traffic,
     }
     out = {
-        "metric": "sparse-attn effective TFLOP/s (reordered path incl. reordering overhead)",
+        "metric": "sparse-attn effective TFLOP/s (skip rule + reordering + attention, overhead included)",
         "value": r["tflops_step"],
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -726,11 +746,14 @@ def main() -> int:
                               "total": algo_bytes, "flop_per_byte": flop / algo_bytes},
         "variants": results,
     }
-    if "natural" in results and "reordered" in results:
-        out["speedup_reordered_vs_natural"] = {
-            "step": results["natural"]["ms_per_step"] / results["reordered"]["ms_per_step"],
-            "attention_kernel": results["natural"]["attn_ms"] / results["reordered"]["attn_ms"],
-        }
+    if "natural" in results:
+        out["speedup_vs_natural"] = {
+            v: {"step": results["natural"]["ms_per_step"] / rv["ms_per_step"],
+                "attention_kernel": results["natural"]["attn_ms"] / rv["attn_ms"]}
+            for v, rv in results.items() if v != "natural"}
+    counters = {v: c for v in results if (c := load_counters(wl.name, v)) is not None}
+    if counters:
+        out["counters"] = counters
     if not args.no_cpu_baseline:
         log("timing the oracle on the host")
         out["cpu_baseline"] = cpu_baseline(wl, q, k, v, mask, flop, args.cpu_budget)

@@ -339,18 +339,22 @@ class _DeviceRows:
         return self.o[b, h, rows].float().cpu().numpy().astype(np.float64)
 
 
-def _bench_launch(wl, md, qd, kd, vd, perm_kind):
+def _bench_launch(wl, md, qd, kd, vd, perm_kind, with_perm=False):
     """The path as the benchmark times it: CSR lists from compact_mask and one queue (n_xcd = 1);
-    perm_kind "reordered" uses the two-stage order over chip-wide waves, "natural" none."""
+    perm_kind "reordered" uses the two-stage order over chip-wide waves on every head, "auto" the
+    same with the skip rule deciding per head, "natural" none. With with_perm, the permutation and
+    the head flags are returned too."""
     W_ = _w()
-    perm = seg = None
-    if perm_kind == "reordered":
+    perm = seg = flags = None
+    if perm_kind in ("reordered", "auto"):
         wave = W_.wave_size(wl.head_dim, wl.block) * 8
-        perm, seg, _ = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
-                                            wave=wave, n_xcd=1, skip="never")
+        perm, seg, flags = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
+                                                wave=wave, n_xcd=1, skip="never" if perm_kind == "reordered" else "auto")
     rp, ci = W_.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
     o, lse = W_.sparse_attn_csr(qd, kd, vd, rp, ci, perm, seg, block=wl.block, n_xcd=1, return_lse=True)
     torch.cuda.synchronize()
+    if with_perm:
+        return o, lse, perm, flags
     return o, lse
 
 
@@ -379,7 +383,19 @@ def test_attention_bench_launch_full_size():
     o_nat, lse_nat = _bench_launch(wl, md, qd, kd, vd, "natural")
     assert torch.equal(o.view(torch.int16), o_nat.view(torch.int16))
     assert torch.equal(lse.view(torch.int32), lse_nat.view(torch.int32))
-    del o_nat, lse_nat
+    # the skip rule's launch: its tier-1 decision per head equals the oracle's on the same statistics,
+    # a skipped head keeps the identity order, and O / LSE are again bit-identical
+    o_auto, lse_auto, perm_auto, flags_auto = _bench_launch(wl, md, qd, kd, vd, "auto", with_perm=True)
+    assert torch.equal(o_auto.view(torch.int16), o_nat.view(torch.int16))
+    assert torch.equal(lse_auto.view(torch.int32), lse_nat.view(torch.int32))
+    flags_auto, perm_auto = flags_auto.cpu().numpy(), perm_auto.cpu().numpy()
+    tier1 = S.FLAG_FITS_CACHE | S.FLAG_LITTLE_WORK | S.FLAG_LOCAL
+    for h in range(wl.heads):
+        want = S.tier1_flags(S.head_stats(mask[0, h]), S.SkipProfile(), wl.block, wl.head_dim)
+        assert int(flags_auto[0, h]) & tier1 == want, h
+        if want:
+            assert np.array_equal(perm_auto[0, h], np.arange(wl.mb)), h
+    del o_nat, lse_nat, o_auto, lse_auto
     picks = _few_blocks(mask, (0, 19, 39), 12, seed=4)
     ref = A.block_sparse_attention_rows(q, k, v, mask, wl.block, picks)
     st = compare_blocks(_DeviceRows(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
