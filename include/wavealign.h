@@ -198,8 +198,10 @@ wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* sh
  * maxima of Q and K, and their int8 codes. */
 wa_status wa_mask_producer_workspace_size(const wa_shape* shape, size_t* bytes);
 
-/* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters
- * and per-queue prefix tables, (64 + 64 * (B*H + 1)) int32 rounded up to 256 bytes),
+/* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters,
+ * per-queue prefix tables and the per-queue order of the last heads: 64 + 64 * (B*H + 1)
+ * int32 rounded up to 64 entries, plus 64 * T * M_B int32 with T = min(B*H, 16384 / M_B, 256),
+ * rounded up to 256 bytes),
  * a zero-padded transposed copy of V (bf16 [B][H][head_dim][M_B*block], rounded up
  * to 256 bytes), then the compacted lists. The first two parts (the leading part)
  * suffice for wa_sparse_attn_csr. Calls that share a workspace must not overlap. */
@@ -224,7 +226,12 @@ wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
  *                per resident slot); queue x holds segment x of every head, heads in order,
  *                and a workgroup takes the next slot of the queue of the XCD it runs on
  *                (hardware XCC id mod n_xcd), then of the other queues once that one is
- *                empty. 1: one queue, plain slot order on every XCD
+ *                empty. 1: one queue, plain slot order on every XCD. In the last
+ *                T = min(B*H, 16384 / M_B, 256) heads of each queue, a slot whose row
+ *                could still be running when the rest of the queue is done (twice its
+ *                block count times the queue's share of workgroups exceeds the blocks
+ *                queued after it) is taken first, longest first; the others keep their
+ *                order. The order changes when rows run, never what they compute.
  *   o            out bf16 [B][H][N][d]
  *   lse          out float [B][H][N] natural-log sum-exp of the scaled scores, nullable
  *   workspace    >= wa_attn_workspace_size(shape) */

@@ -125,7 +125,7 @@ void perm_ws_pointers(WaPermLaunch& a, const PermWs& L, char* base) {
 // Attention workspace: [scheduler state][V^T copy][row_ptr][col_idx]; the CSR entry point uses the
 // first two parts. The scheduler part is sized for the largest n_xcd.
 constexpr int kMaxXcd = 64;
-size_t attn_sched_bytes(const Dims& d) { return align_up(wa::sched_ints(d.bh, kMaxXcd) * 4); }
+size_t attn_sched_bytes(const Dims& d) { return align_up(wa::sched_state_ints(d.bh, d.mb, kMaxXcd) * 4); }
 size_t attn_csr_ws_bytes(const Dims& d) {
   return attn_sched_bytes(d) + align_up(wa_vt_bytes(d.bh, d.mb, d.d, d.blk));
 }

@@ -39,9 +39,15 @@
 // that the query blocks that run together on one XCD, and share its L2, are
 // consecutive slots of one segment (Sec. IV-D), and when that queue is empty
 // it takes slots from the other queues. Slot s of head bh computes original
-// query block perm[bh][s] (identity when perm is null).
+// query block perm[bh][s] (identity when perm is null). Row lengths are
+// heavy-tailed (a row can hold ten times the mean number of blocks), and a launch
+// whose last task is a long row ends with every other workgroup idle; so the last
+// heads of each queue run in an order built at each call: a row that could still
+// be running once the rest of the queue is done starts first, longest first, and
+// every other row keeps its place (tail_order_kernel).
 
 #include "common.h"
+#include "wavealign.h"
 
 #include <algorithm>
 #include <type_traits>
@@ -198,6 +204,7 @@ __device__ __forceinline__ void issue_vt(unsigned char* tile, const unsigned cha
 __device__ bool fetch_task(const WaAttnLaunch& a, int home, int* bh_out, int* slot_out) {
   int32_t* cnt = a.sched;
   const int32_t* pre = a.sched + 64;
+  const int th = wa::tail_heads(a.bh, a.mb);
   for (int k = 0; k < a.n_xcd; ++k) {
     const int x = (home + k) % a.n_xcd;
     const int32_t* px = pre + (int64_t)x * (a.bh + 1);
@@ -205,6 +212,13 @@ __device__ bool fetch_task(const WaAttnLaunch& a, int home, int* bh_out, int* sl
     if (__hip_atomic_load(cnt + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= total) continue;
     const int t = atomicAdd(cnt + x, 1);
     if (t >= total) continue;
+    const int tb = px[a.bh - th];
+    if (t >= tb) {  // the last heads: the call's tail order
+      const int e = a.sched[wa::tail_offset(a.bh, a.n_xcd) + (int64_t)x * th * a.mb + (t - tb)];
+      *bh_out = a.bh - th + (e >> 16);
+      *slot_out = e & 0xFFFF;
+      return true;
+    }
     // head h with px[h] <= t < px[h+1]
     int lo = 0, hi = a.bh - 1;
     while (lo < hi) {
@@ -526,6 +540,152 @@ __global__ __launch_bounds__(64) void sched_kernel(int32_t* sched, const int32_t
   }
 }
 
+// Tail order of queue x (one workgroup per queue): entries e = 0, 1, ... enumerate, in queue order,
+// the slots of segment x of the last th heads. A row of n blocks that starts with fewer than
+// 2 n (grid / n_xcd) blocks queued after it could outlast the rest of the queue; such rows go first,
+// by descending n (ties in queue order), and the others follow in queue order. Each entry is
+// (head offset << 16) | slot. The order is a permutation of the queue's slots, so every row still
+// runs exactly once.
+__global__ __launch_bounds__(1024) void tail_order_kernel(WaAttnLaunch a, int grid) {
+  constexpr int NT = 1024;
+  constexpr int PER = wa::kTailEntries / NT;
+  __shared__ int32_t hstart[wa::kTailMaxHeads + 1];  // first entry of each head's segment
+  __shared__ int32_t hslot0[wa::kTailMaxHeads];      // its first slot
+  __shared__ int32_t part[NT];
+  __shared__ uint32_t key[wa::kTailEntries];
+  const int x = blockIdx.x;
+  const int t = threadIdx.x;
+  const int th = wa::tail_heads(a.bh, a.mb);
+  const int hb = a.bh - th;
+  int32_t* tail = a.sched + wa::tail_offset(a.bh, a.n_xcd) + (int64_t)x * th * a.mb;
+  if (t < th) {
+    int s0, s1;
+    wa::xcd_segment(x, a.mb, a.n_xcd, a.seg ? a.seg + (int64_t)(hb + t) * (a.n_xcd + 1) : nullptr, &s0, &s1);
+    hslot0[t] = s0;
+    part[t] = s1 - s0;
+  }
+  __syncthreads();
+  if (t == 0) {
+    int acc = 0;
+    for (int k = 0; k < th; ++k) {
+      hstart[k] = acc;
+      acc += part[k];
+    }
+    hstart[th] = acc;
+  }
+  __syncthreads();
+  const int total = hstart[th];
+  // head offset of entry e: the last k with hstart[k] <= e
+  auto head_of = [&](int e) {
+    int lo = 0, hi = th - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (hstart[mid] <= e) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+  };
+  // block counts of this thread's entries PER t .. PER t + PER - 1 (independent loads first)
+  int row[PER], nb[PER];
+  const int e0 = t * PER;
+  int k = e0 < total ? head_of(e0) : 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = e0 + i;
+    row[i] = -1;
+    if (e < total) {
+      while (e >= hstart[k + 1]) ++k;
+      const int slot = hslot0[k] + (e - hstart[k]);
+      row[i] = a.perm ? a.perm[(int64_t)(hb + k) * a.mb + slot] : slot;
+    }
+  }
+  k = e0 < total ? head_of(e0) : 0;
+  int sum = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = e0 + i;
+    nb[i] = 0;
+    if (e < total) {
+      while (e >= hstart[k + 1]) ++k;
+      if ((unsigned)row[i] < (unsigned)a.mb) {
+        const int32_t* rp = a.row_ptr + (int64_t)(hb + k) * (a.mb + 1);
+        nb[i] = min(max(rp[row[i] + 1] - rp[row[i]], 0), WA_MAX_BLOCKS);
+      }
+    }
+    sum += nb[i];
+  }
+  // blocks queued after each entry, then the late entries and their ranks (block-wide scans)
+  auto block_scan = [&](int v, int* all) {  // inclusive prefix sum over the threads, and the total
+    part[t] = v;
+    __syncthreads();
+    for (int off = 1; off < NT; off <<= 1) {
+      const int u = t >= off ? part[t - off] : 0;
+      __syncthreads();
+      part[t] += u;
+      __syncthreads();
+    }
+    const int r = part[t];
+    *all = part[NT - 1];
+    __syncthreads();
+    return r;
+  };
+  const int64_t wgs = max(grid / a.n_xcd, 1);
+  int all = 0;
+  const int incl = block_scan(sum, &all);
+  int64_t after = (int64_t)all - incl;  // blocks of the entries after this thread's
+  uint32_t late_bits = 0;
+  int nlate_mine = 0;
+#pragma unroll
+  for (int i = PER - 1; i >= 0; --i) {
+    const int e = e0 + i;
+    if (e < total && 2 * (int64_t)nb[i] * wgs > after) {
+      late_bits |= 1u << i;
+      ++nlate_mine;
+    }
+    after += nb[i];
+  }
+  int nlate = 0;
+  const int late_incl = block_scan(nlate_mine, &nlate);
+  int late_before = late_incl - nlate_mine;
+  int P = 1;
+  while (P < nlate) P <<= 1;
+  for (int i = t; i < P; i += NT) key[i] = 0xFFFFFFFFu;
+  __syncthreads();
+  k = e0 < total ? head_of(e0) : 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = e0 + i;
+    if (e < total) {
+      while (e >= hstart[k + 1]) ++k;
+      if (late_bits >> i & 1u) {
+        key[late_before++] = ((uint32_t)(WA_MAX_BLOCKS - nb[i]) << 14) | (uint32_t)e;
+      } else {
+        tail[nlate + (e - late_before)] = (k << 16) | (hslot0[k] + (e - hstart[k]));
+      }
+    }
+  }
+  __syncthreads();
+  // late entries: bitonic sort ascending = descending block count, ties in queue order
+  for (int kk = 2; kk <= P; kk <<= 1)
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      for (int i = t; i < P; i += NT) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint32_t u = key[i], v = key[l];
+          if ((u > v) == ((i & kk) == 0)) {
+            key[i] = v;
+            key[l] = u;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  for (int i = t; i < nlate; i += NT) {
+    const int e = (int)(key[i] & 0x3FFFu);
+    const int kh = head_of(e);
+    tail[i] = (kh << 16) | (hslot0[kh] + (e - hstart[kh]));
+  }
+}
+
 // V [bh][n][D] -> V^T [bh][D][npad], zero for keys >= n. One 64-key x 64-column tile per workgroup,
 // 16-byte loads and stores, transposed through LDS.
 template <int D>
@@ -579,6 +739,15 @@ hipError_t launch_t(const WaAttnLaunch& a, hipStream_t stream) {
   hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(64), 0, stream, a.sched, a.seg, a.bh, a.mb, a.n_xcd);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int64_t tasks = (int64_t)a.bh * a.mb;
+  int occ = 0;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, attn_fwd_kernel<D, BLK>, BLK * 2, 0);
+  if (e != hipSuccess) return e;
+  const int64_t grid = std::min<int64_t>(tasks, (int64_t)resident_cus() * std::max(occ, 1));
+  if (tasks > 0) {
+    hipLaunchKernelGGL(tail_order_kernel, dim3(a.n_xcd), dim3(1024), 0, stream, a, (int)grid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   const int64_t npad = (int64_t)a.mb * BLK;
   const int tiles_n = (int)((npad + 63) / 64);
   const int64_t tgrid = (int64_t)a.bh * (D / 64) * tiles_n;
@@ -588,12 +757,7 @@ hipError_t launch_t(const WaAttnLaunch& a, hipStream_t stream) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const int64_t tasks = (int64_t)a.bh * a.mb;
   if (tasks <= 0) return hipSuccess;
-  int occ = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, attn_fwd_kernel<D, BLK>, BLK * 2, 0);
-  if (e != hipSuccess) return e;
-  const int64_t grid = std::min<int64_t>(tasks, (int64_t)resident_cus() * std::max(occ, 1));
   hipLaunchKernelGGL((attn_fwd_kernel<D, BLK>), dim3((unsigned)grid), dim3(BLK * 2), 0, stream, a);
   return hipGetLastError();
 }

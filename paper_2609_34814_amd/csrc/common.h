@@ -29,6 +29,22 @@ __host__ __device__ inline void xcd_segment(int x, int m, int n_xcd, const int32
 // segment lengths over the heads.
 __host__ __device__ inline size_t sched_ints(int64_t bh, int n_xcd) { return 64 + (size_t)n_xcd * (bh + 1); }
 
+// The last tail_heads(bh, m) heads of every queue run in an order built at each call (the tail
+// order table, n_xcd x tail_heads x m int32 after the prefix tables): at most kTailEntries entries
+// and kTailMaxHeads heads per queue.
+constexpr int kTailEntries = 16384;
+constexpr int kTailMaxHeads = 256;
+__host__ __device__ inline int tail_heads(int64_t bh, int m) {
+  if (bh <= 0 || m <= 0) return 0;
+  int64_t w = kTailEntries / m;
+  if (w > kTailMaxHeads) w = kTailMaxHeads;
+  return (int)(bh < w ? bh : w);
+}
+__host__ __device__ inline size_t tail_offset(int64_t bh, int n_xcd) { return (sched_ints(bh, n_xcd) + 63) / 64 * 64; }
+__host__ __device__ inline size_t sched_state_ints(int64_t bh, int m, int n_xcd) {
+  return tail_offset(bh, n_xcd) + (size_t)n_xcd * tail_heads(bh, m) * (m > 0 ? m : 0);
+}
+
 }  // namespace wa
 
 // Launch helpers (implemented in the .hip sources, called by the ABI layer).
@@ -37,7 +53,8 @@ struct WaAttnLaunch {
   const void* k;
   const void* v;
   void* vt;          // workspace: V transposed to [bh][head_dim][mb*block], zero-padded
-  int32_t* sched;    // workspace: sched_ints(bh, n_xcd) int32 (counters at [0, n_xcd), prefix table at 64)
+  int32_t* sched;    // workspace: sched_state_ints(bh, mb, n_xcd) int32 (counters at [0, n_xcd), prefix
+                     // tables at 64, the tail order table at tail_offset(bh, n_xcd))
   const int32_t* row_ptr;
   const int32_t* col_idx;
   const int32_t* perm;

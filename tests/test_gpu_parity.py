@@ -328,6 +328,75 @@ def test_repeated_runs_identical():
 # ------------------------------------------------------------------------------------------------
 # the benchmark's launch configuration at full size, and the largest supported head
 # ------------------------------------------------------------------------------------------------
+# the order of the last heads of each queue (load balance at the end of a launch)
+# ------------------------------------------------------------------------------------------------
+def _expected_tail_order(x, bh, mb, n_xcd, seg, perm, row_ptr, grid):
+    """The queue's last heads: slots whose rows could outlast the rest of the queue (twice their
+    block count times the queue's workgroups above the blocks queued after them) first, longest
+    first, ties in queue order; the other slots in queue order. Entries (head offset << 16) | slot."""
+    th = min(bh, 16384 // mb, 256)
+    hb = bh - th
+    ents = []
+    for kh in range(th):
+        if seg is None:
+            base, extra = divmod(mb, n_xcd)
+            s0 = x * base + min(x, extra)
+            s1 = s0 + base + (1 if x < extra else 0)
+        else:
+            s0 = min(max(int(seg[hb + kh][x]), 0), mb)
+            s1 = min(max(int(seg[hb + kh][x + 1]), s0), mb)
+        ents += [(kh, s) for s in range(s0, s1)]
+    nb = []
+    for kh, s in ents:
+        r = int(perm[hb + kh][s]) if perm is not None else s
+        nb.append(int(row_ptr[hb + kh][r + 1] - row_ptr[hb + kh][r]) if 0 <= r < mb else 0)
+    wgs = max(grid // n_xcd, 1)
+    after = np.concatenate([np.cumsum(nb[::-1])[::-1][1:], [0]])
+    late = sorted((e for e in range(len(ents)) if 2 * nb[e] * wgs > after[e]), key=lambda e: (-nb[e], e))
+    rest = [e for e in range(len(ents)) if not 2 * nb[e] * wgs > after[e]]
+    return th, [(ents[e][0] << 16) | ents[e][1] for e in late + rest]
+
+
+@pytest.mark.parametrize("name,n_xcd,reorder", [("tiny", 1, False), ("wan14b-720p-81f", 1, False),
+                                                 ("wan14b-720p-81f", 8, True), ("skip-d64", 8, False),
+                                                 ("long-720p-401f", 1, True)])
+def test_tail_order_table(name, n_xcd, reorder):
+    """The order the call builds for the last heads of every queue equals the rule computed here from
+    the lists and the permutation, and with O pre-filled with NaN every row is written."""
+    W_ = _w()
+    wl = CONFIGS[name]
+    mask = make_mask(wl, threads=16)
+    q, k, v = make_qkv(wl, threads=16)
+    md = u8_dev(mask)
+    b_, h_, mb = wl.batch, wl.heads, wl.mb
+    bh = b_ * h_
+    rp, ci = W_.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
+    perm = seg = None
+    wave = W_.wave_size(wl.head_dim, wl.block)
+    if reorder:
+        perm, seg, _ = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
+                                            wave=wave if n_xcd > 1 else wave * 8, n_xcd=n_xcd, skip="never")
+    ws = torch.empty(W_.attn_workspace_size(W_.shape_of(b_, h_, wl.seq_len, wl.head_dim, wl.block)),
+                     dtype=torch.uint8, device="cuda")
+    qd, kd, vd = bf16_dev(q), bf16_dev(k), bf16_dev(v)
+    o = torch.full_like(qd, float("nan"))
+    W_.sparse_attn_csr(qd, kd, vd, rp, ci, perm, seg, block=wl.block, n_xcd=n_xcd, out=o, workspace=ws)
+    torch.cuda.synchronize()
+    assert not bool(torch.isnan(o.float()).any().item())
+    del o, qd, kd, vd
+    grid = min(bh * mb, torch.cuda.get_device_properties(0).multi_processor_count * (wave // 32))
+    sched = ws[:4 * (64 + 64 * (bh + 1) + 64 * 16384)].view(torch.int32).cpu().numpy()
+    off = (64 + n_xcd * (bh + 1) + 63) // 64 * 64
+    rp_h = rp.cpu().numpy().reshape(bh, mb + 1)
+    perm_h = perm.cpu().numpy().reshape(bh, mb) if perm is not None else None
+    seg_h = seg.cpu().numpy().reshape(bh, n_xcd + 1) if seg is not None else None
+    for x in range(n_xcd):
+        th, want = _expected_tail_order(x, bh, mb, n_xcd, seg_h, perm_h, rp_h, grid)
+        got = sched[off + x * th * mb: off + x * th * mb + len(want)]
+        assert np.array_equal(got, np.asarray(want, dtype=np.int32)), (name, x)
+
+
+# ------------------------------------------------------------------------------------------------
 class _DeviceRows:
     """O[b, h, lo:hi] pulled from the device as fp64 on demand (the full tensor is too big to copy)."""
 
