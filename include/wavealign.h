@@ -72,6 +72,9 @@ typedef struct wa_shape {
  *   2  nnz * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row * M_B
  *                                 + ovh_ns_per_nnz * nnz                (too little work)
  *   3  sum_i |M_i & M_i+1| / sum_i |M_i | M_i+1| >= j_max              (already local)
+ *      or, once the order P is built, J(P) <= J(natural order), with J that
+ *      overlap over consecutive rows of an order, compared as exact integer
+ *      cross-products                                                    (no locality gained)
  *   4  (lambda_1 + lambda_2) / ||M~||_F^2 < eta_min                      (no rank-2 structure)
  * Each comparison is one fixed sequence of IEEE fp64 operations. */
 typedef struct wa_skip_profile {

@@ -2,7 +2,9 @@
 
 Mirrors the per-head flow of Sec. IV-A and Alg. 2: the adaptive guard first
 (cases 1-3 from mask statistics), then Stage 1 and Stage 2; case 4 uses the
-Rayleigh-Ritz trace of Stage 1. A skipped head keeps the identity order.
+Rayleigh-Ritz trace of Stage 1, and case 3 is checked once more against the
+built order (it must raise the adjacent-row overlap). A skipped head keeps the
+identity order.
 """
 from __future__ import annotations
 
@@ -48,7 +50,13 @@ def build_permutation(mask: np.ndarray, *, block: int, head_dim: int, wave: int,
                 info["seg"][(b, h)] = P.work_segments(perm[b, h], st.row_nnz, n_xcd)
                 continue
             seg = P.work_segments(s1.order, st.row_nnz, n_xcd)
-            perm[b, h] = P.stage2(s1.order, st.row_nnz, n_xcd, wave, seg)
+            built = P.stage2(s1.order, st.row_nnz, n_xcd, wave, seg)
+            if skip_mode == S.SKIP_AUTO and S.order_not_more_local(st, mask[b, h], built):
+                perm[b, h] = P.identity_permutation(m)
+                flags[b, h] = f | S.FLAG_LOCAL | S.FLAG_IDENTITY
+                info["seg"][(b, h)] = P.work_segments(perm[b, h], st.row_nnz, n_xcd)
+                continue
+            perm[b, h] = built
             info["seg"][(b, h)] = seg
             flags[b, h] = f
     return perm, flags, info

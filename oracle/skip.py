@@ -14,7 +14,11 @@ very sparse masks. The paper gives no formula, so the reading here is:
           the reordering overhead, both linear models from offline profiles:
           nnz_h * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row*m + ovh_ns_per_nnz*nnz_h
   case 3 "already local": adjacent rows already share most blocks:
-          J_h = sum_i |M_i & M_{i+1}| / sum_i |M_i | M_{i+1}| >= j_max
+          J_h = sum_i |M_i & M_{i+1}| / sum_i |M_i | M_{i+1}| >= j_max,
+          or, once the two-stage order P is built, it does not raise that overlap:
+          J_h(P) <= J_h, compared exactly as integer cross-products (the order
+          cannot make the rows that run together share more blocks than the
+          natural order already does)
   case 4 (our addition) "no low-rank structure": the rank-2 embedding keeps too
           little of the centred mask's energy for Stage 1 to group anything:
           eta_h = (lambda_1 + lambda_2) / ||M~||_F^2 < eta_min,
@@ -100,6 +104,20 @@ def tier1_flags(st: HeadStats, prof: SkipProfile, block: int, head_dim: int) -> 
     if st.adj_or > 0 and float(st.adj_and) / float(st.adj_or) >= prof.j_max:
         flags |= FLAG_LOCAL
     return flags
+
+
+def adjacent_overlap(mask_h: np.ndarray, order: np.ndarray) -> tuple[int, int]:
+    """(sum_s |M_order[s] & M_order[s+1]|, sum_s |M_order[s] | M_order[s+1]|) over consecutive rows of an order."""
+    mb = (np.asarray(mask_h) != 0)[np.asarray(order)]
+    if mb.shape[0] < 2:
+        return 0, 0
+    return int((mb[:-1] & mb[1:]).sum()), int((mb[:-1] | mb[1:]).sum())
+
+
+def order_not_more_local(st: HeadStats, mask_h: np.ndarray, order: np.ndarray) -> bool:
+    """Case 3 against a built order: J(order) <= J(natural order), by exact integer cross-products."""
+    a, o = adjacent_overlap(mask_h, order)
+    return a * st.adj_or <= st.adj_and * o
 
 
 def eta(st: HeadStats, trace: int, scale_exp: int) -> float:

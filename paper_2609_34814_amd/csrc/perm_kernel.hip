@@ -467,6 +467,7 @@ struct HeadInit {
                // 2: the start block is degenerate
   int flags;   // skip-rule flags of cases 1-3
   int64_t nnz, sum_c2;
+  int64_t adj_and, adj_or;  // adjacent-row overlap of the natural order
 };
 constexpr int HEAD_ITERATE = 0, HEAD_DONE = 1, HEAD_DEGENERATE = 2;
 
@@ -506,7 +507,7 @@ __device__ HeadInit init_head(const WaPermLaunch& a, Shared& sh, int h) {
     hs[4] = sum_c2;
     hs[5] = 0;
   }
-  if (a.stats_only) return {HEAD_DONE, 0, nnz, sum_c2};
+  if (a.stats_only) return {HEAD_DONE, 0, nnz, sum_c2, adj[0], adj[1]};
 
   // ---- phase 1: skip cases 1-3 ----
   if (tid == 0) {
@@ -531,7 +532,7 @@ __device__ HeadInit init_head(const WaPermLaunch& a, Shared& sh, int h) {
       S->done = 1;
       S->flags = flags;
     }
-    return {HEAD_DONE, flags, nnz, sum_c2};
+    return {HEAD_DONE, flags, nnz, sum_c2, adj[0], adj[1]};
   }
 
   // ---- phase 2 starts: seeded start block and its QR ----
@@ -553,8 +554,10 @@ __device__ HeadInit init_head(const WaPermLaunch& a, Shared& sh, int h) {
     S->flags = flags;
     S->nnz = nnz;
     S->sum_c2 = sum_c2;
+    S->adj_and = adj[0];
+    S->adj_or = adj[1];
   }
-  return {degen ? HEAD_DEGENERATE : HEAD_ITERATE, flags, nnz, sum_c2};
+  return {degen ? HEAD_DEGENERATE : HEAD_ITERATE, flags, nnz, sum_c2, adj[0], adj[1]};
 }
 
 __global__ __launch_bounds__(NT) void perm_init_kernel(WaPermLaunch a) {
@@ -585,9 +588,11 @@ __global__ __launch_bounds__(NT) void orth_step_kernel(WaPermLaunch a) {
 }
 
 // Rayleigh-Ritz on the last product Z (thread-owned rows, zr) of X (in sh.xs), canonical sign, skip
-// case 4, Stage 1 and Stage 2. maxy is the max |Ym| of that product's first half (it fixes sy).
+// case 4, Stage 1 and Stage 2, then case 3 against the built order. maxy is the max |Ym| of that
+// product's first half (it fixes sy); adj_and / adj_or: the natural order's adjacent-row overlap.
 __device__ void finish_head(const WaPermLaunch& a, Shared& sh, int h, bool degen, int64_t nnz, int64_t sum_c2,
-                            int flags, uint64_t maxy, const int64_t (&zr)[PER][2]) {
+                            int flags, uint64_t maxy, const int64_t (&zr)[PER][2], int64_t adj_and,
+                            int64_t adj_or) {
   const int tid = threadIdx.x;
   const int m = a.m;
   const Head H = head_of(a, h);
@@ -752,7 +757,26 @@ __device__ void finish_head(const WaPermLaunch& a, Shared& sh, int h, bool degen
       }
       __syncthreads();
     }
-  for (int s = tid; s < m; s += NT) perm[s] = sh.cc[(int)(keys[s] & 0xFFFFull)];
+  int32_t* fin = sh.xs;  // the built order (the segment map is no longer needed)
+  for (int s = tid; s < m; s += NT) fin[s] = sh.cc[(int)(keys[s] & 0xFFFFull)];
+  __syncthreads();
+  for (int s = tid; s < m; s += NT) perm[s] = fin[s];
+
+  // ---- case 3 against the built order: it must raise the adjacent-row overlap ----
+  if (a.skip_mode == SKIP_AUTO) {
+    int64_t ov[2] = {0, 0};
+    for (int t = tid; t < (m - 1) * H.nw; t += NT) {
+      const int w = t / (m - 1), s = t % (m - 1);
+      const uint64_t x = H.rowbits[(int64_t)w * m + fin[s]], y = H.rowbits[(int64_t)w * m + fin[s + 1]];
+      ov[0] += __popcll(x & y);
+      ov[1] += __popcll(x | y);
+    }
+    block_sum<2>(sh, ov);
+    if (ov[0] * adj_or <= adj_and * ov[1]) {  // J(built order) <= J(natural order), exactly
+      write_identity(a, sh, h, flags | FLAG_LOCAL, false);
+      return;
+    }
+  }
   if (a.flags && tid == 0) a.flags[h] = (uint8_t)flags;
 }
 
@@ -773,7 +797,7 @@ __global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
     }
     gather_partials(a, h, zr);
   }
-  finish_head(a, sh, h, degen, S->nnz, S->sum_c2, S->flags, S->maxy, zr);
+  finish_head(a, sh, h, degen, S->nnz, S->sum_c2, S->flags, S->maxy, zr, S->adj_and, S->adj_or);
 }
 
 // The whole permutation of a head in one workgroup, for heads too small to fill the chip with column
@@ -872,7 +896,7 @@ __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
       }
     }
   }
-  finish_head(a, sh, h, degen, hi.nnz, hi.sum_c2, hi.flags, maxy, zr);
+  finish_head(a, sh, h, degen, hi.nnz, hi.sum_c2, hi.flags, maxy, zr, hi.adj_and, hi.adj_or);
 }
 
 // Arithmetic self-check: the fp64 operations the permutation relies on, evaluated on the GPU.

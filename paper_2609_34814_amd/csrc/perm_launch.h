@@ -14,7 +14,8 @@ struct PermState {
   int32_t done;     // the init kernel already wrote this head's result (skipped head)
   int32_t flags;    // skip-rule flags of cases 1-3
   int64_t nnz, sum_c2;
-  int64_t pad[3];
+  int64_t adj_and, adj_or;  // adjacent-row overlap of the natural order: sum |M_i & M_i+1|, sum |M_i | M_i+1|
+  int64_t pad[1];
 };
 static_assert(sizeof(PermState) == 64, "PermState is 64 bytes");
 

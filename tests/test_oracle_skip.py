@@ -95,7 +95,9 @@ def test_default_rule_decides_per_head_on_mixed_heads():
 
 def test_driver_modes():
     wl = CONFIGS["skip-d64"]
-    mask = make_mask(wl)[:, [0, 1, 20, 21]]
+    mask = make_mask(wl)[:, [0, 1, 20, 21]].copy()
+    # head 3: a locality head with its rows shuffled, so that its natural order is not local
+    mask[0, 3] = mask[0, 3][np.random.default_rng(7).permutation(wl.mb)]
     kw = dict(block=wl.block, head_dim=wl.head_dim, wave=64, n_xcd=8, iters=10, seed=0)
     p_always, f_always, _ = R.build_permutation(mask, skip_mode=S.SKIP_ALWAYS, **kw)
     assert np.all(p_always == np.arange(wl.mb)) and np.all(f_always & S.FLAG_IDENTITY)
@@ -106,13 +108,42 @@ def test_driver_modes():
     assert not np.any(f_never & S.FLAG_IDENTITY)
     # a 4 MiB cache keeps case 1 quiet (11.6 MiB of K/V per head), so the later cases decide
     p_auto, f_auto, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, profile=PERMISSIVE, **kw)
-    # random heads: unstructured -> identity; locality heads: reordered
+    # random heads: unstructured -> identity; a locality head in raster order: the built order does
+    # not raise the adjacent-row overlap (case 3 after the fact) -> identity; the shuffled one: reordered
     assert f_auto[0, 0] & S.FLAG_UNSTRUCTURED and np.all(p_auto[0, 0] == np.arange(wl.mb))
-    assert f_auto[0, 2] == 0 and np.array_equal(p_auto[0, 2], p_never[0, 2])
+    st2 = S.head_stats(mask[0, 2])
+    assert S.order_not_more_local(st2, mask[0, 2], p_never[0, 2])
+    assert f_auto[0, 2] == S.FLAG_LOCAL | S.FLAG_IDENTITY and np.all(p_auto[0, 2] == np.arange(wl.mb))
+    st3 = S.head_stats(mask[0, 3])
+    a3, o3 = S.adjacent_overlap(mask[0, 3], p_never[0, 3])
+    assert a3 / o3 > 2 * st3.adj_and / st3.adj_or
+    assert f_auto[0, 3] == 0 and np.array_equal(p_auto[0, 3], p_never[0, 3])
     # default profile: every head's K/V fits the shared cache, so case 1 keeps the identity order
     p_def, f_def, _ = R.build_permutation(mask, skip_mode=S.SKIP_AUTO, **kw)
     assert np.all(f_def & S.FLAG_FITS_CACHE) and np.all(f_def & S.FLAG_IDENTITY)
     assert np.all(p_def == np.arange(wl.mb))
+
+
+def test_adjacent_overlap_brute_force():
+    """The overlap of consecutive rows of an order, by sets on a small mask, and case 3 against a built
+    order on a band (its natural order is the most local) and on the band with rows shuffled."""
+    rng = np.random.default_rng(3)
+    m = 40
+    band = np.zeros((m, m), np.uint8)
+    for i in range(m):
+        band[i, max(0, i - 3): i + 4] = 1
+    order = rng.permutation(m)
+    a, o = S.adjacent_overlap(band, order)
+    rows = [set(np.nonzero(band[r])[0]) for r in order]
+    assert a == sum(len(rows[s] & rows[s + 1]) for s in range(m - 1))
+    assert o == sum(len(rows[s] | rows[s + 1]) for s in range(m - 1))
+    st = S.head_stats(band)
+    assert (st.adj_and, st.adj_or) == S.adjacent_overlap(band, np.arange(m))
+    assert S.order_not_more_local(st, band, order)            # a shuffle only loses locality
+    assert S.order_not_more_local(st, band, np.arange(m))     # equal overlap counts as no gain
+    shuffled = band[order]
+    st_s = S.head_stats(shuffled)
+    assert not S.order_not_more_local(st_s, shuffled, np.argsort(order))  # un-shuffling gains
 
 
 def test_compaction_brute_force():
