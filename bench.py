@@ -310,6 +310,29 @@ VARIANT_HELP = {
 FLAG_NAMES = ((1, "fits_cache"), (2, "little_work"), (4, "local"), (8, "unstructured"), (16, "degenerate"))
 
 
+def gemm_reference(attn_tflops: float, n: int = 16384, reps: int = 5) -> dict:
+    """Context for the roofline fraction: the rate of a large dense bf16 GEMM from the vendor library
+    (torch.matmul -> hipBLASLt) on the same GPU and clock conditions. Not part of the path."""
+    import torch
+    a = torch.randn((n, n), device="cuda", dtype=torch.bfloat16)
+    b = torch.randn((n, n), device="cuda", dtype=torch.bfloat16)
+    for _ in range(2):
+        c = a @ b
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        c = a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    tflops = 2.0 * n ** 3 / (e0.elapsed_time(e1) / reps * 1e-3) / 1e12
+    del a, b, c
+    torch.cuda.empty_cache()
+    log(f"library bf16 GEMM {n}^3: {tflops:.1f} TFLOP/s")
+    return {"op": f"torch.matmul bf16 {n}x{n}x{n}", "tflops": tflops, "frac_of_peak": tflops / MFMA_BF16_PEAK_TFLOPS,
+            "attention_vs_gemm": attn_tflops / tflops}
+
+
 def _median(xs):
     return float(np.median(np.asarray(xs, dtype=np.float64)))
 
@@ -541,6 +564,8 @@ def main() -> int:
                     help="comma list of: " + "; ".join(f"{k}: {v}" for k, v in VARIANT_HELP.items()))
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm-reference", action="store_true",
+                    help="skip timing the vendor library's dense bf16 GEMM (context for the roofline fraction)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (3 times), to calibrate the HBM counters")
     ap.add_argument("--summarize-pmc", metavar="DIR", help="summarize rocprofv3 counter passes found in DIR "
@@ -754,6 +779,8 @@ def main() -> int:
     counters = {v: c for v in results if (c := load_counters(wl.name, v)) is not None}
     if counters:
         out["counters"] = counters
+    if not args.no_gemm_reference:
+        out["library_gemm_reference"] = gemm_reference(r["tflops_attn"])
     if not args.no_cpu_baseline:
         log("timing the oracle on the host")
         out["cpu_baseline"] = cpu_baseline(wl, q, k, v, mask, flop, args.cpu_budget)

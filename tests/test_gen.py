@@ -26,6 +26,17 @@ def test_tensor_determinism_and_head_independence():
     assert abs(x.mean()) < 0.02 and abs(x.std() - 1) < 0.02
 
 
+def test_positional_tensors_same_in_threads():
+    """Q with a positional component, generated one head at a time and by four threads at once, is the
+    same bit for bit. (The generator once took the phase from a BLAS product, which returned wrong
+    values now and then when several threads called it at once at the 363,600-token size.)"""
+    wl = G.Workload("pos", 1, 4, 128, 128, (12, 45, 80), 1103,
+                    qk_rules=G._rules((0, 2, G._SPATIAL_QK), (2, 4, G._TEMPORAL_QK)))
+    a = make_tensor(wl, G.STREAM_Q, threads=1)
+    b = make_tensor(wl, G.STREAM_Q, threads=4)
+    assert np.array_equal(a, b)
+
+
 def test_block_centres_ragged_last_block():
     wl = CONFIGS["wan1.3b-480p-81f"]
     t, p = block_centres(wl)

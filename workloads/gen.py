@@ -216,7 +216,10 @@ def positional_features(wl: Workload, flat_head: int, rule: dict) -> np.ndarray:
     phi = rng.uniform(0.0, 2.0 * math.pi, size=d)
     t = np.arange(n, dtype=np.int64)
     pos = np.stack([t // (hh * ww), (t // ww) % hh, t % ww], axis=1).astype(np.float64)
-    return math.sqrt(2.0 / d) * np.cos(pos @ w + phi)
+    # the phase written out element by element (a BLAS product here gave wrong values when the
+    # generator ran in several threads at once, so the inputs were not reproducible)
+    arg = pos[:, 0:1] * w[0] + pos[:, 1:2] * w[1] + pos[:, 2:3] * w[2] + phi
+    return math.sqrt(2.0 / d) * np.cos(arg)
 
 
 def make_tensor(wl: Workload, stream: int, heads: Optional[Sequence[int]] = None,
