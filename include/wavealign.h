@@ -197,8 +197,8 @@ wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* r
 wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* shape, int32_t keep, int32_t diagonal,
                                 uint8_t* mask, int8_t* codes, void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes needed by wa_produce_block_mask: float32 block means and per-head
- * maxima of Q and K, and their int8 codes. */
+/* Workspace bytes needed by wa_produce_block_mask: float32 block means, per-block and
+ * per-head maxima of Q and K, and their int8 codes. */
 wa_status wa_mask_producer_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters,

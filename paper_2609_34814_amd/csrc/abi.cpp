@@ -73,7 +73,7 @@ wa_status check_shape(const wa_shape* s, Dims* out) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 struct ProducerWs {
-  size_t means, amax, codes, total;
+  size_t means, amax, bmax, codes, total;
 };
 
 ProducerWs producer_ws_layout(const Dims& d) {
@@ -81,6 +81,7 @@ ProducerWs producer_ws_layout(const Dims& d) {
   size_t off = 0;
   w.means = off; off = align_up(off + (size_t)2 * d.bh * d.mb * d.d * 4);
   w.amax = off; off = align_up(off + (size_t)2 * d.bh * 4);
+  w.bmax = off; off = align_up(off + (size_t)2 * d.bh * d.mb * 4);
   w.codes = off; off = align_up(off + (size_t)2 * d.bh * d.mb * d.d);
   w.total = off;
   return w;
@@ -347,6 +348,7 @@ wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* sh
   a.q = q; a.k = k;
   a.means = (float*)(base + L.means);
   a.amax = (uint32_t*)(base + L.amax);
+  a.bmax = (uint32_t*)(base + L.bmax);
   a.codes = codes ? codes : (int8_t*)(base + L.codes);
   a.mask = mask;
   a.bh = (int32_t)d.bh; a.mb = d.mb; a.seq_len = d.n; a.block = d.blk; a.head_dim = d.d;

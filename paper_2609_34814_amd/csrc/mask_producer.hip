@@ -3,9 +3,12 @@
 //
 //   pool_kernel         block means of Q and K: each thread folds 8 channels of one block over
 //                       its tokens in ascending order (IEEE float32, one rounding per addition,
-//                       16-byte loads), then one correctly rounded division by the token count;
-//                       the per-head maximum |mean| by an atomic max on the float's bits
-//                       (non-negative floats order like their bit patterns);
+//                       16-byte loads), then one correctly rounded division by the token count,
+//                       and each block's maximum |mean| (as float bits: non-negative floats order
+//                       like their bit patterns);
+//   head_max_kernel     the per-head maximum over the block maxima (one workgroup per head and
+//                       tensor; a global atomic max per block instead serialised 2,841 updates on
+//                       each of 80 addresses and cost a quarter of the producer's time);
 //   quant_kernel        int8 codes rint(mean * fl32(127 / max)), clamped to [-127, 127];
 //   score_select_kernel one workgroup per ROWS query blocks of a head: exact int32 scores
 //                       s_ij = sum_c qcode_i[c] kcode_j[c] (v_dot4_i32_i8) for every KV block j
@@ -28,8 +31,24 @@ constexpr int kPoolThreads = 256;
 constexpr int kRows = 4;          // query blocks per score_select workgroup
 constexpr int kSelThreads = 256;  // 4 wavefronts, one row each
 
-__global__ __launch_bounds__(64) void zero_amax_kernel(uint32_t* amax, int n) {
-  for (int i = threadIdx.x; i < n; i += 64) amax[i] = 0u;
+// amax[which][bh] = max over the head's blocks of bmax[which][bh][j]; one workgroup per (which, bh)
+__global__ __launch_bounds__(256) void head_max_kernel(WaProducerLaunch a) {
+  __shared__ uint32_t part[4];
+  const int64_t wh = blockIdx.x;  // which * bh + bh
+  const uint32_t* b = a.bmax + wh * a.mb;
+  uint32_t mx = 0u;
+  for (int j = threadIdx.x; j < a.mb; j += 256) mx = b[j] > mx ? b[j] : mx;
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t u = __shfl_xor(mx, o);
+    mx = u > mx ? u : mx;
+  }
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t m = part[0];
+    for (int w = 1; w < 4; ++w) m = part[w] > m ? part[w] : m;
+    a.amax[wh] = m;
+  }
 }
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -93,13 +112,13 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(WaProducerLaunch a) 
       mx = b > mx ? b : mx;
     }
   }
-  // maximum over the G lanes of this block (every lane takes part), then one atomic per block
+  // maximum over the G lanes of this block (every lane takes part)
 #pragma unroll
   for (int o = G / 2; o > 0; o >>= 1) {
     const uint32_t u = __shfl_xor(mx, o);
     mx = u > mx ? u : mx;
   }
-  if (active && g == 0) atomicMax(a.amax + (int64_t)which * a.bh + bj / a.mb, mx);
+  if (active && g == 0) a.bmax[(int64_t)which * a.bh * a.mb + bj] = mx;
 }
 
 // codes[which][bh][mb][D] = rint(mean * fl32(127 / max)) clamped, 0 when max = 0
@@ -223,9 +242,7 @@ size_t wa_producer_select_smem(int mb) { return (size_t)kRows * mb * sizeof(int3
 
 hipError_t wa_launch_producer(const WaProducerLaunch& a, hipStream_t stream) {
   if (a.bh <= 0 || a.mb <= 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_amax_kernel, dim3(1), dim3(64), 0, stream, a.amax, 2 * a.bh);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
   const int64_t pool_threads = (int64_t)a.bh * a.mb * (a.head_dim / 8);
   const dim3 pgrid((unsigned)((pool_threads + kPoolThreads - 1) / kPoolThreads), 2);
   const int64_t qn = 2ll * a.bh * a.mb * a.head_dim;
@@ -235,6 +252,8 @@ hipError_t wa_launch_producer(const WaProducerLaunch& a, hipStream_t stream) {
   if (a.head_dim == 128) {
     hipLaunchKernelGGL(pool_kernel<128>, pgrid, dim3(kPoolThreads), 0, stream, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(head_max_kernel, dim3((unsigned)(2 * a.bh)), dim3(256), 0, stream, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(quant_kernel<128>, qgrid, dim3(256), 0, stream, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = hipFuncSetAttribute((const void*)score_select_kernel<128>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -243,6 +262,8 @@ hipError_t wa_launch_producer(const WaProducerLaunch& a, hipStream_t stream) {
     hipLaunchKernelGGL(score_select_kernel<128>, sgrid, dim3(kSelThreads), smem, stream, a);
   } else if (a.head_dim == 64) {
     hipLaunchKernelGGL(pool_kernel<64>, pgrid, dim3(kPoolThreads), 0, stream, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(head_max_kernel, dim3((unsigned)(2 * a.bh)), dim3(256), 0, stream, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(quant_kernel<64>, qgrid, dim3(256), 0, stream, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -9,6 +9,7 @@ struct WaProducerLaunch {
   const void* k;
   float* means;       // workspace float32 [2][bh][mb][head_dim]: block means of Q, then K
   uint32_t* amax;     // workspace [2][bh]: bits of the per-head maximum |mean|
+  uint32_t* bmax;     // workspace [2][bh][mb]: bits of each block's maximum |mean|
   int8_t* codes;      // [2][bh][mb][head_dim]: int8 codes of Q, then K
   uint8_t* mask;      // out [bh][mb][mb]
   int32_t bh, mb, seq_len, block, head_dim, keep, diagonal;
