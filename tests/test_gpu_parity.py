@@ -308,8 +308,9 @@ def test_output_bit_identical_across_permutations(name):
     lop[:, :, 1:] = wl.mb
     lop[:, :, 1] = wl.mb - 2
     lop = torch.from_numpy(lop).cuda()
+    # 64 queues: more queues than rows on the small heads (empty segments) and one row per segment on others
     for p, nx, sg in ((perm, 8, seg), (perm, 8, None), (perm, 1, None), (rnd, 8, None), (None, 1, None),
-                      (rnd, 8, lop)):
+                      (rnd, 8, lop), (rnd, 64, None), (None, 64, None)):
         o2, l2 = _run_attn(wl, mask, q, k, v, perm=p, n_xcd=nx, seg=sg)
         assert torch.equal(o2.view(torch.int16), o_nat.view(torch.int16))
         assert torch.equal(l2.view(torch.int32), l_nat.view(torch.int32))
