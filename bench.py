@@ -605,8 +605,8 @@ def main() -> int:
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the path is a single-GPU kernel pipeline "
-              "(see DESIGN.md for how it would shard across GPUs)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the path is a single-GPU kernel pipeline; across GPUs the "
+              "heads would shard with no exchange, each GPU running this path on its share", file=sys.stderr)
         return 2
 
     import torch
