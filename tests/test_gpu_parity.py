@@ -441,10 +441,11 @@ def _few_blocks(mask, heads, extra, seed):
     return sorted(picks)
 
 
-def test_attention_bench_launch_full_size():
-    """363,600 tokens, 40 heads: sampled rows against the oracle, and O / LSE bit-identical to the
-    natural order in the same launch configuration."""
-    wl = CONFIGS["long-720p-401f"]
+@pytest.mark.parametrize("name", ["long-720p-401f", "wan14b-720p-81f", "wan1.3b-480p-81f", "skip-d64"])
+def test_attention_bench_launch_full_size(name):
+    """Full-size workloads in the benchmark's launch configurations: sampled rows against the oracle,
+    and O / LSE bit-identical to the natural order."""
+    wl = CONFIGS[name]
     q, k, v = make_qkv(wl, threads=16)
     mask = make_mask(wl, threads=16)
     qd, kd, vd = bf16_dev(q), bf16_dev(k), bf16_dev(v)
@@ -462,11 +463,14 @@ def test_attention_bench_launch_full_size():
     tier1 = S.FLAG_FITS_CACHE | S.FLAG_LITTLE_WORK | S.FLAG_LOCAL
     for h in range(wl.heads):
         want = S.tier1_flags(S.head_stats(mask[0, h]), S.SkipProfile(), wl.block, wl.head_dim)
-        assert int(flags_auto[0, h]) & tier1 == want, h
+        got = int(flags_auto[0, h])
         if want:
+            assert got & tier1 == want, h
             assert np.array_equal(perm_auto[0, h], np.arange(wl.mb)), h
+        else:  # case 3 may still fire against the built order
+            assert got & (S.FLAG_FITS_CACHE | S.FLAG_LITTLE_WORK) == 0, h
     del o_nat, lse_nat, o_auto, lse_auto
-    picks = _few_blocks(mask, (0, 19, 39), 12, seed=4)
+    picks = _few_blocks(mask, (0, wl.heads // 2, wl.heads - 1), 12, seed=4)
     ref = A.block_sparse_attention_rows(q, k, v, mask, wl.block, picks)
     st = compare_blocks(_DeviceRows(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
     print(wl.name, st)
