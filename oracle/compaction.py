@@ -15,10 +15,6 @@ from __future__ import annotations
 import numpy as np
 
 
-def row_counts(mask: np.ndarray) -> np.ndarray:
-    return (np.asarray(mask) != 0).sum(axis=-1).astype(np.int32)
-
-
 def compact_head(mask_h: np.ndarray):
     """(row_ptr [M_B+1] int32, col_idx [nnz] int32) for one head."""
     m = mask_h.shape[0]

@@ -1,9 +1,10 @@
 """Mask statistics and the adaptive reordering skip (test infrastructure only).
 
-Sec. IV-E states the three situations in which reordering does not pay, and that
-the decision combines cheap mask statistics with offline profiles of kernel
-latency and reordering cost; Sec. VI-F shows it firing for short sequences and
-very sparse masks. The paper gives no formula, so the reading here is:
+Sec. IV-E names three situations in which reordering cannot repay its cost and
+says the decision is taken from a few mask statistics weighed against costs
+measured ahead of time on the target; Sec. VI-F shows the rule firing for short
+sequences and very sparse masks. The paper prints no formula, so the reading
+here is:
 
   case 1 "fits in cache": the head's distinct K/V blocks fit in the last-level
           cache that all compute units share (the paper's GPU: its L2; on the

@@ -23,6 +23,31 @@ def _wl(n=None, heads=2, d=32, blk=16, grid=(2, 4, 8), rule=None, seed=3):
     return custom("pin", heads=heads, head_dim=d, block=blk, grid=grid, rule=rule, seed=seed, seq_len=n)
 
 
+def _bf16_closed_form(b: int) -> float:
+    """Value of bf16 bit pattern b from the format's definition: sign bit, 8-bit biased
+    exponent (bias 127), 7-bit fraction; exponent 0 is subnormal, 255 infinity / NaN."""
+    sign = -1.0 if b >> 15 else 1.0
+    e, f = (b >> 7) & 0xFF, b & 0x7F
+    if e == 255:
+        return sign * math.inf if f == 0 else math.nan
+    if e == 0:
+        return sign * math.ldexp(f, -126 - 7)
+    return sign * math.ldexp(128 + f, e - 127 - 7)
+
+
+def test_bf16_widening_matches_torch_and_the_format_on_every_pattern():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    ours = A.bf16_to_f64(bits)
+    lib = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    form = np.array([_bf16_closed_form(int(b)) for b in bits])
+    nan = np.isnan(form)
+    assert nan.sum() == 2 * 127                        # 0x7F81..0x7FFF and 0xFF81..0xFFFF
+    assert np.array_equal(np.isnan(ours), nan) and np.array_equal(np.isnan(lib), nan)
+    assert np.array_equal(ours[~nan], form[~nan]) and np.array_equal(lib[~nan], form[~nan])
+    # signed zeros keep their sign
+    assert math.copysign(1.0, ours[0x8000]) == -1.0 and math.copysign(1.0, ours[0]) == 1.0
+
+
 def test_all_ones_equals_dense_and_library_sdpa():
     wl = _wl(rule=dict(kind="ones"))
     q, k, v = _qkv(wl)

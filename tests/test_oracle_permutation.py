@@ -279,6 +279,29 @@ def test_stage2_invariants(m, n_xcd, w):
             assert np.all(np.diff(nnz[perm[b0:b1]]) <= 0)
 
 
+def test_wave_objective_equals_brute_force_pairs_with_a_ragged_last_wave():
+    """Eq. 1 summed literally: over consecutive waves of at most W rows of the permuted
+    mask, over every ordered pair (i, j) of rows of a wave, the squared distance of the
+    two 0/1 rows (the size of their symmetric difference). 23 rows in waves of 5 leave
+    a last wave of 3 rows."""
+    rng = np.random.default_rng(31)
+    m, n, w = 23, 17, 5
+    mask = (rng.random((m, n)) < 0.35).astype(np.uint8)
+    for perm in (np.arange(m), rng.permutation(m), rng.permutation(m)):
+        rows = mask[perm].astype(np.int64)
+        brute = 0
+        for s in range(0, m, w):
+            wave = range(s, min(s + w, m))
+            for i in wave:
+                for j in wave:
+                    brute += int(((rows[i] - rows[j]) ** 2).sum())
+        assert OBJ.wave_objective(mask, perm, w) == brute
+    # one wave holding every row: the ordering cannot matter
+    assert OBJ.wave_objective(mask, rng.permutation(m), m) == OBJ.wave_objective(mask, np.arange(m), m)
+    # waves of one row: every term is a row with itself
+    assert OBJ.wave_objective(mask, rng.permutation(m), 1) == 0
+
+
 def test_wave_objective_improves_on_shuffled_clusters():
     rng = np.random.default_rng(12)
     protos = (rng.random((6, 64)) < 0.3).astype(np.uint8)
