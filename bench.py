@@ -246,11 +246,22 @@ def cpu_baseline(wl, q, k, v, mask, total_flop, budget_s: float):
     """The oracle, as it stands, timed on a bounded sample of the workload on the host cores."""
     from oracle import attention as A
     from oracle import permutation as P
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        pools = threadpool_info()
+        cores = max([p.get("num_threads", 1) for p in pools] or [1])
+        libs = [f"{p.get('internal_api')} {p.get('version')} ({p.get('threading_layer', '?')} threads)"
+                for p in pools if p.get("user_api") == "blas"]
+        blas = "; ".join(libs) or blas
     except Exception:
         cores = os.cpu_count() or 1
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next(ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
     rng = np.random.default_rng(7)
     # attention oracle on random query blocks until the budget is spent
     t0 = time.perf_counter()
@@ -272,6 +283,9 @@ def cpu_baseline(wl, q, k, v, mask, total_flop, budget_s: float):
         "value": total_flop / est_step / 1e12,
         "unit": "TFLOP/s",
         "cores": int(cores),
+        "cpu_model": cpu_model,
+        "host_threads": os.cpu_count(),
+        "blas": blas,
         "kind": "oracle",
         "sample": (f"fp64 oracle attention on {blocks} random query blocks ({flop_done / 1e9:.1f} GFLOP, "
                    f"{t_attn:.1f} s) plus the permutation oracle on 1 of {wl.batch * wl.heads} heads "
@@ -293,6 +307,9 @@ VARIANTS = {
     "random": dict(perm="random", n_xcd=1),
     "reordered-xcd": dict(perm="two-stage", skip="never", n_xcd=8),
     "natural-xcd": dict(perm=None, n_xcd=8),
+    "natural-interleaved": dict(perm=None, n_xcd=1, head_order="interleaved"),
+    "reordered-interleaved": dict(perm="two-stage", skip="never", n_xcd=1, wave_mult=8, head_order="interleaved"),
+    "auto-vnatural": dict(perm="two-stage", skip="auto", n_xcd=1, wave_mult=8, v_layout="natural"),
 }
 VARIANT_HELP = {
     "reordered": "two-stage order (Stage 1 polar sort + Stage 2 bucket sort), chip-wide waves, one queue, "
@@ -304,7 +321,12 @@ VARIANT_HELP = {
     "random": "a seeded random order, one queue (built on the host)",
     "reordered-xcd": "two-stage order, work-balanced XCD segments, one queue per XCD, skip never",
     "natural-xcd": "identity order, equal row-count XCD segments, one queue per XCD",
+    "natural-interleaved": "identity order, one queue, the heads' slots dealt round-robin (head-parallel)",
+    "reordered-interleaved": "as reordered, the heads' slots dealt round-robin (head-parallel)",
+    "auto-vnatural": "as auto, V passed in its natural [B][H][N][d] layout (transposed inside every call)",
 }
+# Every other variant passes V as V^T ([B][H][d][M_B*block], written once by transpose_v before the
+# timed steps, the layout a value projection can emit directly) and runs the heads in order.
 
 
 FLAG_NAMES = ((1, "fits_cache"), (2, "little_work"), (4, "local"), (8, "unstructured"), (16, "degenerate"))
@@ -564,6 +586,7 @@ def main() -> int:
                     help="comma list of: " + "; ".join(f"{k}: {v}" for k, v in VARIANT_HELP.items()))
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-xcd-bytes", action="store_true", help="skip the per-XCD compulsory K/V bytes (host work)")
     ap.add_argument("--no-gemm-reference", action="store_true",
                     help="skip timing the vendor library's dense bf16 GEMM (context for the roofline fraction)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -656,9 +679,18 @@ def main() -> int:
     col_idx = torch.empty((b_ * h_ * mb * mb,), dtype=torch.int32, device="cuda")
     o = torch.empty_like(qd)
     flags = torch.empty((b_, h_), dtype=torch.uint8, device="cuda")
-    attn_ws = torch.empty(W.attn_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    status = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    # V^T, as a value projection can emit it: written once here, an input of every timed step
+    vtd = W.transpose_v(vd, block=wl.block)
+    need_vnat = any(VARIANTS[x.strip()].get("v_layout") == "natural" for x in args.variants.split(",") if x.strip())
+    attn_ws = torch.empty(W.attn_workspace_size(shape) if need_vnat else W.attn_vt_workspace_size(shape),
+                          dtype=torch.uint8, device="cuda")
     wave = W.wave_size(wl.head_dim, wl.block)
     stream = torch.cuda.current_stream()
+    # 1 GiB written, then read, before every timed step: more than the eight L2s and the shared
+    # last-level cache hold, and the read evicts the written lines, so no step starts with cached
+    # K/V or pays for another call's write-backs
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     log(f"uploaded; nnz={nnz} density={nnz / (b_ * h_ * mb * mb):.4f} wave_per_xcd={wave}")
 
     rng = np.random.default_rng(12345)
@@ -684,10 +716,13 @@ def main() -> int:
     def make_step(variant):
         spec = VARIANTS[variant]
         n_xcd = spec["n_xcd"]
+        head_order = spec.get("head_order", "in-order")
+        v_natural = spec.get("v_layout") == "natural"
         fixed = (host_perm(spec["perm"], n_xcd, wave * spec.get("wave_mult", 1))
                  if spec["perm"] in ("random", "s2-only") else None)
         s1 = torch.empty((b_, h_, mb), dtype=torch.int32, device="cuda") if spec["perm"] == "stage1" else None
         seg_q = torch.empty((b_, h_, n_xcd + 1), dtype=torch.int32, device="cuda")
+        used_perm = {}
 
         def step(ev=None):
             p, sg = fixed, None
@@ -706,12 +741,47 @@ def main() -> int:
                                     row_ptr=row_ptr, col_idx=col_idx)
             if ev is not None:
                 ev[0].record(stream)
-            W.sparse_attn_csr(qd, kd, vd, rp, ci, p, sg, block=wl.block, n_xcd=n_xcd, out=o, workspace=attn_ws)
+            if v_natural:
+                W.sparse_attn_csr(qd, kd, vd, rp, ci, p, sg, block=wl.block, n_xcd=n_xcd, out=o, workspace=attn_ws,
+                                  status=status)
+            else:
+                W.sparse_attn_vt(qd, kd, vtd, rp, ci, p, sg, block=wl.block, n_xcd=n_xcd, head_order=head_order,
+                                 out=o, workspace=attn_ws, status=status)
             if ev is not None:
                 ev[1].record(stream)
+            used_perm["perm"], used_perm["seg"] = p, sg
+        step.used = used_perm
         return step
 
+    def xcd_kv_bytes(variant, used_perm):
+        """Compulsory K/V bytes when each XCD fetches every distinct block its own rows reference: with
+        one queue per XCD (n_xcd = 8) the rows of segment x run on XCD x; with one queue the slots go
+        round-robin over the 8 XCDs (slot t on XCD t mod 8, the order in which the first workgroups
+        start). Divided by the global compulsory bytes it is the duplication across the private L2s."""
+        spec = VARIANTS[variant]
+        p, sg = used_perm.get("perm"), used_perm.get("seg")
+        ph = p.cpu().numpy().reshape(b_ * h_, mb) if p is not None else None
+        sgh = sg.cpu().numpy().reshape(b_ * h_, -1) if sg is not None else None
+        total = 0
+        mk = mask.reshape(b_ * h_, mb, mb)
+        for hh in range(b_ * h_):
+            order = ph[hh] if ph is not None else np.arange(mb)
+            for x in range(8):
+                if spec["n_xcd"] == 8:
+                    if sgh is not None:
+                        rows = order[sgh[hh, x]:sgh[hh, x + 1]]
+                    else:
+                        base, extra = divmod(mb, 8)
+                        a0 = x * base + min(x, extra)
+                        rows = order[a0:a0 + base + (1 if x < extra else 0)]
+                else:
+                    rows = order[x::8]
+                if rows.size:
+                    total += int((mk[hh, rows].any(axis=0) * blk_tokens).sum())
+        return total * wl.head_dim * 2 * 2
+
     results = {}
+    xcd_bytes = {}
     for variant in [s.strip() for s in args.variants.split(",") if s.strip()]:
         step = make_step(variant)
         for _ in range(args.warmup):
@@ -719,24 +789,34 @@ def main() -> int:
         torch.cuda.synchronize()
         # per step: [0] attention start, [1] attention end, [2] step start, [3] permutation end
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         w0 = time.perf_counter()
-        start.record(stream)
         for i in range(args.steps):
+            flush.fill_(1.0)
+            flush.sum()
             step(evs[i])
-        end.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - w0
-        ms_step = start.elapsed_time(end) / args.steps
-        attn_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-        perm_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-        compact_ms = float(np.mean([e[3].elapsed_time(e[0]) for e in evs]))
+        steps_ms = [e[2].elapsed_time(e[1]) for e in evs]
+        attn = [e[0].elapsed_time(e[1]) for e in evs]
+        ms_step = _median(steps_ms)
+        attn_ms = _median(attn)
+        perm_ms = _median([e[2].elapsed_time(e[3]) for e in evs])
+        compact_ms = _median([e[3].elapsed_time(e[0]) for e in evs])
+        st = int(status.item())
+        if st != 0:
+            raise RuntimeError(f"{variant}: the attention call reported status {st}")
         results[variant] = dict(ms_per_step=ms_step, wall_ms_per_step=wall * 1e3 / args.steps, attn_ms=attn_ms,
+                                attn_ms_min=float(min(attn)), attn_ms_max=float(max(attn)),
                                 perm_ms=perm_ms, compact_ms=compact_ms,
                                 tflops_step=flop / (ms_step * 1e-3) / 1e12,
                                 tflops_attn=flop / (attn_ms * 1e-3) / 1e12)
-        log(f"{variant}: step {ms_step:.2f} ms, attention kernel {attn_ms:.2f} ms "
+        if VARIANTS[variant]["perm"] in ("two-stage", "stage1"):
+            f = flags.cpu().numpy().reshape(-1)
+            results[variant]["identity_heads"] = int(np.count_nonzero(f & 64))
+        if not args.no_xcd_bytes:
+            xcd_bytes[variant] = xcd_kv_bytes(variant, step.used)
+        log(f"{variant}: step {ms_step:.2f} ms, attention call {attn_ms:.2f} ms "
             f"({results[variant]['tflops_attn']:.1f} TFLOP/s)")
 
     head = next((v for v in ("auto", "reordered") if v in results), next(iter(results)))
@@ -765,12 +845,16 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": b_, "heads": h_, "seq_len": wl.seq_len, "head_dim": wl.head_dim,
                    "block": wl.block, "kept_blocks": nnz, "density": nnz / (b_ * h_ * mb * mb),
-                   "flop_per_step": flop, "variant": head, "wave_per_xcd": wave},
+                   "flop_per_step": flop, "variant": head, "wave_per_xcd": wave, "v_input": "transposed",
+                   "timing": "median over steps, each after a 1 GiB write + read cache flush"},
         "roofline": roof,
         "algorithmic_bytes": {"kv_compulsory": kv_bytes, "q_and_o": qo_bytes, "kv_lists": list_bytes,
                               "total": algo_bytes, "flop_per_byte": flop / algo_bytes},
         "variants": results,
     }
+    if xcd_bytes:
+        out["algorithmic_bytes"]["kv_compulsory_per_xcd"] = {
+            v: {"bytes": b, "vs_global": b / kv_bytes} for v, b in xcd_bytes.items()}
     if "natural" in results:
         out["speedup_vs_natural"] = {
             v: {"step": results["natural"]["ms_per_step"] / rv["ms_per_step"],

@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define WA_ABI_VERSION 1
+#define WA_ABI_VERSION 2
 #define WA_MAX_BLOCKS 4096
 
 typedef enum wa_status {
@@ -203,12 +203,21 @@ wa_status wa_mask_producer_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters,
  * per-queue prefix tables and the per-queue order of the last heads: 64 + 64 * (B*H + 1)
- * int32 rounded up to 64 entries, plus 64 * T * M_B int32 with T = min(B*H, 16384 / M_B, 256),
+ * int32 rounded up to 64 entries, plus 64 * T * M_B int32 with T = min(B*H, 16384 / M_B, 256)
+ * rounded up to 64 entries, plus 64 + B*H*M_B int32 for the head-interleaved order,
  * rounded up to 256 bytes),
  * a zero-padded transposed copy of V (bf16 [B][H][head_dim][M_B*block], rounded up
  * to 256 bytes), then the compacted lists. The first two parts (the leading part)
  * suffice for wa_sparse_attn_csr. Calls that share a workspace must not overlap. */
 wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
+
+/* Status word of the attention calls (device int32, nullable): zeroed by the call, then
+ * bits are set for what the call found. An invalid perm entry (outside 0..M_B-1)
+ * occupies its slot without computing anything, so the query block it should have
+ * named keeps whatever O held; an invalid KV index (outside 0..N_B-1, only possible
+ * with caller-built lists) is read as block 0. Readable once the stream has passed
+ * the call. Bijectivity of perm is not checked here (wa_check_perm does). */
+enum { WA_ATTN_BAD_PERM = 1, WA_ATTN_BAD_KV_INDEX = 2 };
 
 /* Block-sparse attention forward: for every query block i and token q in it,
  * O_q = softmax(scale * Q_q K_S^T) V_S over the tokens of the KV blocks with
@@ -237,10 +246,12 @@ wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes);
  *                order. The order changes when rows run, never what they compute.
  *   o            out bf16 [B][H][N][d]
  *   lse          out float [B][H][N] natural-log sum-exp of the scaled scores, nullable
+ *   status       out int32 status word (WA_ATTN_* bits), device, nullable
  *   workspace    >= wa_attn_workspace_size(shape) */
 wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint8_t* mask, const int32_t* perm,
                          const int32_t* seg_start, const wa_shape* shape, float softmax_scale, int32_t n_xcd,
-                         void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream);
+                         void* o, float* lse, int32_t* status, void* workspace, size_t workspace_bytes,
+                         void* stream);
 
 /* As wa_sparse_attn, from lists already built by wa_compact_mask (row i of head
  * (b,h) visits col_idx[(b*H+h)*M_B*N_B + row_ptr[b][h][i] ...] in list order).
@@ -248,8 +259,48 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                              const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
                              const wa_shape* shape,
-                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* workspace,
-                             size_t workspace_bytes, void* stream);
+                             float softmax_scale, int32_t n_xcd, void* o, float* lse, int32_t* status,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* V in the layout the attention kernel reads its P V operand from (Sec. II-C: the
+ * value tile of each kept KV block): vt[b][h][c][t] = V[b][h][t][c] for tokens
+ * t < N and 0 for N <= t < M_B*block.
+ *   v   bf16 [B][H][N][d], 16-byte aligned
+ *   vt  out bf16 [B][H][d][M_B*block], 16-byte aligned
+ * A model whose value projection writes this layout directly can skip this call and
+ * hand its output to wa_sparse_attn_vt. */
+wa_status wa_transpose_v(const void* v, const wa_shape* shape, void* vt, void* stream);
+
+/* Order of the query-block tasks of different heads within each task queue.
+ * IN_ORDER runs the heads one after another (each queue finishes head h's segment
+ * before head h+1's), so one head's K/V is in use at a time, as in the paper's
+ * sequential-head scheduling (Sec. V); INTERLEAVED deals the slots round-robin over the
+ * heads (slot r of every head, then slot r+1), so query blocks of all heads run
+ * together, as a head-parallel scheduler does (the baseline of Sec. VI-B). Both compute
+ * the same O; only the IN_ORDER form applies the end-of-launch order of the last heads. */
+enum { WA_HEADS_IN_ORDER = 0, WA_HEADS_INTERLEAVED = 1 };
+
+typedef struct wa_attn_options {
+  float softmax_scale;  /* <= 0 selects 1/sqrt(d) */
+  int32_t n_xcd;        /* XCD segments / task queues, 1..64 (as for wa_sparse_attn) */
+  int32_t head_order;   /* WA_HEADS_IN_ORDER or WA_HEADS_INTERLEAVED */
+} wa_attn_options;
+
+/* Workspace bytes needed by wa_sparse_attn_vt: the scheduler state of
+ * wa_attn_workspace_size alone. */
+wa_status wa_attn_vt_workspace_size(const wa_shape* shape, size_t* bytes);
+
+/* As wa_sparse_attn_csr, with V already in the layout wa_transpose_v writes, so the
+ * call reads V^T tiles straight from the caller's tensor (no copy of V per call).
+ *   vt         bf16 [B][H][d][M_B*block], 16-byte aligned; entries of tokens >= N must
+ *              be finite (wa_transpose_v writes zeros)
+ *   options    host pointer: softmax scale, n_xcd, head order
+ *   status     as for wa_sparse_attn
+ *   workspace  >= wa_attn_vt_workspace_size(shape), 256-byte aligned */
+wa_status wa_sparse_attn_vt(const void* q, const void* k, const void* vt, const int32_t* row_ptr,
+                            const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
+                            const wa_shape* shape, const wa_attn_options* options, void* o, float* lse,
+                            int32_t* status, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- diagnostics (used by the test suite; not needed by callers) ---- */
 

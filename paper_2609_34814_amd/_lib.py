@@ -17,6 +17,8 @@ WA_ERR_HIP = -6
 
 WA_SKIP_AUTO, WA_SKIP_NEVER, WA_SKIP_ALWAYS = 0, 1, 2
 FLAG_FITS_CACHE, FLAG_LITTLE_WORK, FLAG_LOCAL, FLAG_UNSTRUCTURED, FLAG_DEGENERATE, FLAG_IDENTITY = 1, 2, 4, 8, 16, 64
+WA_ATTN_BAD_PERM, WA_ATTN_BAD_KV_INDEX = 1, 2
+WA_HEADS_IN_ORDER, WA_HEADS_INTERLEAVED = 0, 1
 
 
 class WaShape(ctypes.Structure):
@@ -33,6 +35,10 @@ class WaSkipProfile(ctypes.Structure):
 class WaPermParams(ctypes.Structure):
     _fields_ = [("wave_per_xcd", c_int32), ("n_xcd", c_int32), ("iters", c_int32), ("skip_mode", c_int32),
                 ("seed", c_uint64), ("profile", POINTER(WaSkipProfile))]
+
+
+class WaAttnOptions(ctypes.Structure):
+    _fields_ = [("softmax_scale", c_float), ("n_xcd", c_int32), ("head_order", c_int32)]
 
 
 class WaError(RuntimeError):
@@ -60,10 +66,15 @@ _SIGNATURES = {
                                         c_void_p, c_size_t, c_void_p]),
     "wa_attn_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
     "wa_sparse_attn": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(WaShape),
-                                 c_float, c_int32, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+                                 c_float, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "wa_sparse_attn_csr": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                     POINTER(WaShape), c_float, c_int32, c_void_p, c_void_p, c_void_p, c_size_t,
-                                     c_void_p]),
+                                     POINTER(WaShape), c_float, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_size_t, c_void_p]),
+    "wa_transpose_v": (c_int32, [c_void_p, POINTER(WaShape), c_void_p, c_void_p]),
+    "wa_attn_vt_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
+    "wa_sparse_attn_vt": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                    POINTER(WaShape), POINTER(WaAttnOptions), c_void_p, c_void_p, c_void_p, c_void_p,
+                                    c_size_t, c_void_p]),
     "wa_fp64_probe": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p]),
     "wa_xcc_probe": (c_int32, [c_void_p, c_int32, c_void_p]),
 }

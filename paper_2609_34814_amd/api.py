@@ -14,6 +14,7 @@ import torch
 from . import _lib as L
 
 _SKIP = {"auto": L.WA_SKIP_AUTO, "never": L.WA_SKIP_NEVER, "always": L.WA_SKIP_ALWAYS}
+_HEAD_ORDER = {"in-order": L.WA_HEADS_IN_ORDER, "interleaved": L.WA_HEADS_INTERLEAVED}
 
 
 def _stream() -> ctypes.c_void_p:
@@ -31,13 +32,42 @@ def _dev(t: torch.Tensor, name: str) -> None:
         raise ValueError(f"{name} must be contiguous")
 
 
-def _mask_u8(mask: torch.Tensor) -> torch.Tensor:
-    _dev(mask, "mask")
-    if mask.dtype == torch.bool:
-        return mask.view(torch.uint8)
-    if mask.dtype != torch.uint8:
+def _mask_u8(mask: torch.Tensor, shape=None) -> torch.Tensor:
+    """The mask as uint8, checked against the expected [B][H][M_B][N_B] shape (if given) before
+    its placement, so that a mismatch is reported the same way on any device."""
+    if mask.dtype not in (torch.bool, torch.uint8):
         raise ValueError("mask must be uint8 or bool")
-    return mask
+    if mask.dim() != 4 or (shape is not None and tuple(mask.shape) != tuple(shape)):
+        want = "[B][H][M_B][N_B]" if shape is None else str(tuple(shape))
+        raise ValueError(f"mask must have shape {want}, got {tuple(mask.shape)}")
+    if mask.shape[2] != mask.shape[3]:
+        raise ValueError(f"mask must be square per head (M_B = N_B), got {tuple(mask.shape)}")
+    return mask.view(torch.uint8) if mask.dtype == torch.bool else mask
+
+
+def _check(t: Optional[torch.Tensor], name: str, dtype, shape=None, numel_min: Optional[int] = None) -> None:
+    """dtype and shape (or minimum element count) of an optional tensor argument."""
+    if t is None:
+        return
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if numel_min is not None and t.numel() < numel_min:
+        raise ValueError(f"{name} must hold at least {numel_min} elements, got {t.numel()}")
+
+
+def _on_device(**tensors) -> None:
+    """Placement and layout, checked once every shape is known to be right."""
+    for name, t in tensors.items():
+        if t is not None:
+            _dev(t, name)
+
+
+def _mask_dims(mask: torch.Tensor, seq_len: int, block: int):
+    b, h = mask.shape[0], mask.shape[1]
+    mb = -(-seq_len // block)
+    return b, h, mb
 
 
 def shape_of(batch: int, heads: int, seq_len: int, head_dim: int, block: int) -> L.WaShape:
@@ -79,8 +109,9 @@ def attn_workspace_size(shape: L.WaShape) -> int:
 def mask_stats(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 128):
     """(row_nnz [B][H][M_B], col_cnt [B][H][N_B], head_stats [B][H][6]) as device tensors."""
     lib = L.load()
-    mask = _mask_u8(mask)
-    b, h, mb, _ = mask.shape
+    b, h, mb = _mask_dims(mask, seq_len, block)
+    mask = _mask_u8(mask, (b, h, mb, mb))
+    _on_device(mask=mask)
     shape = shape_of(b, h, seq_len, head_dim, block)
     dev = mask.device
     row_nnz = torch.empty((b, h, mb), dtype=torch.int32, device=dev)
@@ -101,8 +132,16 @@ def build_permutation(mask: torch.Tensor, *, seq_len: int, block: int, head_dim:
     """(perm int32 [B][H][M_B], seg_start int32 [B][H][n_xcd+1], head flags uint8 [B][H])
     (plus embedding and Stage-1 order if asked; stage1_out, if given, receives the Stage-1 order)."""
     lib = L.load()
-    mask = _mask_u8(mask)
-    b, h, mb, nb = mask.shape
+    b, h, mb = _mask_dims(mask, seq_len, block)
+    mask = _mask_u8(mask, (b, h, mb, mb))
+    if skip not in _SKIP:
+        raise ValueError(f"skip must be one of {sorted(_SKIP)}")
+    _check(out, "out", torch.int32, (b, h, mb))
+    _check(flags_out, "flags_out", torch.uint8, (b, h))
+    _check(seg_out, "seg_out", torch.int32, (b, h, n_xcd + 1))
+    _check(stage1_out, "stage1_out", torch.int32, (b, h, mb))
+    _check(workspace, "workspace", torch.uint8)
+    _on_device(mask=mask, out=out, flags_out=flags_out, seg_out=seg_out, stage1_out=stage1_out, workspace=workspace)
     shape = shape_of(b, h, seq_len, head_dim, block)
     dev = mask.device
     perm = torch.empty((b, h, mb), dtype=torch.int32, device=dev) if out is None else out
@@ -128,15 +167,16 @@ def compact_mask(mask: torch.Tensor, *, seq_len: int, block: int, head_dim: int 
                  row_ptr: Optional[torch.Tensor] = None, col_idx: Optional[torch.Tensor] = None):
     """CSR lists: row_ptr int32 [B][H][M_B+1] (head-local offsets), col_idx int32 [B*H*M_B*N_B]."""
     lib = L.load()
-    mask = _mask_u8(mask)
-    b, h, mb, nb = mask.shape
+    b, h, mb = _mask_dims(mask, seq_len, block)
+    mask = _mask_u8(mask, (b, h, mb, mb))
+    _check(row_ptr, "row_ptr", torch.int32, (b, h, mb + 1))
+    _check(col_idx, "col_idx", torch.int32, numel_min=b * h * mb * mb)
+    _on_device(mask=mask, row_ptr=row_ptr, col_idx=col_idx)
     shape = shape_of(b, h, seq_len, head_dim, block)
     if row_ptr is None:
         row_ptr = torch.empty((b, h, mb + 1), dtype=torch.int32, device=mask.device)
     if col_idx is None:
-        col_idx = torch.empty((b * h * mb * nb,), dtype=torch.int32, device=mask.device)
-    if row_ptr.numel() < b * h * (mb + 1) or col_idx.numel() < b * h * mb * nb:
-        raise ValueError("row_ptr / col_idx too small")
+        col_idx = torch.empty((b * h * mb * mb,), dtype=torch.int32, device=mask.device)
     L.check(lib.wa_compact_mask(_ptr(mask), ctypes.byref(shape), _ptr(row_ptr), _ptr(col_idx), _stream()))
     return row_ptr, col_idx
 
@@ -197,54 +237,140 @@ def check_perm(perm: torch.Tensor, *, seq_len: int, block: int, head_dim: int = 
     return True
 
 
-def _attn_args(q, k, v, block):
+def _attn_args(q, k, v, block, v_transposed=False):
+    """Shape of the call from q, k, v (checked before their placement); v may be the transposed
+    [B][H][d][M_B*block] layout."""
     for t, nm in ((q, "q"), (k, "k"), (v, "v")):
-        _dev(t, nm)
         if t.dtype != torch.bfloat16:
             raise ValueError(f"{nm} must be bfloat16")
-    if q.shape != k.shape or q.shape != v.shape or q.dim() != 4:
-        raise ValueError("q, k, v must share one [B][H][N][d] shape")
+    if q.dim() != 4 or q.shape != k.shape:
+        raise ValueError("q and k must share one [B][H][N][d] shape")
     b, h, n, d = q.shape
+    if v_transposed:
+        want = (b, h, d, -(-n // block) * block)
+        if tuple(v.shape) != want:
+            raise ValueError(f"vt must have shape {want} ([B][H][d][M_B*block]), got {tuple(v.shape)}")
+    elif v.shape != q.shape:
+        raise ValueError("q, k, v must share one [B][H][N][d] shape")
     return shape_of(b, h, n, d, block)
+
+
+def _attn_outputs(q, out, status, return_lse):
+    _check(out, "out", torch.bfloat16, tuple(q.shape))
+    _check(status, "status", torch.int32, numel_min=1)
+    if out is None or return_lse:
+        _on_device(q=q)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if return_lse else None
+    return o, lse
+
+
+def _order_args(q, block, perm, seg, n_xcd):
+    b, h, n, _ = q.shape
+    mb = -(-n // block)
+    if not 1 <= int(n_xcd) <= 64:
+        raise ValueError("n_xcd must lie in 1..64")
+    _check(perm, "perm", torch.int32, (b, h, mb))
+    _check(seg, "seg", torch.int32, (b, h, int(n_xcd) + 1))
+    return b, h, mb
+
+
+def _csr_args(row_ptr, col_idx, b, h, mb):
+    if row_ptr is None or col_idx is None:
+        raise ValueError("row_ptr and col_idx are required")
+    _check(row_ptr, "row_ptr", torch.int32, (b, h, mb + 1))
+    _check(col_idx, "col_idx", torch.int32, numel_min=b * h * mb * mb)
 
 
 def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: torch.Tensor,
                 perm: Optional[torch.Tensor] = None, seg: Optional[torch.Tensor] = None, *, block: int,
                 scale: Optional[float] = None,
                 n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None,
-                workspace: Optional[torch.Tensor] = None):
-    """O = block-sparse softmax attention of q over the kept KV blocks, in the original row order."""
+                workspace: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None):
+    """O = block-sparse softmax attention of q over the kept KV blocks, in the original row order.
+    `status` (int32, device) receives the call's WA_ATTN_* bits."""
     lib = L.load()
     shape = _attn_args(q, k, v, block)
-    mask = _mask_u8(mask)
-    if perm is not None:
-        _dev(perm, "perm")
-        if perm.dtype != torch.int32:
-            raise ValueError("perm must be int32")
-    o = torch.empty_like(q) if out is None else out
-    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if return_lse else None
+    b, h, mb = _order_args(q, block, perm, seg, n_xcd)
+    mask = _mask_u8(mask, (b, h, mb, mb))
+    _check(workspace, "workspace", torch.uint8)
+    o, lse = _attn_outputs(q, out, status, return_lse)
+    _on_device(q=q, k=k, v=v, mask=mask, perm=perm, seg=seg, out=o, status=status, workspace=workspace)
     need = attn_workspace_size(shape)
     if workspace is None or workspace.numel() < need:
         workspace = _workspace(need, q.device)
     L.check(lib.wa_sparse_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(mask), _ptr(perm), _ptr(seg), ctypes.byref(shape),
-                               float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse), _ptr(workspace),
+                               float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse), _ptr(status), _ptr(workspace),
                                workspace.numel(), _stream()))
     return (o, lse) if return_lse else o
 
 
 def sparse_attn_csr(q, k, v, row_ptr, col_idx, perm=None, seg=None, *, block: int, scale: Optional[float] = None,
                     n_xcd: int = 8, return_lse: bool = False, out: Optional[torch.Tensor] = None,
-                    workspace: Optional[torch.Tensor] = None):
+                    workspace: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None):
+    """As sparse_attn, from the lists of compact_mask."""
     lib = L.load()
     shape = _attn_args(q, k, v, block)
-    o = torch.empty_like(q) if out is None else out
-    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if return_lse else None
+    b, h, mb = _order_args(q, block, perm, seg, n_xcd)
+    _csr_args(row_ptr, col_idx, b, h, mb)
+    _check(workspace, "workspace", torch.uint8)
+    o, lse = _attn_outputs(q, out, status, return_lse)
+    _on_device(q=q, k=k, v=v, row_ptr=row_ptr, col_idx=col_idx, perm=perm, seg=seg, out=o, status=status,
+               workspace=workspace)
     need = attn_workspace_size(shape)
     if workspace is None or workspace.numel() < need:
         workspace = _workspace(need, q.device)
     L.check(lib.wa_sparse_attn_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr), _ptr(col_idx), _ptr(perm), _ptr(seg),
                                    ctypes.byref(shape), float(scale or 0.0), int(n_xcd), _ptr(o), _ptr(lse),
-                                   _ptr(workspace), workspace.numel(), _stream()))
+                                   _ptr(status), _ptr(workspace), workspace.numel(), _stream()))
+    return (o, lse) if return_lse else o
+
+
+def transpose_v(v: torch.Tensor, *, block: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """V [B][H][N][d] -> V^T [B][H][d][M_B*block], zero past the last token (the layout of sparse_attn_vt)."""
+    lib = L.load()
+    if v.dtype != torch.bfloat16 or v.dim() != 4:
+        raise ValueError("v must be a bfloat16 [B][H][N][d] tensor")
+    b, h, n, d = v.shape
+    want = (b, h, d, -(-n // block) * block)
+    _check(out, "out", torch.bfloat16, want)
+    _on_device(v=v, out=out)
+    vt = torch.empty(want, dtype=torch.bfloat16, device=v.device) if out is None else out
+    shape = shape_of(b, h, n, d, block)
+    L.check(lib.wa_transpose_v(_ptr(v), ctypes.byref(shape), _ptr(vt), _stream()))
+    return vt
+
+
+def attn_vt_workspace_size(shape: L.WaShape) -> int:
+    lib = L.load()
+    n = ctypes.c_size_t(0)
+    L.check(lib.wa_attn_vt_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
+    return n.value
+
+
+def sparse_attn_vt(q, k, vt, row_ptr, col_idx, perm=None, seg=None, *, block: int, scale: Optional[float] = None,
+                   n_xcd: int = 8, head_order: str = "in-order", return_lse: bool = False,
+                   out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                   status: Optional[torch.Tensor] = None):
+    """As sparse_attn_csr with V given as V^T (transpose_v's layout); head_order is "in-order" (heads one
+    after another in every queue) or "interleaved" (round-robin over the heads)."""
+    lib = L.load()
+    if head_order not in _HEAD_ORDER:
+        raise ValueError(f"head_order must be one of {sorted(_HEAD_ORDER)}")
+    shape = _attn_args(q, k, vt, block, v_transposed=True)
+    b, h, mb = _order_args(q, block, perm, seg, n_xcd)
+    _csr_args(row_ptr, col_idx, b, h, mb)
+    _check(workspace, "workspace", torch.uint8)
+    o, lse = _attn_outputs(q, out, status, return_lse)
+    _on_device(q=q, k=k, vt=vt, row_ptr=row_ptr, col_idx=col_idx, perm=perm, seg=seg, out=o, status=status,
+               workspace=workspace)
+    need = attn_vt_workspace_size(shape)
+    if workspace is None or workspace.numel() < need:
+        workspace = _workspace(need, q.device)
+    opts = L.WaAttnOptions(float(scale or 0.0), int(n_xcd), _HEAD_ORDER[head_order])
+    L.check(lib.wa_sparse_attn_vt(_ptr(q), _ptr(k), _ptr(vt), _ptr(row_ptr), _ptr(col_idx), _ptr(perm), _ptr(seg),
+                                  ctypes.byref(shape), ctypes.byref(opts), _ptr(o), _ptr(lse), _ptr(status),
+                                  _ptr(workspace), workspace.numel(), _stream()))
     return (o, lse) if return_lse else o
 
 

@@ -154,11 +154,14 @@ const wa_skip_profile kDefaultProfile = {
     0.05,                    // eta_min
 };
 
-wa_status check_attn_common(const void* q, const void* k, const void* v, void* o, int32_t n_xcd) {
+wa_status check_attn_common(const void* q, const void* k, const void* v, void* o, int32_t n_xcd, float* lse,
+                            int32_t* status) {
   if (!q || !k || !v || !o) return fail(WA_ERR_INVALID_ARG, "q, k, v and o must be non-null");
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16))
     return fail(WA_ERR_ALIGNMENT, "q, k, v and o must be 16-byte aligned");
   if (n_xcd < 1 || n_xcd > kMaxXcd) return fail(WA_ERR_INVALID_ARG, "n_xcd %d outside 1..%d", n_xcd, kMaxXcd);
+  if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
+  if (status && !aligned(status, 4)) return fail(WA_ERR_ALIGNMENT, "status must be 4-byte aligned");
   return WA_OK;
 }
 
@@ -172,15 +175,17 @@ wa_status launch_compact(const uint8_t* mask, const Dims& d, int32_t* row_ptr, i
   return WA_OK;
 }
 
-wa_status launch_attn(const void* q, const void* k, const void* v, void* ws, const int32_t* row_ptr,
+// v: V in its natural layout (transposed into the workspace after the scheduler state), or null with
+// vt: V already transposed by the caller.
+wa_status launch_attn(const void* q, const void* k, const void* v, const void* vt, void* ws, const int32_t* row_ptr,
                       const int32_t* col_idx, const int32_t* perm, const int32_t* seg, const Dims& d, float scale,
-                      int32_t n_xcd, void* o, float* lse, hipStream_t st) {
+                      int32_t n_xcd, int32_t head_order, void* o, float* lse, int32_t* status, hipStream_t st) {
   WaAttnLaunch a{};
   a.q = q; a.k = k; a.v = v;
   a.sched = (int32_t*)ws;
-  a.vt = (char*)ws + attn_sched_bytes(d);
+  a.vt = v ? (void*)((char*)ws + attn_sched_bytes(d)) : const_cast<void*>(vt);
   a.row_ptr = row_ptr; a.col_idx = col_idx; a.perm = perm; a.seg = seg;
-  a.o = o; a.lse = lse;
+  a.o = o; a.lse = lse; a.status = status; a.head_order = head_order;
   a.bh = (int32_t)d.bh; a.seq_len = d.n; a.mb = d.mb; a.head_dim = d.d; a.block = d.blk; a.n_xcd = n_xcd;
   a.scale = (scale > 0.f && std::isfinite(scale)) ? scale : (float)(1.0 / std::sqrt((double)d.d));
   hipError_t e = wa_launch_attention(a, st);
@@ -412,14 +417,14 @@ wa_status wa_attn_workspace_size(const wa_shape* shape, size_t* bytes) {
 
 wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint8_t* mask, const int32_t* perm,
                          const int32_t* seg_start, const wa_shape* shape, float softmax_scale, int32_t n_xcd,
-                         void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+                         void* o, float* lse, int32_t* status, void* workspace, size_t workspace_bytes,
+                         void* stream) {
   Dims d;
   wa_status s = check_shape(shape, &d);
   if (s != WA_OK) return s;
-  s = check_attn_common(q, k, v, o, n_xcd);
+  s = check_attn_common(q, k, v, o, n_xcd, lse, status);
   if (s != WA_OK) return s;
   if (!mask) return fail(WA_ERR_INVALID_ARG, "mask is null");
-  if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
   s = check_ws(workspace, workspace_bytes, attn_ws_bytes(d));
   if (s != WA_OK) return s;
   hipStream_t st = (hipStream_t)stream;
@@ -428,7 +433,8 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
   int32_t* col_idx = (int32_t*)(base + attn_csr_ws_bytes(d) + align_up((size_t)d.bh * (d.mb + 1) * 4));
   s = launch_compact(mask, d, row_ptr, col_idx, st);
   if (s != WA_OK) return s;
-  s = launch_attn(q, k, v, base, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, o, lse, st);
+  s = launch_attn(q, k, v, nullptr, base, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, 0, o, lse,
+                  status, st);
   if (s != WA_OK) return s;
   return ok();
 }
@@ -436,19 +442,59 @@ wa_status wa_sparse_attn(const void* q, const void* k, const void* v, const uint
 wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                              const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
                              const wa_shape* shape,
-                             float softmax_scale, int32_t n_xcd, void* o, float* lse, void* workspace,
-                             size_t workspace_bytes, void* stream) {
+                             float softmax_scale, int32_t n_xcd, void* o, float* lse, int32_t* status,
+                             void* workspace, size_t workspace_bytes, void* stream) {
   Dims d;
   wa_status s = check_shape(shape, &d);
   if (s != WA_OK) return s;
-  s = check_attn_common(q, k, v, o, n_xcd);
+  s = check_attn_common(q, k, v, o, n_xcd, lse, status);
   if (s != WA_OK) return s;
   if (!row_ptr || !col_idx) return fail(WA_ERR_INVALID_ARG, "row_ptr and col_idx must be non-null");
-  if (lse && !aligned(lse, 4)) return fail(WA_ERR_ALIGNMENT, "lse must be 4-byte aligned");
   s = check_ws(workspace, workspace_bytes, attn_csr_ws_bytes(d));
   if (s != WA_OK) return s;
-  s = launch_attn(q, k, v, workspace, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, o, lse,
-                  (hipStream_t)stream);
+  s = launch_attn(q, k, v, nullptr, workspace, row_ptr, col_idx, perm, seg_start, d, softmax_scale, n_xcd, 0, o, lse,
+                  status, (hipStream_t)stream);
+  if (s != WA_OK) return s;
+  return ok();
+}
+
+wa_status wa_transpose_v(const void* v, const wa_shape* shape, void* vt, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!v || !vt) return fail(WA_ERR_INVALID_ARG, "v and vt must be non-null");
+  if (!aligned(v, 16) || !aligned(vt, 16)) return fail(WA_ERR_ALIGNMENT, "v and vt must be 16-byte aligned");
+  hipError_t e = wa_launch_transpose_v(v, vt, d.bh, d.n, d.mb, d.d, d.blk, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "transpose launch");
+  return ok();
+}
+
+wa_status wa_attn_vt_workspace_size(const wa_shape* shape, size_t* bytes) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!bytes) return fail(WA_ERR_INVALID_ARG, "bytes is null");
+  *bytes = attn_sched_bytes(d);
+  return ok();
+}
+
+wa_status wa_sparse_attn_vt(const void* q, const void* k, const void* vt, const int32_t* row_ptr,
+                            const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
+                            const wa_shape* shape, const wa_attn_options* options, void* o, float* lse,
+                            int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!options) return fail(WA_ERR_INVALID_ARG, "options is null");
+  s = check_attn_common(q, k, vt, o, options->n_xcd, lse, status);
+  if (s != WA_OK) return s;
+  if (options->head_order != WA_HEADS_IN_ORDER && options->head_order != WA_HEADS_INTERLEAVED)
+    return fail(WA_ERR_INVALID_ARG, "head_order %d invalid", options->head_order);
+  if (!row_ptr || !col_idx) return fail(WA_ERR_INVALID_ARG, "row_ptr and col_idx must be non-null");
+  s = check_ws(workspace, workspace_bytes, attn_sched_bytes(d));
+  if (s != WA_OK) return s;
+  s = launch_attn(q, k, nullptr, vt, workspace, row_ptr, col_idx, perm, seg_start, d, options->softmax_scale,
+                  options->n_xcd, options->head_order, o, lse, status, (hipStream_t)stream);
   if (s != WA_OK) return s;
   return ok();
 }

@@ -212,6 +212,13 @@ __device__ bool fetch_task(const WaAttnLaunch& a, int home, int* bh_out, int* sl
     if (__hip_atomic_load(cnt + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= total) continue;
     const int t = atomicAdd(cnt + x, 1);
     if (t >= total) continue;
+    if (a.head_order) {  // round-robin over the heads: the call's order table
+      const int32_t* ilv = a.sched + wa::ilv_offset(a.bh, a.mb, a.n_xcd);
+      const int ent = ilv[64 + ilv[x] + t];
+      *bh_out = ent / a.mb;
+      *slot_out = ent - *bh_out * a.mb;
+      return true;
+    }
     const int tb = px[a.bh - th];
     if (t >= tb) {  // the last heads: the call's tail order
       const int e = a.sched[wa::tail_offset(a.bh, a.n_xcd) + (int64_t)x * th * a.mb + (t - tb)];
@@ -281,7 +288,10 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     __syncthreads();  // every wavefront has read the task before it is overwritten
     if (bh < 0) break;
     const int row = a.perm ? a.perm[(int64_t)bh * a.mb + slot] : slot;
-    if ((unsigned)row >= (unsigned)a.mb) continue;  // not a valid block index: nothing to compute
+    if ((unsigned)row >= (unsigned)a.mb) {  // not a valid block index: nothing to compute, reported
+      if (tid == 0 && a.status) atomicOr(a.status, 1);
+      continue;
+    }
 
     const uint16_t* qg = (const uint16_t*)a.q + (int64_t)bh * n * D;
     const unsigned char* kg = (const unsigned char*)a.k + (int64_t)bh * n * D * 2;
@@ -307,6 +317,7 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     }
 
     f32x16 oacc[C::DT];
+    int bad_kv = 0;           // the row's list held an index outside 0..mb-1 (uniform)
     float m_run = -INFINITY;  // reference maximum (log2 units), set by the row's first block
     float l_run = 0.f;
     int j_cur = 0;
@@ -376,7 +387,10 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       int j_next = 0;
       if (has_next) {
         j_next = cols[e + 1];
-        if ((unsigned)j_next >= (unsigned)a.mb) j_next = 0;
+        if ((unsigned)j_next >= (unsigned)a.mb) {  // invalid KV index: block 0 is read, reported
+          j_next = 0;
+          bad_kv = 1;
+        }
       }
 
       // K_j resident (V_j may still be in flight)
@@ -450,7 +464,10 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
     for (int pass = 0;; ++pass) {
       if (beg < end) {
         j_cur = cols[beg];
-        if ((unsigned)j_cur >= (unsigned)a.mb) j_cur = 0;
+        if ((unsigned)j_cur >= (unsigned)a.mb) {
+          j_cur = 0;
+          bad_kv = 1;
+        }
         issue_tile<D, BLK, false>(k_lds, kg, j_cur * BLK, n, w, lane);
         issue_vt<D, BLK>(v_lds, vtg, vt_row_bytes, j_cur * BLK, w, lane);
       }
@@ -520,13 +537,16 @@ __global__ __launch_bounds__(BLK * 2, 2) void attn_fwd_kernel(WaAttnLaunch a) {
       if (a.lse && hf == 0)
         a.lse[(int64_t)bh * n + qi] = ltot > 0.f ? (m_run + __log2f(ltot)) * kLn2 : -INFINITY;
     }
+    if (bad_kv && tid == 0 && a.status) atomicOr(a.status, 2);
   }
 }
 
-// Scheduler set-up: zero the queue counters and build, per queue, the prefix sums of its segment
-// lengths over the heads. One workgroup; thread x handles queue x.
-__global__ __launch_bounds__(64) void sched_kernel(int32_t* sched, const int32_t* seg, int bh, int mb, int n_xcd) {
+// Scheduler set-up: zero the queue counters and the status word, and build, per queue, the prefix
+// sums of its segment lengths over the heads. One workgroup; thread x handles queue x.
+__global__ __launch_bounds__(64) void sched_kernel(int32_t* sched, const int32_t* seg, int32_t* status, int bh,
+                                                   int mb, int n_xcd) {
   const int x = threadIdx.x;
+  if (x == 0 && status) *status = 0;
   if (x >= n_xcd) return;
   sched[x] = 0;
   int32_t* px = sched + 64 + (int64_t)x * (bh + 1);
@@ -686,6 +706,46 @@ __global__ __launch_bounds__(1024) void tail_order_kernel(WaAttnLaunch a, int gr
   }
 }
 
+// Head-interleaved order of queue x (one workgroup per queue): the queue's tasks round-robin over the
+// heads, round r taking slot s0_h + r of every head h whose segment of the queue has more than r
+// slots, heads ascending. Entry (h, r) therefore sits at C(r) + #{h' < h : L_h' > r}, with L_h the
+// segment length and C(r) = sum_h min(L_h, r) the entries of the rounds before r. Entries are
+// h * mb + slot; queue x's entries start at the total of queues 0..x-1 (ilv[x]).
+__global__ __launch_bounds__(1024) void ilv_order_kernel(WaAttnLaunch a) {
+  constexpr int NT = 1024;
+  constexpr int RPT = WA_MAX_BLOCKS / NT;  // rounds per thread: r = t + k NT < mb <= WA_MAX_BLOCKS
+  __shared__ int off_s;
+  const int x = blockIdx.x;
+  const int t = threadIdx.x;
+  int32_t* ilv = a.sched + wa::ilv_offset(a.bh, a.mb, a.n_xcd);
+  if (t == 0) {
+    int off = 0;
+    for (int y = 0; y < x; ++y) off += a.sched[64 + (int64_t)y * (a.bh + 1) + a.bh];
+    ilv[x] = off;
+    off_s = off;
+  }
+  __syncthreads();
+  int32_t* out = ilv + 64 + off_s;
+  int c[RPT];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) c[k] = 0;
+  for (int h = 0; h < a.bh; ++h) {
+    int s0, s1;
+    wa::xcd_segment(x, a.mb, a.n_xcd, a.seg ? a.seg + (int64_t)h * (a.n_xcd + 1) : nullptr, &s0, &s1);
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) c[k] += min(s1 - s0, t + k * NT);
+  }
+  for (int h = 0; h < a.bh; ++h) {
+    int s0, s1;
+    wa::xcd_segment(x, a.mb, a.n_xcd, a.seg ? a.seg + (int64_t)h * (a.n_xcd + 1) : nullptr, &s0, &s1);
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      const int r = t + k * NT;
+      if (r < s1 - s0) out[c[k]++] = h * a.mb + s0 + r;
+    }
+  }
+}
+
 // V [bh][n][D] -> V^T [bh][D][npad], zero for keys >= n. One 64-key x 64-column tile per workgroup,
 // 16-byte loads and stores, transposed through LDS.
 template <int D>
@@ -734,9 +794,20 @@ int resident_cus() {
   return cached[dev];
 }
 
+template <int D>
+hipError_t launch_transpose(const void* v, void* vt, int64_t bh, int n, int mb, int blk, hipStream_t stream) {
+  const int64_t npad = (int64_t)mb * blk;
+  const int tiles_n = (int)((npad + 63) / 64);
+  const int64_t tgrid = bh * (D / 64) * tiles_n;
+  if (tgrid <= 0) return hipSuccess;
+  hipLaunchKernelGGL((transpose_v_kernel<D>), dim3((unsigned)tgrid), dim3(256), 0, stream, (const uint16_t*)v,
+                     (uint16_t*)vt, n, npad, tiles_n);
+  return hipGetLastError();
+}
+
 template <int D, int BLK>
 hipError_t launch_t(const WaAttnLaunch& a, hipStream_t stream) {
-  hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(64), 0, stream, a.sched, a.seg, a.bh, a.mb, a.n_xcd);
+  hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(64), 0, stream, a.sched, a.seg, a.status, a.bh, a.mb, a.n_xcd);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t tasks = (int64_t)a.bh * a.mb;
@@ -745,16 +816,15 @@ hipError_t launch_t(const WaAttnLaunch& a, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const int64_t grid = std::min<int64_t>(tasks, (int64_t)resident_cus() * std::max(occ, 1));
   if (tasks > 0) {
-    hipLaunchKernelGGL(tail_order_kernel, dim3(a.n_xcd), dim3(1024), 0, stream, a, (int)grid);
+    if (a.head_order) {
+      hipLaunchKernelGGL(ilv_order_kernel, dim3(a.n_xcd), dim3(1024), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL(tail_order_kernel, dim3(a.n_xcd), dim3(1024), 0, stream, a, (int)grid);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  const int64_t npad = (int64_t)a.mb * BLK;
-  const int tiles_n = (int)((npad + 63) / 64);
-  const int64_t tgrid = (int64_t)a.bh * (D / 64) * tiles_n;
-  if (tgrid > 0) {
-    hipLaunchKernelGGL((transpose_v_kernel<D>), dim3((unsigned)tgrid), dim3(256), 0, stream, (const uint16_t*)a.v,
-                       (uint16_t*)a.vt, a.seq_len, npad, tiles_n);
-    e = hipGetLastError();
+  if (a.v) {  // V given in its natural layout: the call's transposed copy
+    e = launch_transpose<D>(a.v, a.vt, a.bh, a.seq_len, a.mb, BLK, stream);
     if (e != hipSuccess) return e;
   }
   if (tasks <= 0) return hipSuccess;
@@ -778,6 +848,13 @@ hipError_t wa_launch_attention(const WaAttnLaunch& a, hipStream_t stream) {
   if (a.head_dim == 64 && a.block == 128) return launch_t<64, 128>(a, stream);
   if (a.head_dim == 128 && a.block == 64) return launch_t<128, 64>(a, stream);
   if (a.head_dim == 64 && a.block == 64) return launch_t<64, 64>(a, stream);
+  return hipErrorInvalidValue;
+}
+
+hipError_t wa_launch_transpose_v(const void* v, void* vt, int64_t bh, int seq_len, int mb, int head_dim, int block,
+                                 hipStream_t stream) {
+  if (head_dim == 128) return launch_transpose<128>(v, vt, bh, seq_len, mb, block, stream);
+  if (head_dim == 64) return launch_transpose<64>(v, vt, bh, seq_len, mb, block, stream);
   return hipErrorInvalidValue;
 }
 

@@ -41,8 +41,13 @@ __host__ __device__ inline int tail_heads(int64_t bh, int m) {
   return (int)(bh < w ? bh : w);
 }
 __host__ __device__ inline size_t tail_offset(int64_t bh, int n_xcd) { return (sched_ints(bh, n_xcd) + 63) / 64 * 64; }
+// Head-interleaved queue order (the alternative to heads in order): after the tail table, 64 queue
+// offsets, then one entry h * m + slot per task, each queue's tasks round-robin over the heads.
+__host__ __device__ inline size_t ilv_offset(int64_t bh, int m, int n_xcd) {
+  return (tail_offset(bh, n_xcd) + (size_t)n_xcd * tail_heads(bh, m) * (m > 0 ? m : 0) + 63) / 64 * 64;
+}
 __host__ __device__ inline size_t sched_state_ints(int64_t bh, int m, int n_xcd) {
-  return tail_offset(bh, n_xcd) + (size_t)n_xcd * tail_heads(bh, m) * (m > 0 ? m : 0);
+  return ilv_offset(bh, m, n_xcd) + 64 + (size_t)(bh > 0 ? bh : 0) * (m > 0 ? m : 0);
 }
 
 }  // namespace wa
@@ -51,8 +56,9 @@ __host__ __device__ inline size_t sched_state_ints(int64_t bh, int m, int n_xcd)
 struct WaAttnLaunch {
   const void* q;
   const void* k;
-  const void* v;
-  void* vt;          // workspace: V transposed to [bh][head_dim][mb*block], zero-padded
+  const void* v;     // null when the caller passes V already transposed (vt)
+  void* vt;          // V transposed to [bh][head_dim][mb*block], zero-padded: the caller's, or the
+                     // workspace copy that the launch writes from v
   int32_t* sched;    // workspace: sched_state_ints(bh, mb, n_xcd) int32 (counters at [0, n_xcd), prefix
                      // tables at 64, the tail order table at tail_offset(bh, n_xcd))
   const int32_t* row_ptr;
@@ -67,10 +73,14 @@ struct WaAttnLaunch {
   int32_t head_dim;
   int32_t block;
   int32_t n_xcd;
-  float scale;       // softmax scale
+  int32_t head_order;  // 0 heads in order within each queue, 1 round-robin over the heads
+  int32_t* status;     // device word, nullable: bit 0 an invalid perm entry, bit 1 an invalid KV index
+  float scale;         // softmax scale
 };
 
 hipError_t wa_launch_attention(const WaAttnLaunch& a, hipStream_t stream);
+hipError_t wa_launch_transpose_v(const void* v, void* vt, int64_t bh, int seq_len, int mb, int head_dim, int block,
+                                 hipStream_t stream);
 hipError_t wa_attention_occupancy(int head_dim, int block, int* wgs_per_cu);
 size_t wa_vt_bytes(int64_t bh, int mb, int head_dim, int block);
 

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_version_and_strings():
     lib = _lib()
-    assert lib.wa_abi_version() == 1
+    assert lib.wa_abi_version() == 2
     for code in (0, -1, -2, -3, -4, -6):
         assert lib.wa_status_string(code)
     p = L.WaSkipProfile()
@@ -94,7 +94,7 @@ def test_sparse_attn_validation():
         a = dict(args)
         a.update(kw)
         return lib.wa_sparse_attn(a["q"], a["k"], a["v"], a["mask"], a["perm"], None, ctypes.byref(s), 0.0,
-                                  a["n_xcd"], a["o"], None, a["ws"], a["ws_bytes"], None)
+                                  a["n_xcd"], a["o"], None, a.get("status"), a["ws"], a["ws_bytes"], None)
 
     assert call(q=None) == L.WA_ERR_INVALID_ARG
     assert call(o=None) == L.WA_ERR_INVALID_ARG
@@ -106,10 +106,44 @@ def test_sparse_attn_validation():
     assert call(ws=ctypes.c_void_p((1 << 24) + 64)) == L.WA_ERR_ALIGNMENT
     assert call(ws_bytes=ws_n.value - 1) == L.WA_ERR_WORKSPACE
     assert b"workspace" in lib.wa_last_error()
+    assert call(status=ctypes.c_void_p((1 << 20) + 2)) == L.WA_ERR_ALIGNMENT
     assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, None, FAKE, None, None, ctypes.byref(s), 0.0, 8, FAKE, None,
-                                  ctypes.c_void_p(1 << 24), ws_n.value, None) == L.WA_ERR_INVALID_ARG
+                                  None, ctypes.c_void_p(1 << 24), ws_n.value, None) == L.WA_ERR_INVALID_ARG
     assert lib.wa_sparse_attn_csr(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, ctypes.byref(s), 0.0, 8, FAKE, None,
-                                  ctypes.c_void_p(1 << 24), 256, None) == L.WA_ERR_WORKSPACE
+                                  None, ctypes.c_void_p(1 << 24), 256, None) == L.WA_ERR_WORKSPACE
+
+
+def test_sparse_attn_vt_validation():
+    lib = _lib()
+    s = _shape()
+    n_full, n_vt = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.wa_attn_workspace_size(ctypes.byref(s), ctypes.byref(n_full)) == 0
+    assert lib.wa_attn_vt_workspace_size(ctypes.byref(s), ctypes.byref(n_vt)) == 0
+    # the V^T copy is not part of this call's workspace: at least B*H*d*M_B*block*2 bytes smaller
+    assert n_vt.value + 1 * 2 * 64 * 64 * 64 * 2 <= n_full.value
+    assert n_vt.value % 256 == 0 and n_vt.value >= 4 * (64 + 64 * 3 + 2 * 64)
+    opts = L.WaAttnOptions(0.0, 8, L.WA_HEADS_IN_ORDER)
+    ws = ctypes.c_void_p(1 << 24)
+
+    def call(o=None, **kw):
+        a = dict(q=FAKE, k=FAKE, vt=FAKE, rp=FAKE, ci=FAKE, out=FAKE, status=None, ws=ws, ws_bytes=n_vt.value)
+        a.update(kw)
+        return lib.wa_sparse_attn_vt(a["q"], a["k"], a["vt"], a["rp"], a["ci"], None, None, ctypes.byref(s),
+                                     ctypes.byref(o) if o is not None else None, a["out"], None, a["status"], a["ws"],
+                                     a["ws_bytes"], None)
+
+    assert call(None) == L.WA_ERR_INVALID_ARG
+    assert call(opts, vt=None) == L.WA_ERR_INVALID_ARG
+    assert call(opts, rp=None) == L.WA_ERR_INVALID_ARG
+    assert call(opts, vt=ctypes.c_void_p((1 << 20) + 4)) == L.WA_ERR_ALIGNMENT
+    assert call(opts, status=ctypes.c_void_p((1 << 20) + 1)) == L.WA_ERR_ALIGNMENT
+    assert call(L.WaAttnOptions(0.0, 0, 0)) == L.WA_ERR_INVALID_ARG
+    assert call(L.WaAttnOptions(0.0, 8, 2)) == L.WA_ERR_INVALID_ARG
+    assert b"head_order" in lib.wa_last_error()
+    assert call(opts, ws_bytes=n_vt.value - 1) == L.WA_ERR_WORKSPACE
+    assert lib.wa_transpose_v(None, ctypes.byref(s), FAKE, None) == L.WA_ERR_INVALID_ARG
+    assert lib.wa_transpose_v(FAKE, ctypes.byref(s), ctypes.c_void_p((1 << 20) + 2), None) == L.WA_ERR_ALIGNMENT
+    assert lib.wa_transpose_v(FAKE, ctypes.byref(_shape(head_dim=96)), FAKE, None) == L.WA_ERR_UNSUPPORTED
 
 
 def test_produce_block_mask_validation():
@@ -197,3 +231,105 @@ def test_product_path_fails_loudly_without_library(tmp_path):
             L.load(str(tmp_path / "missing.so"))
         finally:
             L._LIB = L._LIB_SAVED
+
+
+# ------------------------------------------------------------------------------------------------
+# the Python binding rejects mismatched shapes and dtypes before any device work (CPU tensors here:
+# the shape checks come before the placement check)
+# ------------------------------------------------------------------------------------------------
+def _cpu_args(b=1, h=2, n=300, d=64, blk=64):
+    import torch
+    mb = -(-n // blk)
+    q = torch.zeros((b, h, n, d), dtype=torch.bfloat16)
+    return dict(q=q, k=q.clone(), v=q.clone(), mask=torch.zeros((b, h, mb, mb), dtype=torch.uint8),
+                perm=torch.zeros((b, h, mb), dtype=torch.int32), seg=torch.zeros((b, h, 9), dtype=torch.int32),
+                rp=torch.zeros((b, h, mb + 1), dtype=torch.int32), ci=torch.zeros(b * h * mb * mb, dtype=torch.int32),
+                vt=torch.zeros((b, h, d, mb * blk), dtype=torch.bfloat16), mb=mb, blk=blk, n=n, d=d)
+
+
+@pytest.mark.parametrize("case,match", [
+    ("mask_shape", "mask must have shape"),
+    ("mask_dtype", "mask must be uint8"),
+    ("perm_shape", "perm must have shape"),
+    ("perm_dtype", "perm must be torch.int32"),
+    ("seg_for_other_n_xcd", "seg must have shape"),
+    ("n_xcd", "n_xcd"),
+    ("out_shape", "out must have shape"),
+    ("status_dtype", "status must be torch.int32"),
+    ("not_on_device", "must be a device tensor"),
+])
+def test_binding_rejects_bad_sparse_attn_arguments(case, match):
+    import torch
+    _lib()
+    import paper_2609_34814_amd as W
+    a = _cpu_args()
+    kw = dict(block=a["blk"], n_xcd=8)
+    mask, perm, seg = a["mask"], a["perm"], a["seg"]
+    if case == "mask_shape":
+        mask = torch.zeros((1, 2, a["mb"], a["mb"] + 1), dtype=torch.uint8)
+    elif case == "mask_dtype":
+        mask = mask.to(torch.int32)
+    elif case == "perm_shape":
+        perm = torch.zeros((1, 2, a["mb"] + 1), dtype=torch.int32)
+    elif case == "perm_dtype":
+        perm = perm.to(torch.int64)
+    elif case == "seg_for_other_n_xcd":
+        seg = torch.zeros((1, 2, 2), dtype=torch.int32)    # built with n_xcd = 1, passed with 8
+    elif case == "n_xcd":
+        kw["n_xcd"] = 65
+    elif case == "out_shape":
+        kw["out"] = torch.zeros((1, 2, a["n"] - 1, a["d"]), dtype=torch.bfloat16)
+    elif case == "status_dtype":
+        kw["status"] = torch.zeros(1, dtype=torch.int64)
+    with pytest.raises(ValueError, match=match):
+        W.sparse_attn(a["q"], a["k"], a["v"], mask, perm, seg, **kw)
+
+
+@pytest.mark.parametrize("case,match", [
+    ("row_ptr_shape", "row_ptr must have shape"),
+    ("row_ptr_dtype", "row_ptr must be torch.int32"),
+    ("col_idx_small", "col_idx must hold at least"),
+    ("vt_shape", "vt must have shape"),
+    ("head_order", "head_order"),
+])
+def test_binding_rejects_bad_list_and_vt_arguments(case, match):
+    import torch
+    _lib()
+    import paper_2609_34814_amd as W
+    a = _cpu_args()
+    rp, ci, vt = a["rp"], a["ci"], a["vt"]
+    kw = dict(block=a["blk"], n_xcd=8)
+    if case == "row_ptr_shape":
+        rp = torch.zeros((1, 2, a["mb"]), dtype=torch.int32)
+    elif case == "row_ptr_dtype":
+        rp = rp.to(torch.int64)
+    elif case == "col_idx_small":
+        ci = ci[:-1]
+    elif case == "vt_shape":
+        vt = torch.zeros((1, 2, a["d"], a["n"]), dtype=torch.bfloat16)   # not padded to whole blocks
+    elif case == "head_order":
+        kw["head_order"] = "by-xcd"
+    with pytest.raises(ValueError, match=match):
+        if case in ("vt_shape", "head_order"):
+            W.sparse_attn_vt(a["q"], a["k"], vt, rp, ci, **kw)
+        else:
+            W.sparse_attn_csr(a["q"], a["k"], a["v"], rp, ci, **kw)
+    if case in ("row_ptr_shape", "row_ptr_dtype", "col_idx_small"):
+        with pytest.raises(ValueError, match=match):
+            W.sparse_attn_vt(a["q"], a["k"], a["vt"], rp, ci, **kw)
+
+
+def test_binding_rejects_bad_permutation_outputs():
+    import torch
+    _lib()
+    import paper_2609_34814_amd as W
+    a = _cpu_args()
+    with pytest.raises(ValueError, match="seg_out must have shape"):
+        W.build_permutation(a["mask"], seq_len=a["n"], block=a["blk"], head_dim=a["d"], n_xcd=1,
+                            seg_out=torch.zeros((1, 2, 9), dtype=torch.int32))
+    with pytest.raises(ValueError, match="mask must have shape"):
+        W.build_permutation(a["mask"], seq_len=a["n"] + a["blk"], block=a["blk"], head_dim=a["d"])
+    with pytest.raises(ValueError, match="skip must be one of"):
+        W.build_permutation(a["mask"], seq_len=a["n"], block=a["blk"], head_dim=a["d"], skip="sometimes")
+    with pytest.raises(ValueError, match="row_ptr must have shape"):
+        W.compact_mask(a["mask"], seq_len=a["n"], block=a["blk"], row_ptr=torch.zeros(3, dtype=torch.int32))

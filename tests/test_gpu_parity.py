@@ -171,6 +171,15 @@ def test_permutation_bit_exact_full_size(name, mode, profile):
     _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=mode, profile=profile)
 
 
+@pytest.mark.parametrize("name,mode", [("long-720p-401f", S.SKIP_NEVER), ("long-720p-401f", S.SKIP_AUTO),
+                                       ("wan14b-720p-81f", S.SKIP_AUTO)])
+def test_permutation_bit_exact_bench_layout(name, mode):
+    """The permutation the benchmark times: one segment (n_xcd = 1), chip-wide waves of
+    W = 8 x wa_wave_size rows, the built-in skip profile (auto) or none (never)."""
+    wl = CONFIGS[name]
+    _perm_case(wl, make_mask(wl, threads=16), wave=_w().wave_size(wl.head_dim, wl.block) * 8, n_xcd=1, mode=mode)
+
+
 @pytest.mark.parametrize("n_xcd,wave,seed", [(1, 132, 5), (2, 7, 99), (8, 1, 3)])
 def test_permutation_bit_exact_params(n_xcd, wave, seed):
     wl = CONFIGS["wan1.3b-480p-81f"]
@@ -316,6 +325,160 @@ def test_output_bit_identical_across_permutations(name):
         assert torch.equal(l2.view(torch.int32), l_nat.view(torch.int32))
 
 
+@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64"])
+def test_transpose_v_layout(name):
+    """wa_transpose_v writes vt[b][h][c][t] = V[b][h][t][c] for t < N and zeros up to M_B*block."""
+    wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
+    _, _, v = make_qkv(wl)
+    vt = _w().transpose_v(bf16_dev(v), block=wl.block)
+    torch.cuda.synchronize()
+    got = vt.view(torch.int16).cpu().numpy().view(np.uint16)
+    want = np.zeros((wl.batch, wl.heads, wl.head_dim, wl.mb * wl.block), dtype=np.uint16)
+    want[..., :wl.seq_len] = np.swapaxes(v, 2, 3)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64"])
+def test_vt_entry_and_head_orders_bit_identical(name):
+    """V given transposed, heads in order or interleaved, one or eight queues, with and without a
+    segment table: O and LSE bit-identical to the natural-order call, status word 0."""
+    wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
+    W_ = _w()
+    q, k, v = (bf16_dev(x) for x in make_qkv(wl))
+    mask = make_mask(wl)
+    md = u8_dev(mask)
+    o_nat, l_nat = _run_attn(wl, mask, q, k, v, perm=None, n_xcd=8)
+    vt = W_.transpose_v(v, block=wl.block)
+    rp, ci = W_.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
+    rng = np.random.default_rng(5)
+    rnd = np.stack([np.stack([rng.permutation(wl.mb) for _ in range(wl.heads)]) for _ in range(wl.batch)])
+    rnd = torch.from_numpy(rnd.astype(np.int32)).cuda()
+    lop = np.zeros((wl.batch, wl.heads, 9), dtype=np.int32)
+    lop[:, :, 1:] = wl.mb
+    lop[:, :, 1] = max(wl.mb - 2, 0)
+    lop = torch.from_numpy(lop).cuda()
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    for order in ("in-order", "interleaved"):
+        for n_xcd in (1, 8):
+            perm, seg, _ = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
+                                                n_xcd=n_xcd, skip="never")
+            for p, sg in ((None, None), (perm, seg), (rnd, None)) + (((rnd, lop),) if n_xcd == 8 else ()):
+                status.fill_(-1)
+                o2, l2 = W_.sparse_attn_vt(q, k, vt, rp, ci, p, sg, block=wl.block, n_xcd=n_xcd, head_order=order,
+                                           return_lse=True, status=status)
+                torch.cuda.synchronize()
+                assert int(status.item()) == 0
+                assert torch.equal(o2.view(torch.int16), o_nat.view(torch.int16)), (order, n_xcd)
+                assert torch.equal(l2.view(torch.int32), l_nat.view(torch.int32)), (order, n_xcd)
+
+
+def _expected_interleaved(x, bh, mb, n_xcd, seg):
+    """Queue x's tasks round-robin over the heads: slot s0 + r of every head whose segment is longer
+    than r, for r = 0, 1, ...; entries h * mb + slot."""
+    def segment(h):
+        if seg is None:
+            base, extra = divmod(mb, n_xcd)
+            s0 = x * base + min(x, extra)
+            return s0, s0 + base + (1 if x < extra else 0)
+        s0 = min(max(int(seg[h][x]), 0), mb)
+        return s0, min(max(int(seg[h][x + 1]), s0), mb)
+    segs = [segment(h) for h in range(bh)]
+    out = []
+    for r in range(mb):
+        out += [h * mb + s0 + r for h, (s0, s1) in enumerate(segs) if r < s1 - s0]
+    return out
+
+
+@pytest.mark.parametrize("name,n_xcd,reorder", [("tiny", 1, False), ("wan14b-720p-81f", 8, True),
+                                                 ("skip-d64", 8, False), ("wan1.3b-480p-81f", 3, True)])
+def test_interleaved_order_table(name, n_xcd, reorder):
+    """The head-interleaved order the call builds equals the round-robin rule computed here, queue by
+    queue, and the queue offsets partition the table."""
+    W_ = _w()
+    wl = CONFIGS[name]
+    mask = make_mask(wl, threads=16)
+    q, k, v = make_qkv(wl, threads=16)
+    md = u8_dev(mask)
+    bh, mb = wl.batch * wl.heads, wl.mb
+    rp, ci = W_.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
+    perm = seg = None
+    if reorder:
+        perm, seg, _ = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim, wave=64,
+                                            n_xcd=n_xcd, skip="never")
+    shape = W_.shape_of(wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block)
+    ws = torch.empty(W_.attn_vt_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    qd, kd = bf16_dev(q), bf16_dev(k)
+    vt = W_.transpose_v(bf16_dev(v), block=wl.block)
+    o = torch.full_like(qd, float("nan"))
+    W_.sparse_attn_vt(qd, kd, vt, rp, ci, perm, seg, block=wl.block, n_xcd=n_xcd, head_order="interleaved", out=o,
+                      workspace=ws)
+    torch.cuda.synchronize()
+    assert not bool(torch.isnan(o.float()).any().item())
+    sched = ws.view(torch.int32).cpu().numpy()
+    th = min(bh, 16384 // mb, 256)
+    tail_off = (64 + n_xcd * (bh + 1) + 63) // 64 * 64
+    ilv = (tail_off + n_xcd * th * mb + 63) // 64 * 64
+    seg_h = seg.cpu().numpy().reshape(bh, n_xcd + 1) if seg is not None else None
+    off = 0
+    for x in range(n_xcd):
+        want = _expected_interleaved(x, bh, mb, n_xcd, seg_h)
+        assert sched[ilv + x] == off, (name, x)
+        got = sched[ilv + 64 + off: ilv + 64 + off + len(want)]
+        assert np.array_equal(got, np.asarray(want, dtype=np.int32)), (name, x)
+        off += len(want)
+    assert off == bh * mb
+
+
+def test_status_word_reports_invalid_entries():
+    """An out-of-range perm entry computes nothing (the row it should have named keeps its old
+    contents) and sets bit 0; an out-of-range KV index in caller-built lists is read as block 0 and
+    sets bit 1; everything else is computed as usual. Both are forced from the host and stay in
+    bounds on the device."""
+    W_ = _w()
+    wl = {w.name: w for w in SMALL}["ragged"]
+    q, k, v = (bf16_dev(x) for x in make_qkv(wl))
+    mask = make_mask(wl)
+    md = u8_dev(mask)
+    o_nat, _ = _run_attn(wl, mask, q, k, v, perm=None, n_xcd=8)
+    rp, ci = W_.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
+    vt = W_.transpose_v(v, block=wl.block)
+    perm = torch.arange(wl.mb, dtype=torch.int32, device="cuda").repeat(wl.batch, wl.heads, 1).contiguous()
+    perm[0, 1, 3] = wl.mb            # slot 3 of head 1 names no block: row 3 is not computed
+    perm[0, 0, 5] = -7               # slot 5 of head 0 likewise
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    for call in ("csr", "vt", "mask"):
+        o = torch.full_like(q, float("nan"))
+        status.fill_(-1)
+        if call == "csr":
+            W_.sparse_attn_csr(q, k, v, rp, ci, perm, block=wl.block, n_xcd=1, out=o, status=status)
+        elif call == "vt":
+            W_.sparse_attn_vt(q, k, vt, rp, ci, perm, block=wl.block, n_xcd=8, out=o, status=status)
+        else:
+            W_.sparse_attn(q, k, v, md, perm, block=wl.block, n_xcd=8, out=o, status=status)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 1, call
+        lo1, hi1 = A.block_token_range(3, wl.block, wl.seq_len)
+        lo0, hi0 = A.block_token_range(5, wl.block, wl.seq_len)
+        assert bool(torch.isnan(o[0, 1, lo1:hi1].float()).all()) and bool(torch.isnan(o[0, 0, lo0:hi0].float()).all())
+        keep = torch.ones(wl.seq_len, dtype=torch.bool, device="cuda")
+        for (h, lo, hi) in ((1, lo1, hi1), (0, lo0, hi0)):
+            kk = keep.clone()
+            kk[lo:hi] = False
+            assert torch.equal(o[0, h][kk].view(torch.int16), o_nat[0, h][kk].view(torch.int16))
+        assert torch.equal(o[0, 2:].view(torch.int16), o_nat[0, 2:].view(torch.int16))
+    # an invalid KV index: the last entry of row 0 of head 0 points past N_B
+    bad = ci.clone()
+    bad[int(rp[0, 0, 1].item()) - 1] = wl.mb + 3
+    status.fill_(-1)
+    W_.sparse_attn_vt(q, k, vt, rp, bad, block=wl.block, n_xcd=8, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 2
+    status.fill_(-1)
+    W_.sparse_attn_vt(q, k, vt, rp, ci, block=wl.block, n_xcd=8, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+
+
 def test_repeated_runs_identical():
     wl = CONFIGS["wan1.3b-480p-81f"]
     q, k, v = (bf16_dev(x) for x in make_qkv(wl))
@@ -409,11 +572,12 @@ class _DeviceRows:
         return self.o[b, h, rows].float().cpu().numpy().astype(np.float64)
 
 
-def _bench_launch(wl, md, qd, kd, vd, perm_kind, with_perm=False):
-    """The path as the benchmark times it: CSR lists from compact_mask and one queue (n_xcd = 1);
-    perm_kind "reordered" uses the two-stage order over chip-wide waves on every head, "auto" the
-    same with the skip rule deciding per head, "natural" none. With with_perm, the permutation and
-    the head flags are returned too."""
+def _bench_launch(wl, md, qd, kd, vtd, perm_kind, with_perm=False, head_order="in-order"):
+    """The path as the benchmark times it: CSR lists from compact_mask, V given transposed (vtd, from
+    transpose_v), one queue (n_xcd = 1), heads in order; perm_kind "reordered" uses the two-stage
+    order over chip-wide waves on every head, "auto" the same with the skip rule deciding per head,
+    "natural" none. With with_perm, the permutation and the head flags are returned too. The status
+    word must stay 0."""
     W_ = _w()
     perm = seg = flags = None
     if perm_kind in ("reordered", "auto"):
@@ -421,15 +585,19 @@ def _bench_launch(wl, md, qd, kd, vd, perm_kind, with_perm=False):
         perm, seg, flags = W_.build_permutation(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim,
                                                 wave=wave, n_xcd=1, skip="never" if perm_kind == "reordered" else "auto")
     rp, ci = W_.compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
-    o, lse = W_.sparse_attn_csr(qd, kd, vd, rp, ci, perm, seg, block=wl.block, n_xcd=1, return_lse=True)
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    o, lse = W_.sparse_attn_vt(qd, kd, vtd, rp, ci, perm, seg, block=wl.block, n_xcd=1, head_order=head_order,
+                               return_lse=True, status=status)
     torch.cuda.synchronize()
+    assert int(status.item()) == 0
     if with_perm:
         return o, lse, perm, flags
     return o, lse
 
 
 def _few_blocks(mask, heads, extra, seed):
-    """First, last (ragged), heaviest and lightest rows of the given heads plus seeded random rows."""
+    """First, last (ragged), heaviest and lightest rows of the given heads plus `extra` seeded random
+    rows."""
     b_, h_, mb, _ = mask.shape
     n = mask.sum(-1)
     picks = set()
@@ -450,13 +618,23 @@ def test_attention_bench_launch_full_size(name):
     mask = make_mask(wl, threads=16)
     qd, kd, vd = bf16_dev(q), bf16_dev(k), bf16_dev(v)
     md = u8_dev(mask)
-    o, lse = _bench_launch(wl, md, qd, kd, vd, "reordered")
-    o_nat, lse_nat = _bench_launch(wl, md, qd, kd, vd, "natural")
+    vtd = _w().transpose_v(vd, block=wl.block)
+    o, lse = _bench_launch(wl, md, qd, kd, vtd, "reordered")
+    o_nat, lse_nat = _bench_launch(wl, md, qd, kd, vtd, "natural")
     assert torch.equal(o.view(torch.int16), o_nat.view(torch.int16))
     assert torch.equal(lse.view(torch.int32), lse_nat.view(torch.int32))
+    # V in its natural layout (transposed inside the call) and heads interleaved: the same O
+    rp, ci = _w().compact_mask(md, seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
+    o2 = _w().sparse_attn_csr(qd, kd, vd, rp, ci, block=wl.block, n_xcd=1)
+    torch.cuda.synchronize()
+    assert torch.equal(o2.view(torch.int16), o_nat.view(torch.int16))
+    del o2, rp, ci, vd
+    o2, _ = _bench_launch(wl, md, qd, kd, vtd, "natural", head_order="interleaved")
+    assert torch.equal(o2.view(torch.int16), o_nat.view(torch.int16))
+    del o2
     # the skip rule's launch: its tier-1 decision per head equals the oracle's on the same statistics,
     # a skipped head keeps the identity order, and O / LSE are again bit-identical
-    o_auto, lse_auto, perm_auto, flags_auto = _bench_launch(wl, md, qd, kd, vd, "auto", with_perm=True)
+    o_auto, lse_auto, perm_auto, flags_auto = _bench_launch(wl, md, qd, kd, vtd, "auto", with_perm=True)
     assert torch.equal(o_auto.view(torch.int16), o_nat.view(torch.int16))
     assert torch.equal(lse_auto.view(torch.int32), lse_nat.view(torch.int32))
     flags_auto, perm_auto = flags_auto.cpu().numpy(), perm_auto.cpu().numpy()
@@ -470,7 +648,9 @@ def test_attention_bench_launch_full_size(name):
         else:  # case 3 may still fire against the built order
             assert got & (S.FLAG_FITS_CACHE | S.FLAG_LITTLE_WORK) == 0, h
     del o_nat, lse_nat, o_auto, lse_auto
-    picks = _few_blocks(mask, (0, wl.heads // 2, wl.heads - 1), 12, seed=4)
+    # every head: its first, ragged last, heaviest and lightest rows, plus random rows up to 256 blocks
+    picks = _few_blocks(mask, range(wl.heads), max(16, 256 - 4 * wl.heads), seed=4)
+    assert len(picks) >= 256
     ref = A.block_sparse_attention_rows(q, k, v, mask, wl.block, picks)
     st = compare_blocks(_DeviceRows(o), ref, wl.block, wl.seq_len, lse.cpu().numpy().astype(np.float64))
     print(wl.name, st)
@@ -503,7 +683,7 @@ def test_max_blocks_attention():
     mask = make_mask(wl)
     qd, kd, vd = bf16_dev(q), bf16_dev(k), bf16_dev(v)
     md = u8_dev(mask)
-    o, lse = _bench_launch(wl, md, qd, kd, vd, "reordered")
+    o, lse = _bench_launch(wl, md, qd, kd, _w().transpose_v(vd, block=wl.block), "reordered")
     o_nat, lse_nat = _run_attn(wl, mask, qd, kd, vd, perm=None, n_xcd=8)
     assert torch.equal(o.view(torch.int16), o_nat.view(torch.int16))
     assert torch.equal(lse.view(torch.int32), lse_nat.view(torch.int32))
