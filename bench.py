@@ -70,105 +70,168 @@ def load_counters(workload: str, variant: str):
     if not entry or entry.get("kernel_sha") != kernel_source_hash() or entry.get("variant_spec") != VARIANTS[variant]:
         return None
     return {"l2_hit": entry.get("l2_hit"), "l2_fabric_read_bytes": entry.get("fetch_bytes"),
-            "mfma_busy": entry.get("mfma_busy"), "clock_ghz": entry.get("clock_ghz"),
-            "source": "profiles/attn_traffic.json"}
+            "dram_addressed_read_bytes": entry.get("dram_read_bytes"), "mfma_busy": entry.get("mfma_busy"),
+            "clock_ghz": entry.get("clock_ghz"), "source": "profiles/attn_traffic.json"}
 
 
-def _pmc_means(csv_path: str, kernel_substr: str):
-    """Mean of every counter over the matching dispatches (and the mean dispatch duration in ns)."""
+def _pmc_dispatches(csv_path: str, kernel_substr: str):
+    """Counters of every matching dispatch, in launch order: [(name, duration ns, {counter: value})]."""
     import csv
-    vals = {}
-    durs = {}
+    rows = {}
     with open(csv_path) as f:
         for r in csv.DictReader(f):
-            if kernel_substr in r["Kernel_Name"]:
-                vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
-                durs[r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
-    out = {k: sum(v) / len(v) for k, v in vals.items()}
-    if durs:
-        out["duration_ns"] = sum(durs.values()) / len(durs)
-    return out, max((len(v) for v in vals.values()), default=0)
+            if kernel_substr not in r["Kernel_Name"]:
+                continue
+            d = rows.setdefault(int(r["Dispatch_Id"]), [r["Kernel_Name"],
+                                                       int(r["End_Timestamp"]) - int(r["Start_Timestamp"]), {}])
+            d[2][r["Counter_Name"]] = d[2].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return [tuple(rows[k]) for k in sorted(rows)]
 
 
+def _mean_counters(disp):
+    out = {}
+    for _, _, c in disp:
+        for k, v in c.items():
+            out[k] = out.get(k, 0.0) + v / len(disp)
+    out["duration_ns"] = sum(d for _, d, _ in disp) / len(disp)
+    return out
+
+
+# rocprofv3 --pmc passes (one run each; every pass stays within one run's counter limits: at most
+# 4 TCC, 8 SQ, 4 TCP, 2 GRBM counters)
 PMC_PASSES = {
     "A": "TCC_HIT_sum TCC_MISS_sum SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE",
     "B": "FETCH_SIZE",
-    "C": "WRITE_SIZE TCC_EA0_RDREQ_DRAM_sum",
+    "C": "WRITE_SIZE",
     "D": "TCP_TCC_READ_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_LEVEL_sum",
+    "E": "TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_32B_sum TCC_BUBBLE_sum TCC_EA0_RDREQ_DRAM_sum",
 }
 
 
-def summarize_pmc(root: str, workload: str, out_json: str, out_md: str, command_note: str) -> None:
-    """Turn rocprofv3 --pmc CSV passes into the traffic figure and a text summary.
+def _read_bytes_e(c):
+    """L2 read bytes to the fabric from pass E (128-, 64- and 32-byte requests), and the share of them
+    addressed to DRAM: on MI355X those go through the 256 MiB last-level cache on the way, and no
+    counter of this pool tells its hits from HBM reads."""
+    rd, r32, bub, dram = (c["TCC_EA0_RDREQ_sum"], c["TCC_EA0_RDREQ_32B_sum"], c["TCC_BUBBLE_sum"],
+                          c["TCC_EA0_RDREQ_DRAM_sum"])
+    total = bub * 128.0 + (rd - bub - r32) * 64.0 + r32 * 32.0
+    return total, (dram / rd if rd else 0.0)
 
-    Expects <root>/<variant>_{A,B,C,D}/run_counter_collection.csv for the attention kernel (the
-    counters of PMC_PASSES; pass D is optional) and copy_{B,C} for a plain 1 GiB device copy, whose
-    FETCH_SIZE / WRITE_SIZE give the byte-scaling factors.
-    """
-    cb, _ = _pmc_means(os.path.join(root, "copy_B", "run_counter_collection.csv"), "copyBuffer")
-    cc, _ = _pmc_means(os.path.join(root, "copy_C", "run_counter_collection.csv"), "copyBuffer")
+
+def summarize_pmc(root: str, workload: str, variants, warmup: int, steps: int, bench_json: str, out_json: str,
+                  out_md: str, command_note: str) -> None:
+    """Counter tables of one workload from rocprofv3 --pmc passes of ONE bench.py run per pass.
+
+    <root>/<pass>/run_counter_collection.csv holds the attention kernel's dispatches of
+    `bench.py --variants v1,v2,... --warmup W --steps K` in launch order: variant i owns dispatches
+    [i (W+K), (i+1)(W+K)), of which the last K are averaged. <root>/copy_{B,C,E} hold a plain 1 GiB
+    device copy, whose FETCH_SIZE, WRITE_SIZE and pass-E read bytes give the byte-scaling factors.
+    bench_json is the line of an unprofiled run of the same variants (flushed median call times,
+    effective TFLOP/s, order statistics)."""
+    def copy_pass(p):
+        d = _pmc_dispatches(os.path.join(root, "copy_" + p, "run_counter_collection.csv"), "")
+        big = [x for x in d if "opy" in x[0] or "elementwise" in x[0]]
+        return _mean_counters(big or d)
+
     copy_bytes = float(1 << 30)
-    f_fetch = copy_bytes / (cb["FETCH_SIZE"] * 1024.0)
-    f_write = copy_bytes / (cc["WRITE_SIZE"] * 1024.0)
+    f_fetch = copy_bytes / (copy_pass("B")["FETCH_SIZE"] * 1024.0)
+    f_write = copy_bytes / (copy_pass("C")["WRITE_SIZE"] * 1024.0)
+    f_e = copy_bytes / _read_bytes_e(copy_pass("E"))[0]
+    with open(bench_json) as f:
+        line = json.loads([ln for ln in f.read().splitlines() if ln.startswith("{")][-1])
+    per = warmup + steps
+    passes = {}
+    for p in PMC_PASSES:
+        path = os.path.join(root, p, "run_counter_collection.csv")
+        if not os.path.exists(path):
+            continue
+        disp = _pmc_dispatches(path, "attn_fwd_kernel")
+        if len(disp) != per * len(variants):
+            raise RuntimeError(f"pass {p}: {len(disp)} attention dispatches, expected {per * len(variants)}")
+        passes[p] = {v: _mean_counters(disp[i * per + warmup:(i + 1) * per]) for i, v in enumerate(variants)}
     sha = kernel_source_hash()
     try:
         with open(out_json) as f:
             data = json.load(f)
     except (OSError, ValueError):
         data = {}
-    run = ("cd /tmp && export TMPDIR=/tmp && cd $GRAFT_REPO_ROOT && timeout -s KILL 240 rocprofv3 --pmc {ctr} "
-           "--kernel-include-regex {kre} --output-format csv -d {root}/{{variant}}_{p} -o run -- {cmd}")
-    bench_cmd = (f"python bench.py --config {workload} --steps 2 --warmup 1 --no-cpu-baseline "
-                 "--variants {variant}")
-    passes = [("A", PMC_PASSES["A"], "attn_fwd", bench_cmd), ("B", PMC_PASSES["B"], "attn_fwd", bench_cmd),
-              ("C", PMC_PASSES["C"], "attn_fwd", bench_cmd), ("D", PMC_PASSES["D"], "attn_fwd", bench_cmd),
-              ("copy B", PMC_PASSES["B"], "'copyBuffer|elementwise|copy'", "python bench.py --copy-calibration 1024"),
-              ("copy C", PMC_PASSES["C"].split()[0], "'copyBuffer|elementwise|copy'",
-               "python bench.py --copy-calibration 1024")]
-    lines = [f"# attention kernel counters, workload {workload}", "", "Commands (one rocprofv3 run per pass; "
-             "{variant} is the row of the table, the copy passes write to copy_B and copy_C):", ""]
-    for p, ctr, kre, cmd in passes:
-        lines.append(f"* pass {p}: `" + run.format(ctr=ctr, kre=kre, root=root, p=p.split()[-1], cmd=cmd)
-                     .replace("{variant}_B", "copy_B" if p == "copy B" else "{variant}_B")
-                     .replace("{variant}_C", "copy_C" if p == "copy C" else "{variant}_C") + "`")
+    entry = data.setdefault(workload, {})
+    alg = line["algorithmic_bytes"]
+    kv_global = alg["kv_compulsory"]
+    xcd = alg.get("kv_compulsory_per_xcd", {})
+    ost = line.get("order_stats", {})
+    cfg = line["config"]
+    lines = [f"# attention kernel counters, workload {workload}", "",
+             f"{cfg['heads']} heads x {cfg['seq_len']} tokens, d {cfg['head_dim']}, {cfg['block']}-token blocks, "
+             f"density {100 * cfg['density']:.2f}% ({cfg['kept_blocks']} kept blocks, "
+             f"{cfg['flop_per_step']:.4g} FLOP per call); compulsory K/V {kv_global / 1e9:.3f} GB, Q+O "
+             f"{alg['q_and_o'] / 1e9:.3f} GB.", "",
+             "Commands (one rocprofv3 run per pass, each running the variants below in this order):", ""]
+    run = ("cd /tmp && export TMPDIR=/tmp && cd $GRAFT_REPO_ROOT && timeout -s KILL 300 rocprofv3 --pmc {ctr} "
+           "--kernel-include-regex {kre} --output-format csv -d {root}/{p} -o run -- {cmd}")
+    bench_cmd = (f"python bench.py --config {workload} --steps {steps} --warmup {warmup} --no-cpu-baseline "
+                 f"--no-gemm-reference --no-order-stats --variants {','.join(variants)}")
+    for p, ctr in PMC_PASSES.items():
+        lines.append(f"* pass {p}: `" + run.format(ctr=ctr, kre="attn_fwd", root=root, p=p, cmd=bench_cmd) + "`")
+    for p in ("B", "C", "E"):
+        lines.append(f"* copy pass {p}: `" + run.format(ctr=PMC_PASSES[p], kre="'copy|elementwise'", root=root,
+                                                      p="copy_" + p, cmd="python bench.py --copy-calibration 1024")
+                     + "`")
+    lines += [f"* timings and order statistics: `python bench.py --config {workload} --steps 10 --warmup 2 "
+              f"--no-cpu-baseline --no-gemm-reference --variants {','.join(variants)}`"]
     if command_note:
         lines += ["", f"Driver: {command_note}"]
     lines += ["",
-             "L2 hit % = TCC_HIT / (TCC_HIT + TCC_MISS). L2->fabric read bytes = FETCH_SIZE x the copy factor, "
-             "write bytes = WRITE_SIZE x its factor (both per launch). MFMA FLOP = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512. "
-             "MFMA busy % = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs), i.e. against the clock "
-             "the chip actually ran at; that clock = GRBM_GUI_ACTIVE / 8 XCDs / the dispatch's duration. "
-             "L2 latency = TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ (cycles per request from a CU); fabric "
-             "latency = TCC_EA0_RDREQ_LEVEL / TCC_EA0_RDREQ (cycles a read to the fabric is outstanding).", "",
-             f"Copy calibration (1 GiB device copy): FETCH_SIZE x {f_fetch:.3f}, WRITE_SIZE x {f_write:.3f}", "",
-             "| variant | dispatches | kernel ms | clock GHz | L2 hit % | L2->fabric read GB/launch (scaled) | "
-             "write GB/launch (scaled) | DRAM read req | MFMA FLOP (MOPS x 512) | MFMA busy % | L2 latency | "
-             "fabric latency |",
-             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
-    entry = data.setdefault(workload, {})
-    variants = sorted({d.rsplit("_", 1)[0] for d in os.listdir(root) if d.endswith("_A")})
+              "Columns. call ms / TFLOP/s: the unprofiled run, median over steps each started after a 1 GiB cache "
+              "flush; frac = TFLOP/s / 2500 (dense bf16 peak). kernel ms: the profiled dispatches. L2 hit % = "
+              "TCC_HIT / (TCC_HIT + TCC_MISS). fabric rd GB = FETCH_SIZE x copy factor: what the eight L2s read "
+              "from the fabric, i.e. from the 256 MiB last-level cache and HBM together. DRAM rd GB = pass E's "
+              "read bytes (128/64/32-byte requests) x copy factor x TCC_EA0_RDREQ_DRAM / TCC_EA0_RDREQ: the reads "
+              "addressed to DRAM, which still includes last-level-cache hits (this pool exposes no counter that "
+              "separates them, so true HBM read bytes cannot be measured here). K/V xcd GB: compulsory K/V if each "
+              "XCD fetches every block its own rows need once (per-XCD model, see bench.py). MFMA busy % = "
+              "SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8), against the clock the chip ran at "
+              "(= GRBM_GUI_ACTIVE / 8 / kernel time). J: adjacent-row overlap of the executed order; Eq. 1: the "
+              "paper's objective over chip-wide waves, relative to natural order (lower is better). L2 lat / "
+              "fabric lat: cycles per L2 request from a CU / per fabric read in flight.", "",
+              f"Copy calibration (1 GiB device copy): FETCH_SIZE x {f_fetch:.3f}, WRITE_SIZE x {f_write:.3f}, "
+              f"pass E x {f_e:.3f}.", "",
+              "| variant | call ms | TFLOP/s | frac | kernel ms | clock GHz | L2 hit % | fabric rd GB | DRAM rd GB | "
+              "K/V xcd GB | write GB | MFMA busy % | J | Eq. 1 | L2 lat | fabric lat |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    nan = float("nan")
     for v in variants:
-        a, na = _pmc_means(os.path.join(root, f"{v}_A", "run_counter_collection.csv"), "attn_fwd")
-        b, _ = _pmc_means(os.path.join(root, f"{v}_B", "run_counter_collection.csv"), "attn_fwd")
-        c, _ = _pmc_means(os.path.join(root, f"{v}_C", "run_counter_collection.csv"), "attn_fwd")
+        a, b, c = passes["A"][v], passes["B"][v], passes["C"][v]
+        e = passes.get("E", {}).get(v)
+        dd = passes.get("D", {}).get(v, {})
         hit = a["TCC_HIT_sum"] / (a["TCC_HIT_sum"] + a["TCC_MISS_sum"])
         fetch = b["FETCH_SIZE"] * 1024.0 * f_fetch
         write = c["WRITE_SIZE"] * 1024.0 * f_write
-        cycles = a["GRBM_GUI_ACTIVE"] / 8.0          # summed over the 8 XCDs
+        cycles = a["GRBM_GUI_ACTIVE"] / 8.0
         busy = a["SQ_VALU_MFMA_BUSY_CYCLES"] / (256 * 4 * cycles)
-        entry[v] = {"kernel_sha": sha, "variant_spec": VARIANTS.get(v), "hbm_bytes_per_launch": fetch + write, "fetch_bytes": fetch,
-                    "write_bytes": write, "l2_hit": hit, "dram_read_requests": c["TCC_EA0_RDREQ_DRAM_sum"],
-                    "mfma_flop": a["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512, "mfma_busy": busy}
-        dpath = os.path.join(root, f"{v}_D", "run_counter_collection.csv")
-        dd = _pmc_means(dpath, "attn_fwd")[0] if os.path.exists(dpath) else {}
+        clock = cycles / a["duration_ns"]
+        dram = None
+        if e:
+            tot, share = _read_bytes_e(e)
+            dram = tot * f_e * share
+        bv = line["variants"].get(v, {})
+        entry[v] = {"kernel_sha": sha, "variant_spec": VARIANTS.get(v), "hbm_bytes_per_launch": fetch + write,
+                    "fetch_bytes": fetch, "write_bytes": write, "dram_read_bytes": dram, "l2_hit": hit,
+                    "mfma_flop": a["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512, "mfma_busy": busy, "clock_ghz": clock,
+                    "kernel_ms": a["duration_ns"] / 1e6}
         l2_lat = (f"{dd['TCP_TCC_READ_REQ_LATENCY_sum'] / dd['TCP_TCC_READ_REQ_sum']:.0f}"
                   if dd.get("TCP_TCC_READ_REQ_sum") else "-")
         fab_lat = f"{dd['TCC_EA0_RDREQ_LEVEL_sum'] / dd['TCC_EA0_RDREQ_sum']:.0f}" if dd.get("TCC_EA0_RDREQ_sum") else "-"
-        clock = cycles / a["duration_ns"] if a.get("duration_ns") else float("nan")
-        entry[v]["clock_ghz"] = clock
-        lines.append(f"| {v} | {na} | {a.get('duration_ns', float('nan')) / 1e6:.2f} | {clock:.3f} | {100 * hit:.2f} | "
-                     f"{fetch / 1e9:.1f} | {write / 1e9:.2f} | {c['TCC_EA0_RDREQ_DRAM_sum']:.4g} | "
-                     f"{a['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.4g} | {100 * busy:.1f} | {l2_lat} | {fab_lat} |")
+        o = ost.get(v, {})
+        xb = xcd.get(v, {}).get("bytes")
+        eq1 = o.get("eq1_vs_natural")
+        tf = bv.get("tflops_attn", nan)
+        lines.append(
+            f"| {v} | {bv.get('attn_ms', nan):.3f} | {tf:.1f} | {tf / MFMA_BF16_PEAK_TFLOPS:.3f} | "
+            f"{a['duration_ns'] / 1e6:.3f} | {clock:.3f} | {100 * hit:.2f} | {fetch / 1e9:.2f} | "
+            f"{'-' if dram is None else f'{dram / 1e9:.2f}'} | {'-' if xb is None else f'{xb / 1e9:.2f}'} | "
+            f"{write / 1e9:.3f} | {100 * busy:.1f} | {o.get('adj_jaccard', nan):.3f} | "
+            f"{'-' if eq1 is None else f'{eq1:.3f}'} | {l2_lat} | {fab_lat} |")
     with open(out_json, "w") as f:
         json.dump(data, f, indent=1, sort_keys=True)
     with open(out_md, "w") as f:
@@ -586,7 +649,9 @@ def main() -> int:
                     help="comma list of: " + "; ".join(f"{k}: {v}" for k, v in VARIANT_HELP.items()))
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-xcd-bytes", action="store_true", help="skip the per-XCD compulsory K/V bytes (host work)")
+    ap.add_argument("--no-order-stats", action="store_true",
+                    help="skip the host-side statistics of each executed order (per-XCD compulsory K/V bytes, "
+                         "adjacent-row overlap, Eq. 1 objective)")
     ap.add_argument("--no-gemm-reference", action="store_true",
                     help="skip timing the vendor library's dense bf16 GEMM (context for the roofline fraction)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -594,6 +659,7 @@ def main() -> int:
     ap.add_argument("--summarize-pmc", metavar="DIR", help="summarize rocprofv3 counter passes found in DIR "
                     "into profiles/attn_traffic.json and a markdown table (no GPU needed)")
     ap.add_argument("--pmc-command", default="", help="command line recorded in the counter summary")
+    ap.add_argument("--pmc-bench-json", default="", help="bench line of the unprofiled run summarized with --summarize-pmc")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("STATS_CSV", "BENCH_JSON"),
                     help="summarize a rocprofv3 --kernel-trace --stats run of bench.py into profiles/ (no GPU needed)")
     ap.add_argument("--trace-command", default="", help="command line recorded in the trace summary")
@@ -624,7 +690,8 @@ def main() -> int:
         return 0
     if args.summarize_pmc:
         md = os.path.join(ROOT, "profiles", f"attn_fwd_{args.config}_counters.md")
-        summarize_pmc(args.summarize_pmc, args.config, TRAFFIC_FILE, md, args.pmc_command)
+        summarize_pmc(args.summarize_pmc, args.config, [x.strip() for x in args.variants.split(",") if x.strip()],
+                      args.warmup, args.steps, args.pmc_bench_json, TRAFFIC_FILE, md, args.pmc_command)
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -753,19 +820,33 @@ def main() -> int:
         step.used = used_perm
         return step
 
-    def xcd_kv_bytes(variant, used_perm):
-        """Compulsory K/V bytes when each XCD fetches every distinct block its own rows reference: with
-        one queue per XCD (n_xcd = 8) the rows of segment x run on XCD x; with one queue the slots go
-        round-robin over the 8 XCDs (slot t on XCD t mod 8, the order in which the first workgroups
-        start). Divided by the global compulsory bytes it is the duplication across the private L2s."""
+    def order_stats(variant, used_perm):
+        """Host-side statistics of the order a variant executed (rows in slot order, per head):
+        * per-XCD compulsory K/V bytes: every distinct block the rows of one XCD reference, fetched once
+          per XCD; with one queue per XCD (n_xcd = 8) the rows of segment x run on XCD x, with one queue
+          the slots go round-robin over the 8 XCDs (slot t on XCD t mod 8, the order in which the first
+          workgroups start). Over the global compulsory bytes: the duplication across the private L2s;
+        * adjacent-row overlap J = sum |M_s & M_s+1| / sum |M_s | M_s+1| over consecutive slots;
+        * the Eq. 1 objective: over consecutive waves of W = resident workgroups of the chip rows, the
+          summed squared distance of every ordered pair of rows of a wave."""
         spec = VARIANTS[variant]
         p, sg = used_perm.get("perm"), used_perm.get("seg")
         ph = p.cpu().numpy().reshape(b_ * h_, mb) if p is not None else None
         sgh = sg.cpu().numpy().reshape(b_ * h_, -1) if sg is not None else None
         total = 0
+        adj_and = adj_or = 0
+        eq1 = 0
+        w_chip = wave * 8
         mk = mask.reshape(b_ * h_, mb, mb)
         for hh in range(b_ * h_):
             order = ph[hh] if ph is not None else np.arange(mb)
+            rows_h = mk[hh][order].astype(bool)
+            adj_and += int((rows_h[1:] & rows_h[:-1]).sum())
+            adj_or += int((rows_h[1:] | rows_h[:-1]).sum())
+            for s0 in range(0, mb, w_chip):
+                wv = rows_h[s0:s0 + w_chip]
+                col = wv.sum(axis=0, dtype=np.int64)
+                eq1 += 2 * wv.shape[0] * int(col.sum()) - 2 * int((col * col).sum())
             for x in range(8):
                 if spec["n_xcd"] == 8:
                     if sgh is not None:
@@ -778,7 +859,8 @@ def main() -> int:
                     rows = order[x::8]
                 if rows.size:
                     total += int((mk[hh, rows].any(axis=0) * blk_tokens).sum())
-        return total * wl.head_dim * 2 * 2
+        return {"kv_compulsory_xcd_bytes": total * wl.head_dim * 2 * 2,
+                "adj_jaccard": adj_and / adj_or if adj_or else 0.0, "eq1_objective": eq1, "eq1_wave": w_chip}
 
     results = {}
     xcd_bytes = {}
@@ -814,8 +896,8 @@ def main() -> int:
         if VARIANTS[variant]["perm"] in ("two-stage", "stage1"):
             f = flags.cpu().numpy().reshape(-1)
             results[variant]["identity_heads"] = int(np.count_nonzero(f & 64))
-        if not args.no_xcd_bytes:
-            xcd_bytes[variant] = xcd_kv_bytes(variant, step.used)
+        if not args.no_order_stats:
+            xcd_bytes[variant] = order_stats(variant, step.used)
         log(f"{variant}: step {ms_step:.2f} ms, attention call {attn_ms:.2f} ms "
             f"({results[variant]['tflops_attn']:.1f} TFLOP/s)")
 
@@ -854,7 +936,13 @@ def main() -> int:
     }
     if xcd_bytes:
         out["algorithmic_bytes"]["kv_compulsory_per_xcd"] = {
-            v: {"bytes": b, "vs_global": b / kv_bytes} for v, b in xcd_bytes.items()}
+            v: {"bytes": st["kv_compulsory_xcd_bytes"], "vs_global": st["kv_compulsory_xcd_bytes"] / kv_bytes}
+            for v, st in xcd_bytes.items()}
+        nat = xcd_bytes.get("natural")
+        out["order_stats"] = {
+            v: {"adj_jaccard": st["adj_jaccard"], "eq1_objective": st["eq1_objective"], "eq1_wave": st["eq1_wave"],
+                "eq1_vs_natural": st["eq1_objective"] / nat["eq1_objective"] if nat and nat["eq1_objective"] else None}
+            for v, st in xcd_bytes.items()}
     if "natural" in results:
         out["speedup_vs_natural"] = {
             v: {"step": results["natural"]["ms_per_step"] / rv["ms_per_step"],
