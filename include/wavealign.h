@@ -302,6 +302,25 @@ wa_status wa_sparse_attn_vt(const void* q, const void* k, const void* vt, const 
                             const wa_shape* shape, const wa_attn_options* options, void* o, float* lse,
                             int32_t* status, void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc. The same computation as
+ * wa_sparse_attn_vt, with the scheduler state (queue counters, prefix tables, the
+ * orders of the last heads and the head-interleaved table) kept in a static device
+ * array of the library instead of a workspace: WA_NOALLOC_SCRATCH_BYTES per GPU,
+ * taken when the library's code is loaded on that GPU and held until the process
+ * ends. The call allocates and frees nothing. A shape whose state needs more
+ * (64 + n_xcd*(B*H+1) rounded up to 64, + n_xcd*T*M_B rounded up to 64, + 64 + B*H*M_B
+ * int32, T as for wa_attn_workspace_size) is rejected with WA_ERR_WORKSPACE before
+ * anything is enqueued. Every call on one GPU uses that GPU's one array and rebuilds
+ * it from scratch (counters are re-zeroed by a kernel, not a memset), so calls that
+ * overlap on one GPU (two streams, or two host threads) race: the caller serialises
+ * them. Arguments and status as for wa_sparse_attn_vt. */
+#define WA_NOALLOC_SCRATCH_BYTES (4 * 1024 * 1024)
+wa_status wa_sparse_attn_vt_noalloc(const void* q, const void* k, const void* vt, const int32_t* row_ptr,
+                                    const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
+                                    const wa_shape* shape, const wa_attn_options* options, void* o, float* lse,
+                                    int32_t* status, void* stream);
+
 /* ---- diagnostics (used by the test suite; not needed by callers) ---- */
 
 /* Evaluates on the GPU the fp64 operations the exact permutation relies on, for

@@ -19,6 +19,7 @@ WA_SKIP_AUTO, WA_SKIP_NEVER, WA_SKIP_ALWAYS = 0, 1, 2
 FLAG_FITS_CACHE, FLAG_LITTLE_WORK, FLAG_LOCAL, FLAG_UNSTRUCTURED, FLAG_DEGENERATE, FLAG_IDENTITY = 1, 2, 4, 8, 16, 64
 WA_ATTN_BAD_PERM, WA_ATTN_BAD_KV_INDEX = 1, 2
 WA_HEADS_IN_ORDER, WA_HEADS_INTERLEAVED = 0, 1
+WA_NOALLOC_SCRATCH_BYTES = 4 * 1024 * 1024
 
 
 class WaShape(ctypes.Structure):
@@ -70,6 +71,9 @@ _SIGNATURES = {
     "wa_sparse_attn_csr": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                      POINTER(WaShape), c_float, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                      c_size_t, c_void_p]),
+    "wa_sparse_attn_vt_noalloc": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                            POINTER(WaShape), POINTER(WaAttnOptions), c_void_p, c_void_p, c_void_p,
+                                            c_void_p]),
     "wa_transpose_v": (c_int32, [c_void_p, POINTER(WaShape), c_void_p, c_void_p]),
     "wa_attn_vt_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
     "wa_sparse_attn_vt": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,

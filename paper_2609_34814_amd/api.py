@@ -374,6 +374,33 @@ def sparse_attn_vt(q, k, vt, row_ptr, col_idx, perm=None, seg=None, *, block: in
     return (o, lse) if return_lse else o
 
 
+def sparse_attn_vt_noalloc(q, k, vt, row_ptr, col_idx, perm=None, seg=None, *, block: int,
+                           scale: Optional[float] = None, n_xcd: int = 8, head_order: str = "in-order",
+                           lse: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                           status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """As sparse_attn_vt, for callers that cannot allocate: the library keeps the scheduler state in
+    its static per-GPU scratch, so `out` (and `lse`, if wanted) must be given. Calls that overlap on
+    one GPU race."""
+    lib = L.load()
+    if head_order not in _HEAD_ORDER:
+        raise ValueError(f"head_order must be one of {sorted(_HEAD_ORDER)}")
+    if out is None:
+        raise ValueError("out is required (this entry point allocates nothing)")
+    shape = _attn_args(q, k, vt, block, v_transposed=True)
+    b, h, mb = _order_args(q, block, perm, seg, n_xcd)
+    _csr_args(row_ptr, col_idx, b, h, mb)
+    _check(out, "out", torch.bfloat16, tuple(q.shape))
+    _check(lse, "lse", torch.float32, tuple(q.shape[:3]))
+    _check(status, "status", torch.int32, numel_min=1)
+    _on_device(q=q, k=k, vt=vt, row_ptr=row_ptr, col_idx=col_idx, perm=perm, seg=seg, out=out, lse=lse,
+               status=status)
+    opts = L.WaAttnOptions(float(scale or 0.0), int(n_xcd), _HEAD_ORDER[head_order])
+    L.check(lib.wa_sparse_attn_vt_noalloc(_ptr(q), _ptr(k), _ptr(vt), _ptr(row_ptr), _ptr(col_idx), _ptr(perm),
+                                          _ptr(seg), ctypes.byref(shape), ctypes.byref(opts), _ptr(out), _ptr(lse),
+                                          _ptr(status), _stream()))
+    return out
+
+
 def fp64_probe(a: torch.Tensor, b: torch.Tensor, c: torch.Tensor) -> torch.Tensor:
     lib = L.load()
     out = torch.empty((a.numel(), 6), dtype=torch.float64, device=a.device)

@@ -458,6 +458,36 @@ wa_status wa_sparse_attn_csr(const void* q, const void* k, const void* v, const 
   return ok();
 }
 
+wa_status wa_sparse_attn_vt_noalloc(const void* q, const void* k, const void* vt, const int32_t* row_ptr,
+                                    const int32_t* col_idx, const int32_t* perm, const int32_t* seg_start,
+                                    const wa_shape* shape, const wa_attn_options* options, void* o, float* lse,
+                                    int32_t* status, void* stream) {
+  Dims d;
+  wa_status s = check_shape(shape, &d);
+  if (s != WA_OK) return s;
+  if (!options) return fail(WA_ERR_INVALID_ARG, "options is null");
+  s = check_attn_common(q, k, vt, o, options->n_xcd, lse, status);
+  if (s != WA_OK) return s;
+  if (options->head_order != WA_HEADS_IN_ORDER && options->head_order != WA_HEADS_INTERLEAVED)
+    return fail(WA_ERR_INVALID_ARG, "head_order %d invalid", options->head_order);
+  if (!row_ptr || !col_idx) return fail(WA_ERR_INVALID_ARG, "row_ptr and col_idx must be non-null");
+  // the kernels index the scheduler state with the call's own n_xcd
+  const size_t need = wa::sched_state_ints(d.bh, d.mb, options->n_xcd) * 4;
+  if (need > (size_t)WA_NOALLOC_SCRATCH_BYTES)
+    return fail(WA_ERR_WORKSPACE,
+                "scheduler state of %zu bytes (batch*heads %lld, M_B %d, n_xcd %d) exceeds the %d-byte static scratch",
+                need, (long long)d.bh, d.mb, options->n_xcd, WA_NOALLOC_SCRATCH_BYTES);
+  int32_t* scratch = nullptr;
+  size_t have = 0;
+  hipError_t e = wa_noalloc_scratch(&scratch, &have);
+  if (e != hipSuccess) return hip_fail(e, "static scratch lookup");
+  if (need > have) return fail(WA_ERR_WORKSPACE, "static scratch holds %zu bytes, %zu needed", have, need);
+  s = launch_attn(q, k, nullptr, vt, scratch, row_ptr, col_idx, perm, seg_start, d, options->softmax_scale,
+                  options->n_xcd, options->head_order, o, lse, status, (hipStream_t)stream);
+  if (s != WA_OK) return s;
+  return ok();
+}
+
 wa_status wa_transpose_v(const void* v, const wa_shape* shape, void* vt, void* stream) {
   Dims d;
   wa_status s = check_shape(shape, &d);

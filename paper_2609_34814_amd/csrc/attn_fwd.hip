@@ -50,6 +50,7 @@
 #include "wavealign.h"
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 namespace {
@@ -838,6 +839,32 @@ hipError_t occ_t(int* n) {
 }
 
 }  // namespace
+
+// Scheduler state of the attention entry point that allocates nothing: a static device array of the
+// library, one per GPU, held until the process ends. Host code never uses the array's name as an
+// address: its device address is looked up once per device (with that device current) and cached.
+static constexpr size_t kNoAllocInts = WA_NOALLOC_SCRATCH_BYTES / 4;
+static __device__ __align__(256) int32_t scratch[kNoAllocInts];
+static std::mutex g_scratch_mu;
+static int32_t* g_scratch_ptr[64];
+
+hipError_t wa_noalloc_scratch(int32_t** ptr, size_t* bytes) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = (int32_t*)p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  *bytes = kNoAllocInts * 4;
+  return hipSuccess;
+}
 
 size_t wa_vt_bytes(int64_t bh, int mb, int head_dim, int block) {
   return (size_t)bh * head_dim * (size_t)mb * block * 2;

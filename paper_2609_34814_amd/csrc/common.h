@@ -79,6 +79,8 @@ struct WaAttnLaunch {
 };
 
 hipError_t wa_launch_attention(const WaAttnLaunch& a, hipStream_t stream);
+// device address and size of the calling device's static scheduler scratch (looked up on first use)
+hipError_t wa_noalloc_scratch(int32_t** ptr, size_t* bytes);
 hipError_t wa_launch_transpose_v(const void* v, void* vt, int64_t bh, int seq_len, int mb, int head_dim, int block,
                                  hipStream_t stream);
 hipError_t wa_attention_occupancy(int head_dim, int block, int* wgs_per_cu);

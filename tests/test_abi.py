@@ -333,3 +333,17 @@ def test_binding_rejects_bad_permutation_outputs():
         W.build_permutation(a["mask"], seq_len=a["n"], block=a["blk"], head_dim=a["d"], skip="sometimes")
     with pytest.raises(ValueError, match="row_ptr must have shape"):
         W.compact_mask(a["mask"], seq_len=a["n"], block=a["blk"], row_ptr=torch.zeros(3, dtype=torch.int32))
+
+
+def test_noalloc_rejects_state_beyond_its_static_scratch():
+    """20,000 heads of 64 blocks need a 5 MB scheduler state, more than the static scratch: the call
+    fails before anything is enqueued (the device pointers here are never dereferenced)."""
+    lib = _lib()
+    s = L.WaShape(1, 20000, 64 * 64, 64, 64)
+    opts = L.WaAttnOptions(0.0, 1, L.WA_HEADS_IN_ORDER)
+    assert lib.wa_sparse_attn_vt_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, ctypes.byref(s),
+                                         ctypes.byref(opts), FAKE, None, None, None) == L.WA_ERR_WORKSPACE
+    assert b"static scratch" in lib.wa_last_error()
+    assert lib.wa_sparse_attn_vt_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, ctypes.byref(s), None, FAKE,
+                                         None, None, None) == L.WA_ERR_INVALID_ARG
+    assert L.WA_NOALLOC_SCRATCH_BYTES == 4 * 1024 * 1024
