@@ -253,6 +253,8 @@ def summarize_trace(stats_csv: str, bench_json: str, out_md: str, command_note: 
         return summarize_producer_trace(rows, line, out_md, command_note)
     lines = [f"# kernel trace: {line['config']['workload']}, variant {line['config']['variant']}", "",
              f"Command: `{command_note}`", "",
+             "Kernels of the library (torch's fill and sum of the 1 GiB cache flush before every step are left "
+             "out; the warm-up launches are included).", "",
              "| kernel | calls | average ms | min ms | max ms | share % |", "|---|---|---|---|---|---|"]
     attn_avg = None
     for r in rows:
@@ -261,6 +263,8 @@ def summarize_trace(stats_csv: str, bench_json: str, out_md: str, command_note: 
         avg = float(r["AverageNs"]) / 1e6
         if "attn_fwd_kernel" in name:
             attn_avg = avg
+        if short.startswith("at::"):   # torch's own kernels: the cache flush between steps
+            continue
         lines.append(f"| {short} | {r['Calls']} | {avg:.3f} | {float(r['MinNs']) / 1e6:.3f} | "
                      f"{float(r['MaxNs']) / 1e6:.3f} | {float(r['Percentage']):.2f} |")
     v = line["variants"][line["config"]["variant"]]
@@ -436,8 +440,8 @@ def run_skip_sweep(args) -> int:
     if args.sweep_points:
         keep = [s.strip() for s in args.sweep_points.split(",") if s.strip()]
         points = [p for p in points if any(s in p.name for s in keep)]
-    # 1 GiB, larger than the L2s and the last-level cache together. Each repetition READS it: a write
-    # would leave dirty lines whose write-back the next kernel would pay for.
+    # 1 GiB, larger than the L2s and the last-level cache together, written then read before each
+    # repetition (the read evicts the written lines, so no repetition pays for write-backs)
     flush = torch.zeros(1 << 28, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
     for wl in points:
@@ -452,9 +456,11 @@ def run_skip_sweep(args) -> int:
         gen = torch.Generator(device="cuda")
         gen.manual_seed(wl.seed)
         q, k, v = (torch.randn((b_, h_, n, d), generator=gen, device="cuda", dtype=torch.bfloat16) for _ in range(3))
+        vt = W.transpose_v(v, block=blk)
+        del v
         shape = W.shape_of(b_, h_, n, d, blk)
         perm_ws = torch.empty(W.perm_workspace_size(shape), dtype=torch.uint8, device="cuda")
-        attn_ws = torch.empty(W.attn_workspace_size(shape), dtype=torch.uint8, device="cuda")
+        attn_ws = torch.empty(W.attn_vt_workspace_size(shape), dtype=torch.uint8, device="cuda")
         perm = torch.empty((b_, h_, mb), dtype=torch.int32, device="cuda")
         seg = torch.empty((b_, h_, 2), dtype=torch.int32, device="cuda")
         flags = torch.empty((b_, h_), dtype=torch.uint8, device="cuda")
@@ -476,7 +482,7 @@ def run_skip_sweep(args) -> int:
             ev[1].record(stream)
             rp, ci = W.compact_mask(md, seq_len=n, block=blk, head_dim=d, row_ptr=row_ptr, col_idx=col_idx)
             ev[2].record(stream)
-            W.sparse_attn_csr(q, k, v, rp, ci, p, sg, block=blk, n_xcd=1, out=o, workspace=attn_ws)
+            W.sparse_attn_vt(q, k, vt, rp, ci, p, sg, block=blk, n_xcd=1, out=o, workspace=attn_ws)
             ev[3].record(stream)
 
         rec = {"point": wl.name, "frames": wl.grid[0], "seq_len": n, "mb": mb, "heads": h_,
@@ -486,6 +492,7 @@ def run_skip_sweep(args) -> int:
         for variant in ("natural", "reordered", "auto"):
             times = {"step": [], "perm": [], "compact": [], "attn": []}
             for r in range(1 + args.sweep_reps):
+                flush.fill_(1.0)
                 flush.sum()
                 ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
                 step(variant, ev)
@@ -510,7 +517,7 @@ def run_skip_sweep(args) -> int:
             f"{rec['auto']['identity_heads']}/{h_} heads skipped; gain step {rec['gain_step']:.3f} "
             f"attention {rec['gain_attn']:.3f}")
         print(json.dumps(rec), flush=True)
-        del md, q, k, v, perm_ws, attn_ws, perm, seg, flags, row_ptr, col_idx, o
+        del md, q, k, vt, perm_ws, attn_ws, perm, seg, flags, row_ptr, col_idx, o
         torch.cuda.empty_cache()
     return 0
 
@@ -538,8 +545,11 @@ def run_producer(args) -> int:
     pws = torch.empty(W.mask_producer_workspace_size(shape), dtype=torch.uint8, device="cuda")
     md = torch.empty((b_, h_, mb, mb), dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # as in the main benchmark
     times = []
     for r in range(args.warmup + args.steps):
+        flush.fill_(1.0)
+        flush.sum()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         W.produce_block_mask(qd, kd, block=blk, keep=keep, diagonal=True, out=md, workspace=pws)
@@ -547,25 +557,29 @@ def run_producer(args) -> int:
         torch.cuda.synchronize()
         if r >= args.warmup:
             times.append(e0.elapsed_time(e1))
-    prod_ms = float(np.mean(times))
+    prod_ms = _median(times)
     hbm_bytes = 2.0 * b_ * h_ * n * d * 2 + float(b_ * h_ * mb * mb)
     nnz = int(md.sum(dtype=torch.int64).item())
     log(f"producer: {prod_ms:.3f} ms, keep {keep} + diagonal, nnz {nnz} ({nnz / (b_ * h_ * mb * mb):.4f})")
 
     perm_ws = torch.empty(W.perm_workspace_size(shape), dtype=torch.uint8, device="cuda")
-    attn_ws = torch.empty(W.attn_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    attn_ws = torch.empty(W.attn_vt_workspace_size(shape), dtype=torch.uint8, device="cuda")
     perm = torch.empty((b_, h_, mb), dtype=torch.int32, device="cuda")
     seg = torch.empty((b_, h_, 2), dtype=torch.int32, device="cuda")
     flags = torch.empty((b_, h_), dtype=torch.uint8, device="cuda")
     row_ptr = torch.empty((b_, h_, mb + 1), dtype=torch.int32, device="cuda")
     col_idx = torch.empty((b_ * h_ * mb * mb,), dtype=torch.int32, device="cuda")
     o = torch.empty_like(qd)
+    vtd = W.transpose_v(vd, block=blk)
+    del vd
     wave = W.wave_size(d, blk) * 8
     flop = 4.0 * blk * blk * d * nnz
     res = {}
     for variant in ("natural", "reordered", "auto"):
         st = []
         for r in range(args.warmup + args.steps):
+            flush.fill_(1.0)
+            flush.sum()
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             ev[0].record(stream)
             p = sg = None
@@ -576,12 +590,12 @@ def run_producer(args) -> int:
                 p, sg = perm, seg
             rp, ci = W.compact_mask(md, seq_len=n, block=blk, head_dim=d, row_ptr=row_ptr, col_idx=col_idx)
             ev[1].record(stream)
-            W.sparse_attn_csr(qd, kd, vd, rp, ci, p, sg, block=blk, n_xcd=1, out=o, workspace=attn_ws)
+            W.sparse_attn_vt(qd, kd, vtd, rp, ci, p, sg, block=blk, n_xcd=1, out=o, workspace=attn_ws)
             ev[2].record(stream)
             torch.cuda.synchronize()
             if r >= args.warmup:
                 st.append((ev[0].elapsed_time(ev[2]), ev[1].elapsed_time(ev[2])))
-        step_ms, attn_ms = (float(np.mean([x[i] for x in st])) for i in range(2))
+        step_ms, attn_ms = (_median([x[i] for x in st]) for i in range(2))
         res[variant] = {"step_ms": step_ms, "attn_ms": attn_ms, "tflops_step": flop / (step_ms * 1e-3) / 1e12}
         if variant != "natural":
             res[variant]["identity_heads"] = int(((flags & 64) != 0).sum().item())
@@ -619,17 +633,24 @@ def summarize_sweep(jsonl: str, out_md: str, command_note: str) -> None:
                      f"{r['gain_step']:.3f} | {r['gain_attn']:.3f} | {r['auto']['step']:.2f} "
                      f"({r['auto']['identity_heads']}/{r['heads']}) | {r['auto_vs_best']:.3f} | {cases or '-'} |")
     # calibration of the skip rule's cost model (case 2): the permutation's time per head, amortised
-    # over the heads that run concurrently, as a linear function of M_B and the head's kept blocks;
-    # and the attention time saved per kept block by the reordered order
-    xs = np.array([[1.0, r["mb"], r["nnz"] / r["heads"]] for r in recs])
-    ys = np.array([r["reordered"]["perm"] * 1e6 / r["heads"] for r in recs])
-    coef = np.linalg.lstsq(xs, ys, rcond=None)[0]
-    rel = np.abs(xs @ coef - ys) / ys
-    lines += ["", "Overhead model fitted to the permutation times above (least squares over all points, "
-              "per head = step share / heads):",
-              f"ovh_ns_fixed = {coef[0]:.0f}, ovh_ns_per_row = {coef[1]:.2f}, ovh_ns_per_nnz = {coef[2]:.4f} "
-              f"(largest relative residual {100 * rel.max():.1f}%).", "",
-              "Attention time saved per kept block by the reordered order, ns (natural - reordered attention "
+    # over the heads that run concurrently, as a linear function of M_B and the head's kept blocks,
+    # fitted separately for the two forms that build it (one workgroup per head up to 512 blocks,
+    # column slices above); and the attention time saved per kept block by the reordered order
+    lines += ["", "Overhead model fitted to the permutation times above (least squares, per head = step share / "
+              "heads), one line per form that builds the permutation:"]
+    for form, sel, cols in (("one workgroup per head (M_B <= 512)", lambda r: r["mb"] <= 512, 2),
+                            ("column slices (M_B > 512)", lambda r: r["mb"] > 512, 3)):
+        rs = [r for r in recs if sel(r)]
+        if len(rs) < cols:
+            continue
+        xs = np.array([[1.0, r["mb"], r["nnz"] / r["heads"]][:cols] for r in rs])
+        ys = np.array([r["reordered"]["perm"] * 1e6 / r["heads"] for r in rs])
+        coef = np.linalg.lstsq(xs, ys, rcond=None)[0]
+        rel = np.abs(xs @ coef - ys) / ys
+        terms = f"fixed = {coef[0]:.0f} ns, per row = {coef[1]:.2f} ns" + (
+            f", per kept block = {coef[2]:.4f} ns" if cols == 3 else "")
+        lines.append(f"* {form}, {len(rs)} points: {terms} (largest relative residual {100 * rel.max():.1f}%).")
+    lines += ["", "Attention time saved per kept block by the reordered order, ns (natural - reordered attention "
               "call over the kept blocks):", ""]
     lines.append(" | ".join(f"{r['point']}: {(r['natural']['attn'] - r['reordered']['attn']) * 1e6 / r['nnz']:+.3f}"
                             for r in recs))
