@@ -10,12 +10,15 @@
 //                       tensor; a global atomic max per block instead serialised 2,841 updates on
 //                       each of 80 addresses and cost a quarter of the producer's time);
 //   quant_kernel        int8 codes rint(mean * fl32(127 / max)), clamped to [-127, 127];
-//   score_select_kernel one workgroup per ROWS query blocks of a head: exact int32 scores
-//                       s_ij = sum_c qcode_i[c] kcode_j[c] (v_dot4_i32_i8) for every KV block j
-//                       into LDS, then one wavefront per row, holding the row in registers,
-//                       finds the k-th largest score by bisection over the integer range, keeps every larger score, the first
-//                       equal scores in ascending j up to k, and the diagonal if asked, and
-//                       writes the mask row.
+//   score_select_kernel one workgroup per 16 query blocks of a head: exact int32 scores
+//                       s_ij = sum_c qcode_i[c] kcode_j[c] with int8 MFMAs
+//                       (v_mfma_i32_16x16x64_i8: 16 KV blocks x the 16 query blocks per
+//                       instruction), 256 KV blocks per pass through a small LDS tile, so
+//                       that each K code row is read once per 16 query blocks; each of the 16
+//                       wavefronts collects one row's scores in registers, finds the k-th
+//                       largest by bisection over the integer range (lane counts by ballot and
+//                       popcount), keeps every larger score, the first equal scores in
+//                       ascending j up to k, and the diagonal if asked, and writes the row.
 // Every step is exact or a single float32 rounding in a fixed order, so the mask is the same bit
 // for bit as a plain implementation of the same definition.
 
@@ -28,8 +31,8 @@
 namespace {
 
 constexpr int kPoolThreads = 128;  // (256 took 4% longer: fewer, larger workgroups per CU)
-constexpr int kRows = 4;          // query blocks per score_select workgroup
-constexpr int kSelThreads = 256;  // 4 wavefronts, one row each
+constexpr int kSelThreads = 1024;  // 16 wavefronts: one 16-KV-block tile each, then one row each
+constexpr int kChunk = 256;        // KV blocks scored per pass (16 wavefronts x 16)
 
 // amax[which][bh] = max over the head's blocks of bmax[which][bh][j]; one workgroup per (which, bh)
 __global__ __launch_bounds__(256) void head_max_kernel(WaProducerLaunch a) {
@@ -140,139 +143,176 @@ __global__ __launch_bounds__(256) void quant_kernel(WaProducerLaunch a) {
   a.codes[i] = code;
 }
 
-// One workgroup: query blocks [r0, r0 + kRows) of head bh.
-template <int D>
+// Query blocks per score_select workgroup: RG groups of 16 (the MFMA's 16 columns), two when the
+// rows' scores (2 JT registers) leave room for four wavefronts per SIMD, else one.
+template <int JT>
+struct SelGeom {
+  static constexpr int RG = JT <= 48 ? 2 : 1;
+  static constexpr int ROWS = 16 * RG;
+};
+
+// One workgroup: query blocks [r0, r0 + ROWS) of head bh. JT (a multiple of kChunk / 64 with
+// 64 JT >= mb) is the number of scores of one row each lane holds.
+template <int D, int JT>
 __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLaunch a) {
-  constexpr int W4 = D / 4;  // 32-bit words of one code row
-  constexpr int JT = WA_MAX_BLOCKS / 64;  // scores of one row per lane
-  extern __shared__ __attribute__((aligned(16))) int32_t sc[];  // [kRows][mb] scores
-  __shared__ int32_t qs[kRows][W4];
-  const int tiles = (a.mb + kRows - 1) / kRows;
+  typedef int v4i __attribute__((ext_vector_type(4)));
+  constexpr int RG = SelGeom<JT>::RG;
+  constexpr int ROWS = SelGeom<JT>::ROWS;
+  constexpr int KS = D / 64;                      // 64-channel steps of one MFMA each
+  constexpr int NCH = JT * 64 / kChunk;           // passes over the KV blocks
+  constexpr int CU = kChunk / 64;                 // entries per lane and pass
+  __shared__ int32_t sc[ROWS][kChunk + 1];        // one pass's scores (+1: fewer bank conflicts)
+  const int tiles = (a.mb + ROWS - 1) / ROWS;
   const int64_t bh = blockIdx.x / tiles;
-  const int r0 = (int)(blockIdx.x % tiles) * kRows;
-  const int nr = min(kRows, a.mb - r0);
+  const int r0 = (int)(blockIdx.x % tiles) * ROWS;
+  const int nr = min(ROWS, a.mb - r0);
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int mb = a.mb;
-  const int32_t* qc = (const int32_t*)(a.codes + ((int64_t)bh * mb) * D);
-  const int32_t* kc = (const int32_t*)(a.codes + ((int64_t)a.bh * mb + (int64_t)bh * mb) * D);
-  for (int e = tid; e < kRows * W4; e += kSelThreads) {
-    const int r = e / W4, w = e % W4;
-    qs[r][w] = r < nr ? qc[(int64_t)(r0 + r) * W4 + w] : 0;
+  const int8_t* qc = a.codes + (bh * mb) * D;
+  const int8_t* kc = a.codes + ((int64_t)a.bh * mb + bh * mb) * D;
+  const v4i zero = {0, 0, 0, 0};
+  // MFMA operands: lane l holds bytes [16 (l / 16), +16) of each 64-channel step of one code row,
+  // row l mod 16 (the same channel split for both operands, so each product pairs equal channels).
+  // B of group g: the Q codes of query block r0 + 16 g + l mod 16 (zero past the head).
+  v4i qb[RG][KS];
+#pragma unroll
+  for (int g = 0; g < RG; ++g) {
+    const int qr = r0 + 16 * g + (lane & 15);
+#pragma unroll
+    for (int st = 0; st < KS; ++st)
+      qb[g][st] = qr < mb ? *(const v4i*)(qc + (int64_t)qr * D + 64 * st + 16 * (lane >> 4)) : zero;
   }
-  __syncthreads();
-  // scores: one KV block per thread and pass
-  for (int j = tid; j < mb; j += kSelThreads) {
-    int32_t s[kRows];
+  // A of pass c: the K codes of KV block c kChunk + 16 w + l mod 16 (zero past the head), loaded
+  // one pass ahead
+  auto load_k = [&](int c, v4i (&ka)[KS]) {
+    const int kv = c * kChunk + 16 * w + (lane & 15);
 #pragma unroll
-    for (int r = 0; r < kRows; ++r) s[r] = 0;
-    const int4* kr = (const int4*)(kc + (int64_t)j * W4);
+    for (int st = 0; st < KS; ++st)
+      ka[st] = kv < mb ? *(const v4i*)(kc + (int64_t)kv * D + 64 * st + 16 * (lane >> 4)) : zero;
+  };
+  // the rows' scores: entry t of lane l is KV block 64 t + l; entries past the row hold INT32_MIN
+  // and never count. Wavefront w collects query blocks r0 + w + 16 g. (NCH passes cover the row
+  // exactly: kChunk (NCH - 1) < mb <= kChunk NCH, so every entry is written by its pass.)
+  int32_t val[RG][JT];
+  v4i ka[KS];
+  load_k(0, ka);
 #pragma unroll
-    for (int w4 = 0; w4 < W4 / 4; ++w4) {
-      const int4 kv = kr[w4];
-      const int kw[4] = {kv.x, kv.y, kv.z, kv.w};
+  for (int c = 0; c < NCH; ++c) {
+    v4i acc[RG];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+    for (int g = 0; g < RG; ++g) {
+      acc[g] = zero;
 #pragma unroll
-        for (int r = 0; r < kRows; ++r) s[r] = __builtin_amdgcn_sdot4(qs[r][4 * w4 + u], kw[u], s[r], false);
+      for (int st = 0; st < KS; ++st) acc[g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ka[st], qb[g][st], acc[g], 0, 0, 0);
     }
+    if (c + 1 < NCH) load_k(c + 1, ka);
+    // each 16 x 16 result: lane l holds KV rows 4 (l / 16) + e, query column l mod 16 of its group
 #pragma unroll
-    for (int r = 0; r < kRows; ++r) sc[r * mb + j] = s[r];
+    for (int g = 0; g < RG; ++g)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sc[16 * g + (lane & 15)][16 * w + 4 * (lane >> 4) + e] = acc[g][e];
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < RG; ++g)
+#pragma unroll
+      for (int u = 0; u < CU; ++u) {
+        const int j = c * kChunk + 64 * u + lane;
+        val[g][c * CU + u] = j < mb ? sc[w + 16 * g][64 * u + lane] : INT32_MIN;
+      }
+    __syncthreads();  // every row is collected before the next pass overwrites the tile
   }
-  __syncthreads();
-  // selection: wavefront w handles row w, with the row's scores in registers (entry t of lane l is
-  // block 64 t + l; entries past the row hold INT32_MIN and are never counted)
-  const int lane = tid & 63, r = tid >> 6;
-  if (r >= nr) return;
   const int keep = a.keep < mb ? a.keep : mb;
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-  const int32_t* row = sc + r * mb;
-  const int i = r0 + r;
-  int32_t val[JT];
 #pragma unroll
-  for (int t = 0; t < JT; ++t) {
-    const int j = 64 * t + lane;
-    val[t] = j < mb ? row[j] : INT32_MIN;
-  }
-  // k-th largest value v: the largest v with #{s >= v} >= keep
-  int lo = INT32_MAX, hi = INT32_MIN;
+  for (int g = 0; g < RG; ++g) {
+    if (w + 16 * g >= nr) break;
+    const int i = r0 + w + 16 * g;
+    const int32_t (&v_)[JT] = val[g];
+    // k-th largest value v: the largest v with #{s >= v} >= keep
+    // (a score is at most 128 x 127 x 127 in magnitude, so INT32_MIN marks exactly the missing entries)
+    int lo = INT32_MAX, hi = INT32_MIN;
 #pragma unroll
-  for (int t = 0; t < JT; ++t)
-    if (64 * t + lane < mb) {
-      lo = min(lo, val[t]);
-      hi = max(hi, val[t]);
+    for (int t = 0; t < JT; ++t) {
+      lo = min(lo, v_[t] == INT32_MIN ? INT32_MAX : v_[t]);
+      hi = max(hi, v_[t]);
     }
-  for (int o = 32; o > 0; o >>= 1) {
-    lo = min(lo, __shfl_xor(lo, o));
-    hi = max(hi, __shfl_xor(hi, o));
-  }
-  // invariant: #{s >= lo} >= keep (lo = the minimum counts every entry), #{s >= hi + 1} < keep
-  while (keep > 0 && lo < hi) {
-    const int mid = lo + (int)(((int64_t)hi - lo + 1) / 2);
-    int c = 0;
+    for (int o = 32; o > 0; o >>= 1) {
+      lo = min(lo, __shfl_xor(lo, o));
+      hi = max(hi, __shfl_xor(hi, o));
+    }
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    hi = __builtin_amdgcn_readfirstlane(hi);
+    // invariant: #{s >= lo} >= keep (lo = the minimum counts every entry), #{s >= hi + 1} < keep
+    while (keep > 0 && lo < hi) {
+      const int mid = lo + (int)(((int64_t)hi - lo + 1) / 2);
+      int cnt = 0;  // (the missing entries, INT32_MIN, never reach mid)
 #pragma unroll
-    for (int t = 0; t < JT; ++t) c += val[t] >= mid;
-    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
-    if (c >= keep) lo = mid; else hi = mid - 1;
-  }
-  const int v = lo;
-  int greater = 0;
+      for (int t = 0; t < JT; ++t) cnt += __popcll(__ballot(v_[t] >= mid));
+      if (cnt >= keep) lo = mid; else hi = mid - 1;
+    }
+    const int v = lo;
+    int greater = 0;
 #pragma unroll
-  for (int t = 0; t < JT; ++t) greater += val[t] > v;
-  for (int o = 32; o > 0; o >>= 1) greater += __shfl_xor(greater, o);
-  const int ties = keep - greater;  // equal scores to keep, in ascending j
-  uint8_t* out = a.mask + ((int64_t)bh * mb + i) * mb;
-  int seen = 0;
+    for (int t = 0; t < JT; ++t) greater += __popcll(__ballot(v_[t] > v));
+    const int ties = keep - greater;  // equal scores to keep, in ascending j
+    uint8_t* out = a.mask + ((int64_t)bh * mb + i) * mb;
+    int seen = 0;
 #pragma unroll
-  for (int t = 0; t < JT; ++t) {
-    const int j = 64 * t + lane;
-    const bool in = j < mb;
-    const bool eq = in && keep > 0 && val[t] == v;
-    const uint64_t eqw = __ballot(eq);
-    const int rank = seen + __popcll(eqw & below);
-    const bool kept = keep > 0 && in && (val[t] > v || (eq && rank < ties));
-    const bool diag = a.diagonal && j == i;
-    if (in) out[j] = (kept || diag) ? 1 : 0;
-    seen += __popcll(eqw);
+    for (int t = 0; t < JT; ++t) {
+      if (64 * t >= mb) break;
+      const int j = 64 * t + lane;
+      const bool in = v_[t] != INT32_MIN;  // j < mb
+      const bool eq = in && keep > 0 && v_[t] == v;
+      const uint64_t eqw = __ballot(eq);
+      const int rank = seen + __popcll(eqw & below);
+      const bool kept = keep > 0 && in && (v_[t] > v || (eq && rank < ties));
+      const bool diag = a.diagonal && j == i;
+      if (in) out[j] = (kept || diag) ? 1 : 0;
+      seen += __popcll(eqw);
+    }
   }
+}
+
+template <int D, int JT>
+hipError_t launch_select_t(const WaProducerLaunch& a, hipStream_t stream) {
+  const dim3 grid((unsigned)(a.bh * ((a.mb + SelGeom<JT>::ROWS - 1) / SelGeom<JT>::ROWS)));
+  hipLaunchKernelGGL((score_select_kernel<D, JT>), grid, dim3(kSelThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_select(const WaProducerLaunch& a, hipStream_t stream) {
+  const int jt = (a.mb + kChunk - 1) / kChunk * (kChunk / 64);  // scores per lane, whole passes
+  if (jt <= 16) return launch_select_t<D, 16>(a, stream);
+  if (jt <= 32) return launch_select_t<D, 32>(a, stream);
+  if (jt <= 48) return launch_select_t<D, 48>(a, stream);
+  return launch_select_t<D, WA_MAX_BLOCKS / 64>(a, stream);
+}
+
+template <int D>
+hipError_t launch_all(const WaProducerLaunch& a, hipStream_t stream) {
+  const int64_t pool_threads = (int64_t)a.bh * a.mb * (D / 8);
+  const dim3 pgrid((unsigned)((pool_threads + kPoolThreads - 1) / kPoolThreads), 2);
+  const int64_t qn = 2ll * a.bh * a.mb * D;
+  const dim3 qgrid((unsigned)((qn + 255) / 256));
+  hipError_t e;
+  hipLaunchKernelGGL(pool_kernel<D>, pgrid, dim3(kPoolThreads), 0, stream, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(head_max_kernel, dim3((unsigned)(2 * a.bh)), dim3(256), 0, stream, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(quant_kernel<D>, qgrid, dim3(256), 0, stream, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_select<D>(a, stream);
 }
 
 }  // namespace
 
-size_t wa_producer_select_smem(int mb) { return (size_t)kRows * mb * sizeof(int32_t); }
-
 hipError_t wa_launch_producer(const WaProducerLaunch& a, hipStream_t stream) {
   if (a.bh <= 0 || a.mb <= 0) return hipSuccess;
-  hipError_t e = hipSuccess;
-  const int64_t pool_threads = (int64_t)a.bh * a.mb * (a.head_dim / 8);
-  const dim3 pgrid((unsigned)((pool_threads + kPoolThreads - 1) / kPoolThreads), 2);
-  const int64_t qn = 2ll * a.bh * a.mb * a.head_dim;
-  const dim3 qgrid((unsigned)((qn + 255) / 256));
-  const dim3 sgrid((unsigned)(a.bh * ((a.mb + kRows - 1) / kRows)));
-  const size_t smem = wa_producer_select_smem(a.mb);
-  if (a.head_dim == 128) {
-    hipLaunchKernelGGL(pool_kernel<128>, pgrid, dim3(kPoolThreads), 0, stream, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(head_max_kernel, dim3((unsigned)(2 * a.bh)), dim3(256), 0, stream, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(quant_kernel<128>, qgrid, dim3(256), 0, stream, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipFuncSetAttribute((const void*)score_select_kernel<128>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)smem)) != hipSuccess)
-      return e;
-    hipLaunchKernelGGL(score_select_kernel<128>, sgrid, dim3(kSelThreads), smem, stream, a);
-  } else if (a.head_dim == 64) {
-    hipLaunchKernelGGL(pool_kernel<64>, pgrid, dim3(kPoolThreads), 0, stream, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(head_max_kernel, dim3((unsigned)(2 * a.bh)), dim3(256), 0, stream, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(quant_kernel<64>, qgrid, dim3(256), 0, stream, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipFuncSetAttribute((const void*)score_select_kernel<64>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)smem)) != hipSuccess)
-      return e;
-    hipLaunchKernelGGL(score_select_kernel<64>, sgrid, dim3(kSelThreads), smem, stream, a);
-  } else {
-    return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  if (a.mb > WA_MAX_BLOCKS) return hipErrorInvalidValue;
+  if (a.head_dim == 128) return launch_all<128>(a, stream);
+  if (a.head_dim == 64) return launch_all<64>(a, stream);
+  return hipErrorInvalidValue;
 }

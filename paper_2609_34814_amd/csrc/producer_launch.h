@@ -16,4 +16,3 @@ struct WaProducerLaunch {
 };
 
 hipError_t wa_launch_producer(const WaProducerLaunch& a, hipStream_t stream);
-size_t wa_producer_select_smem(int mb);

@@ -65,6 +65,18 @@ def test_producer_ties_and_zero_maximum():
     assert np.all(mask[..., :5] == 1) and not mask[..., 5:].any()
 
 
+@pytest.mark.parametrize("mb,d,keep", [(1500, 128, 75), (4096, 64, 200), (257, 64, 9)])
+def test_producer_bit_exact_row_widths(mb, d, keep):
+    """Heads of 1,500, 4,096 and 257 blocks (ragged last blocks): every width of the selection's
+    per-lane score array, the largest supported head included."""
+    wl = custom(f"rows{mb}", heads=1, head_dim=d, block=64, grid=(mb, 8, 8), seq_len=mb * 64 - 33, seed=23 + mb)
+    assert wl.mb == mb
+    q, k, _ = make_qkv(wl)
+    mask, codes = _run(q, k, wl.block, keep, True)
+    assert np.array_equal(codes, _oracle_codes(q, k, wl.block))
+    assert np.array_equal(mask, MP.produce_mask(q, k, wl.block, keep, True))
+
+
 def test_producer_bit_exact_full_size():
     """363,600 tokens, 40 heads, 5% of the blocks per row: every row of every head."""
     wl = PRODUCER_CONFIGS["produced-long-720p-401f"]
