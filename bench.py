@@ -935,6 +935,20 @@ def main() -> int:
         "frac": r["tflops_attn"] / MFMA_BF16_PEAK_TFLOPS,
         "traffic": traffic,
     }
+    # The kernel's second roof: LDS bandwidth. Per kept block each of the block/32 wavefronts reads the
+    # whole K tile and V^T tile from LDS (its MFMA operands) and the tiles are written once by the
+    # global->LDS copies: (block/32 + 1) x 2 tiles of block x d bf16. gfx950 moves 128 B/clk/CU in
+    # LDS, so at the 2.4 GHz peak clock 256 x 128 x 2.4e9 B/s; MFMA work per kept block needs
+    # 4 block^2 d / (2500e12 / 256 / 2.4e9 FLOP/clk/CU) cycles, so the LDS roof caps MFMA at
+    # (MFMA cycles) / (LDS cycles) of its peak.
+    lds_bytes_block = (wl.block // 32 + 1) * 2 * wl.block * wl.head_dim * 2
+    lds_peak = 256 * 128 * 2.4e9
+    lds_achieved = lds_bytes_block * nnz / (r["attn_ms"] * 1e-3)
+    mfma_cycles = 4.0 * wl.block * wl.block * wl.head_dim / (MFMA_BF16_PEAK_TFLOPS * 1e12 / 256 / 2.4e9)
+    lds_roof = {"bytes_per_kept_block": lds_bytes_block, "achieved_TBps": lds_achieved / 1e12,
+                "peak_TBps": lds_peak / 1e12, "frac": lds_achieved / lds_peak,
+                "mfma_cap": mfma_cycles / (lds_bytes_block / 128.0),
+                "kind": "derived from the kernel's tile traffic, not a counter"}
     out = {
         "metric": "sparse-attn effective TFLOP/s (skip rule + reordering + attention, overhead included)",
         "value": r["tflops_step"],
@@ -953,6 +967,7 @@ def main() -> int:
                    "flop_per_step": flop, "variant": head, "wave_per_xcd": wave, "v_input": "transposed",
                    "timing": "median over steps, each after a 1 GiB write + read cache flush"},
         "roofline": roof,
+        "lds_roofline": lds_roof,
         "algorithmic_bytes": {"kv_compulsory": kv_bytes, "q_and_o": qo_bytes, "kv_lists": list_bytes,
                               "total": algo_bytes, "flop_per_byte": flop / algo_bytes},
         "variants": results,

@@ -71,6 +71,8 @@ typedef struct wa_shape {
  *   1  distinct_kv_blocks * kv_block_bytes <= cache_bytes             (fits in cache)
  *   2  nnz * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row * M_B
  *                                 + ovh_ns_per_nnz * nnz                (too little work)
+ *      with the ovh_fused_* constants instead when M_B <= fused_max_blocks (heads the
+ *      permutation builds in one workgroup, whose cost grows differently)
  *   3  sum_i |M_i & M_i+1| / sum_i |M_i | M_i+1| >= j_max              (already local)
  *      or, once the order P is built, J(P) <= J(natural order), with J that
  *      overlap over consecutive rows of an order, compared as exact integer
@@ -85,6 +87,10 @@ typedef struct wa_skip_profile {
   double ovh_ns_per_nnz;
   double j_max;
   double eta_min;
+  double fused_max_blocks;
+  double ovh_fused_ns_fixed;
+  double ovh_fused_ns_per_row;
+  double ovh_fused_ns_per_nnz;
 } wa_skip_profile;
 
 enum { WA_SKIP_AUTO = 0, WA_SKIP_NEVER = 1, WA_SKIP_ALWAYS = 2 };

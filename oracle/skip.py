@@ -13,7 +13,10 @@ here is:
           distinct_h * kv_block_bytes <= cache_bytes
   case 2 "too little work": the expected kernel-time saving does not exceed
           the reordering overhead, both linear models from offline profiles:
-          nnz_h * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row*m + ovh_ns_per_nnz*nnz_h
+          nnz_h * gain_ns_per_block < ovh_ns_fixed + ovh_ns_per_row*m + ovh_ns_per_nnz*nnz_h,
+          with a second set of overhead constants (ovh_fused_*) for heads of at
+          most fused_max_blocks rows: the implementation builds those in another
+          form whose measured cost follows another line
   case 3 "already local": adjacent rows already share most blocks:
           J_h = sum_i |M_i & M_{i+1}| / sum_i |M_i | M_{i+1}| >= j_max,
           or, once the two-stage order P is built, it does not raise that overlap:
@@ -59,11 +62,15 @@ SKIP_AUTO, SKIP_NEVER, SKIP_ALWAYS = 0, 1, 2
 class SkipProfile:
     cache_bytes: float = 96.0 * 1024 * 1024
     gain_ns_per_block: float = 0.5
-    ovh_ns_fixed: float = 6122.0
-    ovh_ns_per_row: float = 4.55
-    ovh_ns_per_nnz: float = 0.0567
+    ovh_ns_fixed: float = 10416.0
+    ovh_ns_per_row: float = 3.58
+    ovh_ns_per_nnz: float = 0.0556
     j_max: float = 0.2
     eta_min: float = 0.05
+    fused_max_blocks: float = 512.0
+    ovh_fused_ns_fixed: float = 2618.0
+    ovh_fused_ns_per_row: float = 14.17
+    ovh_fused_ns_per_nnz: float = 0.0
 
 
 @dataclass
@@ -99,7 +106,11 @@ def tier1_flags(st: HeadStats, prof: SkipProfile, block: int, head_dim: int) -> 
     if float(st.distinct) * float(kv_block_bytes(block, head_dim)) <= prof.cache_bytes:
         flags |= FLAG_FITS_CACHE
     saving = float(st.nnz) * prof.gain_ns_per_block
-    cost = prof.ovh_ns_fixed + prof.ovh_ns_per_row * float(st.m) + prof.ovh_ns_per_nnz * float(st.nnz)
+    if float(st.m) <= prof.fused_max_blocks:
+        c0, c1, c2 = prof.ovh_fused_ns_fixed, prof.ovh_fused_ns_per_row, prof.ovh_fused_ns_per_nnz
+    else:
+        c0, c1, c2 = prof.ovh_ns_fixed, prof.ovh_ns_per_row, prof.ovh_ns_per_nnz
+    cost = c0 + c1 * float(st.m) + c2 * float(st.nnz)
     if saving < cost:
         flags |= FLAG_LITTLE_WORK
     if st.adj_or > 0 and float(st.adj_and) / float(st.adj_or) >= prof.j_max:

@@ -30,7 +30,8 @@ class WaShape(ctypes.Structure):
 class WaSkipProfile(ctypes.Structure):
     _fields_ = [("cache_bytes", c_double), ("gain_ns_per_block", c_double), ("ovh_ns_fixed", c_double),
                 ("ovh_ns_per_row", c_double), ("ovh_ns_per_nnz", c_double), ("j_max", c_double),
-                ("eta_min", c_double)]
+                ("eta_min", c_double), ("fused_max_blocks", c_double), ("ovh_fused_ns_fixed", c_double),
+                ("ovh_fused_ns_per_row", c_double), ("ovh_fused_ns_per_nnz", c_double)]
 
 
 class WaPermParams(ctypes.Structure):

@@ -515,7 +515,12 @@ __device__ HeadInit init_head(const WaPermLaunch& a, Shared& sh, int h) {
     const double kvb = (double)(2 * a.block * a.head_dim * 2);
     if ((double)distinct * kvb <= a.prof.cache_bytes) f |= FLAG_FITS_CACHE;
     const double saving = (double)nnz * a.prof.gain_ns_per_block;
-    const double cost = a.prof.ovh_ns_fixed + a.prof.ovh_ns_per_row * (double)m + a.prof.ovh_ns_per_nnz * (double)nnz;
+    // the cost curve of the form that builds this head: one workgroup for small heads, else sliced
+    const bool fused = (double)m <= a.prof.fused_max_blocks;
+    const double c0 = fused ? a.prof.ovh_fused_ns_fixed : a.prof.ovh_ns_fixed;
+    const double c1 = fused ? a.prof.ovh_fused_ns_per_row : a.prof.ovh_ns_per_row;
+    const double c2 = fused ? a.prof.ovh_fused_ns_per_nnz : a.prof.ovh_ns_per_nnz;
+    const double cost = c0 + c1 * (double)m + c2 * (double)nnz;
     if (saving < cost) f |= FLAG_LITTLE_WORK;
     if (adj[1] > 0 && (double)adj[0] / (double)adj[1] >= a.prof.j_max) f |= FLAG_LOCAL;
     sh.i32[1] = f;

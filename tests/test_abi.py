@@ -43,6 +43,11 @@ def test_version_and_strings():
     p = L.WaSkipProfile()
     assert lib.wa_default_skip_profile(ctypes.byref(p)) == 0
     assert p.cache_bytes == 96 * 1024 * 1024 and p.j_max == 0.2 and p.eta_min == 0.05
+    # the library's built-in profile is the oracle's default, field for field
+    from oracle import skip as S
+    ref = S.SkipProfile()
+    for name, _ in L.WaSkipProfile._fields_:
+        assert getattr(p, name) == getattr(ref, name), name
     assert lib.wa_default_skip_profile(None) == L.WA_ERR_INVALID_ARG
 
 

@@ -34,7 +34,8 @@ def _w():
 def _profile_np_to_c(p: S.SkipProfile):
     from paper_2609_34814_amd import _lib
     return _lib.WaSkipProfile(p.cache_bytes, p.gain_ns_per_block, p.ovh_ns_fixed, p.ovh_ns_per_row,
-                              p.ovh_ns_per_nnz, p.j_max, p.eta_min)
+                              p.ovh_ns_per_nnz, p.j_max, p.eta_min, p.fused_max_blocks, p.ovh_fused_ns_fixed,
+                              p.ovh_fused_ns_per_row, p.ovh_fused_ns_per_nnz)
 
 
 # ------------------------------------------------------------------------------------------------

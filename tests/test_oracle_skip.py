@@ -59,7 +59,7 @@ def test_tier1_cases():
     assert f & S.FLAG_FITS_CACHE          # 64 KV blocks of 16 KiB = 1 MiB < 96 MiB
     big = S.head_stats(make_mask_head(CONFIGS["wan14b-720p-81f"], 0, 0))
     # 591 KV blocks of 64 KiB = 37 MiB: below the 96 MiB break-even, not inside one 4 MiB L2;
-    # 84K kept blocks save 42 us at 0.5 ns each, more than the 14 us the permutation costs;
+    # 84K kept blocks save 42 us at 0.5 ns each, more than the 17 us the permutation costs;
     # adjacent rows share 36% of their blocks (raster order is already local)
     assert S.tier1_flags(big, prof, 128, 128) == S.FLAG_FITS_CACHE | S.FLAG_LOCAL
     assert S.tier1_flags(big, PERMISSIVE, 128, 128) == 0
@@ -78,6 +78,26 @@ def test_tier1_cases():
     assert S.tier1_flags(st, exact, 128, 128) & S.FLAG_FITS_CACHE
     below = S.SkipProfile(cache_bytes=128 * S.kv_block_bytes(128, 128) - 1)
     assert not (S.tier1_flags(st, below, 128, 128) & S.FLAG_FITS_CACHE)
+
+
+def test_little_work_uses_the_cost_curve_of_the_form_that_builds_the_head():
+    """Case 2 takes the one-workgroup form's overhead line up to fused_max_blocks rows and the sliced
+    form's line above: the same statistics flip the decision at the boundary when only one of the
+    two lines exceeds the saving."""
+    prof = S.SkipProfile(cache_bytes=0.0, gain_ns_per_block=1.0, j_max=2.0, fused_max_blocks=512.0,
+                         ovh_ns_fixed=0.0, ovh_ns_per_row=0.0, ovh_ns_per_nnz=0.0,
+                         ovh_fused_ns_fixed=1e9, ovh_fused_ns_per_row=0.0, ovh_fused_ns_per_nnz=0.0)
+    for m, want in ((512, S.FLAG_LITTLE_WORK), (513, 0)):
+        st = S.head_stats(np.eye(m, dtype=np.uint8))
+        assert S.tier1_flags(st, prof, 128, 128) == want, m
+    # the saving is compared strictly: equal costs keep the reordering
+    st = S.head_stats(np.eye(600, dtype=np.uint8))
+    even = S.SkipProfile(cache_bytes=0.0, gain_ns_per_block=1.0, j_max=2.0, ovh_ns_fixed=600.0,
+                         ovh_ns_per_row=0.0, ovh_ns_per_nnz=0.0)
+    assert S.tier1_flags(st, even, 128, 128) == 0
+    assert S.tier1_flags(st, S.SkipProfile(cache_bytes=0.0, gain_ns_per_block=1.0, j_max=2.0,
+                                           ovh_ns_fixed=600.5, ovh_ns_per_row=0.0, ovh_ns_per_nnz=0.0),
+                         128, 128) == S.FLAG_LITTLE_WORK
 
 
 def test_default_rule_decides_per_head_on_mixed_heads():
