@@ -74,10 +74,14 @@ SMALL = [
     custom("dense", heads=2, head_dim=128, block=128, grid=(2, 16, 20), rule=dict(kind="ones"), seed=12),
     custom("single", heads=2, head_dim=64, block=128, grid=(1, 5, 20), rule=dict(kind="bernoulli", p=0.5), seed=13),
     custom("diag", heads=2, head_dim=128, block=64, grid=(2, 20, 20), rule=dict(kind="diag"), seed=14),
+    # two sequences of three heads: every flat (batch, head) index, ragged last block of 91 tokens
+    custom("batched", batch=2, heads=3, head_dim=128, block=128, grid=(4, 16, 24), seq_len=4 * 16 * 24 - 37,
+           rule=dict(kind="radius", rt=1, rs=2, g=2), seed=16),
 ]
 
 
-@pytest.mark.parametrize("name", ["tiny", "wan1.3b-480p-81f", "skip-d64", "ragged", "dense", "single", "diag"])
+@pytest.mark.parametrize("name", ["tiny", "wan1.3b-480p-81f", "skip-d64", "ragged", "dense", "single", "diag",
+                                  "batched"])
 def test_compaction_bit_exact(name):
     wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
     mask = make_mask(wl)
@@ -107,18 +111,19 @@ def test_compaction_bit_exact_large(name):
         assert csr_matches_mask(mask[0, h], rp[0, h], ci[base: base + mb * mb])
 
 
-@pytest.mark.parametrize("name", ["tiny", "wan14b-720p-81f", "skip-d64", "ragged", "single"])
+@pytest.mark.parametrize("name", ["tiny", "wan14b-720p-81f", "skip-d64", "ragged", "single", "batched"])
 def test_mask_stats_bit_exact(name):
     wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
     mask = make_mask(wl)
     rn, cc, hs = _w().mask_stats(u8_dev(mask), seq_len=wl.seq_len, block=wl.block, head_dim=wl.head_dim)
     torch.cuda.synchronize()
     rn, cc, hs = rn.cpu().numpy(), cc.cpu().numpy(), hs.cpu().numpy()
-    for h in range(wl.heads):
-        st = S.head_stats(mask[0, h])
-        assert np.array_equal(rn[0, h], st.row_nnz)
-        assert np.array_equal(cc[0, h], st.col_cnt)
-        assert list(hs[0, h]) == [st.nnz, st.distinct, st.adj_and, st.adj_or, st.sum_c2, 0]
+    for b in range(wl.batch):
+        for h in range(wl.heads):
+            st = S.head_stats(mask[b, h])
+            assert np.array_equal(rn[b, h], st.row_nnz)
+            assert np.array_equal(cc[b, h], st.col_cnt)
+            assert list(hs[b, h]) == [st.nnz, st.distinct, st.adj_and, st.adj_or, st.sum_c2, 0]
 
 
 # ------------------------------------------------------------------------------------------------
@@ -155,7 +160,8 @@ _SMALL_CACHE = S.SkipProfile(cache_bytes=4 * 1024 * 1024, gain_ns_per_block=1.0,
                              ovh_ns_per_row=2.0, ovh_ns_per_nnz=0.05, j_max=0.75)
 
 
-@pytest.mark.parametrize("name", ["tiny", "wan1.3b-480p-81f", "skip-d64", "ragged", "dense", "single", "diag"])
+@pytest.mark.parametrize("name", ["tiny", "wan1.3b-480p-81f", "skip-d64", "ragged", "dense", "single", "diag",
+                                  "batched"])
 @pytest.mark.parametrize("mode,profile", [(S.SKIP_NEVER, None), (S.SKIP_AUTO, None), (S.SKIP_AUTO, _SMALL_CACHE)],
                          ids=["never", "auto", "auto-small-cache"])
 def test_permutation_bit_exact(name, mode, profile):
@@ -210,7 +216,7 @@ def _run_attn(wl, mask, q, k, v, perm=None, n_xcd=8, seg=None):
     return o, lse
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged", "dense", "single", "diag"])
+@pytest.mark.parametrize("name", ["tiny", "ragged", "dense", "single", "diag", "batched"])
 def test_attention_full_vs_oracle(name):
     wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
     q, k, v = make_qkv(wl)
@@ -301,7 +307,7 @@ def test_attention_sampled_vs_oracle(name, count):
     _check(st)
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64"])
+@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64", "batched"])
 def test_output_bit_identical_across_permutations(name):
     wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
     q, k, v = (bf16_dev(x) for x in make_qkv(wl))
@@ -326,7 +332,7 @@ def test_output_bit_identical_across_permutations(name):
         assert torch.equal(l2.view(torch.int32), l_nat.view(torch.int32))
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64"])
+@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64", "batched"])
 def test_transpose_v_layout(name):
     """wa_transpose_v writes vt[b][h][c][t] = V[b][h][t][c] for t < N and zeros up to M_B*block."""
     wl = CONFIGS.get(name) or {w.name: w for w in SMALL}[name]
@@ -339,7 +345,7 @@ def test_transpose_v_layout(name):
     assert np.array_equal(got, want)
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64"])
+@pytest.mark.parametrize("name", ["tiny", "ragged", "wan1.3b-480p-81f", "skip-d64", "batched"])
 def test_vt_entry_and_head_orders_bit_identical(name):
     """V given transposed, heads in order or interleaved, one or eight queues, with and without a
     segment table: O and LSE bit-identical to the natural-order call, status word 0."""
