@@ -21,6 +21,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -41,9 +42,16 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+_CODE_TOKENS = re.compile(r'"(?:\\.|[^"\\\n])*"|//[^\n]*|/\*.*?\*/', re.S)
+
+
 def kernel_source_hash() -> str:
-    with open(ATTN_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the attention source's code: comments removed and whitespace runs collapsed, so that a
+    counter summary stays attached to the kernel it measured when only its comments change."""
+    with open(ATTN_SRC, encoding="utf-8") as f:
+        text = f.read()
+    code = _CODE_TOKENS.sub(lambda m: m.group(0) if m.group(0).startswith('"') else " ", text)
+    return hashlib.sha256(" ".join(code.split()).encode()).hexdigest()[:16]
 
 
 def load_traffic(workload: str, variant: str):
@@ -935,20 +943,32 @@ def main() -> int:
         "frac": r["tflops_attn"] / MFMA_BF16_PEAK_TFLOPS,
         "traffic": traffic,
     }
-    # The kernel's second roof: LDS bandwidth. Per kept block each of the block/32 wavefronts reads the
-    # whole K tile and V^T tile from LDS (its MFMA operands) and the tiles are written once by the
-    # global->LDS copies: (block/32 + 1) x 2 tiles of block x d bf16. gfx950 moves 128 B/clk/CU in
-    # LDS, so at the 2.4 GHz peak clock 256 x 128 x 2.4e9 B/s; MFMA work per kept block needs
-    # 4 block^2 d / (2500e12 / 256 / 2.4e9 FLOP/clk/CU) cycles, so the LDS roof caps MFMA at
-    # (MFMA cycles) / (LDS cycles) of its peak.
+    # LDS, the kernel's on-chip operand path. Per kept block each of the block/32 wavefronts reads the
+    # whole K tile and V^T tile from LDS (its MFMA operands) and the global->LDS copies write both tiles
+    # once: (block/32 + 1) x 2 tiles of block x d bf16. gfx950 serves 128-bit LDS reads at 256 B/clk/CU
+    # (225 measured with two wavefronts per SIMD, this kernel's occupancy), so at the 2.4 GHz peak clock
+    # 256 x 256 x 2.4e9 B/s. The MFMA work of a kept block takes 4 block^2 d / (2500e12 / 256 / 2.4e9
+    # FLOP/clk/CU) cycles; LDS would cap MFMA use only if a block's LDS cycles exceeded those.
     lds_bytes_block = (wl.block // 32 + 1) * 2 * wl.block * wl.head_dim * 2
-    lds_peak = 256 * 128 * 2.4e9
+    lds_b_per_clk = 256.0
+    lds_peak = 256 * lds_b_per_clk * 2.4e9
     lds_achieved = lds_bytes_block * nnz / (r["attn_ms"] * 1e-3)
     mfma_cycles = 4.0 * wl.block * wl.block * wl.head_dim / (MFMA_BF16_PEAK_TFLOPS * 1e12 / 256 / 2.4e9)
+    lds_cycles = lds_bytes_block / lds_b_per_clk
     lds_roof = {"bytes_per_kept_block": lds_bytes_block, "achieved_TBps": lds_achieved / 1e12,
                 "peak_TBps": lds_peak / 1e12, "frac": lds_achieved / lds_peak,
-                "mfma_cap": mfma_cycles / (lds_bytes_block / 128.0),
+                "lds_cycles_per_mfma_cycle": lds_cycles / mfma_cycles,
+                "mfma_cap": min(1.0, mfma_cycles / lds_cycles), "binding": lds_cycles > mfma_cycles,
                 "kind": "derived from the kernel's tile traffic, not a counter"}
+    # Where the bf16 fraction goes: the clock the chip held under the kernel (power-limited) times the
+    # share of those cycles the MFMA pipes were busy, both from the committed counter summary.
+    cnt = load_counters(wl.name, head)
+    clock_split = None
+    if cnt and cnt.get("clock_ghz") and cnt.get("mfma_busy") is not None:
+        clock_split = {"clock_ghz": cnt["clock_ghz"], "clock_share_of_2.4GHz": cnt["clock_ghz"] / 2.4,
+                       "mfma_busy": cnt["mfma_busy"],
+                       "frac_at_that_clock": roof["frac"] * 2.4 / cnt["clock_ghz"],
+                       "source": cnt["source"]}
     out = {
         "metric": "sparse-attn effective TFLOP/s (skip rule + reordering + attention, overhead included)",
         "value": r["tflops_step"],
@@ -968,6 +988,7 @@ def main() -> int:
                    "timing": "median over steps, each after a 1 GiB write + read cache flush"},
         "roofline": roof,
         "lds_roofline": lds_roof,
+        "clock_split": clock_split,
         "algorithmic_bytes": {"kv_compulsory": kv_bytes, "q_and_o": qo_bytes, "kv_lists": list_bytes,
                               "total": algo_bytes, "flop_per_byte": flop / algo_bytes},
         "variants": results,

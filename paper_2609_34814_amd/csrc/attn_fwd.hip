@@ -26,8 +26,8 @@
 //   * P^T in bf16 is the B operand of O^T += V^T P^T directly from those
 //     registers; the matching A operand is one 16-byte row chunk of V^T (8 keys
 //     of one d), so every operand read is one ds_read_b128. (Reading V in its
-//     natural layout with ds_read_b64_tr_b16 moves half the bytes per LDS cycle,
-//     and LDS bandwidth, not the MFMA rate, bounds this kernel.)
+//     natural layout with ds_read_b64_tr_b16 takes two LDS instructions per
+//     operand instead of one and measured slower.)
 //   * O^T rows use the same permutation, so each lane finally holds 8 consecutive
 //     output columns and O is written with 16-byte stores at the block's original
 //     rows (the inverse permutation is fused into the store).
