@@ -16,9 +16,10 @@
 //                       instruction), 256 KV blocks per pass through a small LDS tile, so
 //                       that each K code row is read once per 16 query blocks; each of the 16
 //                       wavefronts collects one row's scores in registers, finds the k-th
-//                       largest by bisection over the integer range (lane counts by ballot and
-//                       popcount), keeps every larger score, the first equal scores in
-//                       ascending j up to k, and the diagonal if asked, and writes the row.
+//                       largest exactly by a radix select over 8-bit digits of the score minus
+//                       the row minimum (one 256-bin LDS histogram per wavefront and digit),
+//                       keeps every larger score, the first equal scores in ascending j up to
+//                       k, and the diagonal if asked, and writes the row.
 // Every step is exact or a single float32 rounding in a fixed order, so the mask is the same bit
 // for bit as a plain implementation of the same definition.
 
@@ -162,6 +163,8 @@ __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLau
   constexpr int NCH = JT * 64 / kChunk;           // passes over the KV blocks
   constexpr int CU = kChunk / 64;                 // entries per lane and pass
   __shared__ int32_t sc[ROWS][kChunk + 1];        // one pass's scores (+1: fewer bank conflicts)
+  __shared__ int32_t hist[kSelThreads / 64][256];  // one digit histogram per wavefront
+  __shared__ uint64_t rbits[kSelThreads / 64][JT];  // one row's kept bits per wavefront
   const int tiles = (a.mb + ROWS - 1) / ROWS;
   const int64_t bh = blockIdx.x / tiles;
   const int r0 = (int)(blockIdx.x % tiles) * ROWS;
@@ -230,7 +233,6 @@ __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLau
     if (w + 16 * g >= nr) break;
     const int i = r0 + w + 16 * g;
     const int32_t (&v_)[JT] = val[g];
-    // k-th largest value v: the largest v with #{s >= v} >= keep
     // (a score is at most 128 x 127 x 127 in magnitude, so INT32_MIN marks exactly the missing entries)
     int lo = INT32_MAX, hi = INT32_MIN;
 #pragma unroll
@@ -244,34 +246,124 @@ __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLau
     }
     lo = __builtin_amdgcn_readfirstlane(lo);
     hi = __builtin_amdgcn_readfirstlane(hi);
-    // invariant: #{s >= lo} >= keep (lo = the minimum counts every entry), #{s >= hi + 1} < keep
-    while (keep > 0 && lo < hi) {
-      const int mid = lo + (int)(((int64_t)hi - lo + 1) / 2);
-      int cnt = 0;  // (the missing entries, INT32_MIN, never reach mid)
+    // The keep-th largest score, digit by digit of u = s - lo (0 <= u <= hi - lo < 2^23): at each
+    // level the wavefront counts its candidates (entries whose higher digits equal the prefix found
+    // so far) in 256 bins of the next 8 bits, and the bin holding the kept-th largest candidate fixes
+    // those bits. Three levels resolve any row.
+    // thr: the keep-th largest score; ties: how many scores equal to thr are kept (the first ones in
+    // ascending j); neq: how many scores equal thr
+    int thr = lo, ties = keep, neq = mb;  // all scores equal when lo == hi
+    if (keep > 0 && lo < hi) {
+      int32_t* h = hist[w];
+      int nbits = 32 - __builtin_clz((uint32_t)(hi - lo));
+      uint32_t prefix = 0u;
+      int rem = keep;  // rank of the sought value among the candidates, from the top
+      while (nbits > 0) {
+        const int sh = nbits > 8 ? nbits - 8 : 0;
 #pragma unroll
-      for (int t = 0; t < JT; ++t) cnt += __popcll(__ballot(v_[t] >= mid));
-      if (cnt >= keep) lo = mid; else hi = mid - 1;
+        for (int b = 0; b < 4; ++b) h[4 * lane + b] = 0;
+        // (the wavefront's LDS operations complete in issue order; these fences keep that order)
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int t = 0; t < JT; ++t) {
+          // below the prefix u wraps past 2^nbits; a missing entry (INT32_MIN) lands near 2^31
+          const uint32_t u = (uint32_t)v_[t] - (uint32_t)lo - prefix;
+          if ((u >> nbits) == 0u) atomicAdd(&h[u >> sh], 1);
+        }
+        asm volatile("" ::: "memory");
+        int c[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) c[b] = h[4 * lane + b];
+        asm volatile("" ::: "memory");
+        // candidates in the bins above this lane's four: suffix sum over the lanes
+        const int tot = c[0] + c[1] + c[2] + c[3];
+        int acc = tot;  // inclusive suffix sum: this lane and the lanes above it
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int x = __shfl_down(acc, o);
+          if (lane + o < 64) acc += x;
+        }
+        const int above = acc - tot;
+        // bin 4 lane + b holds the rem-th largest candidate when above(b) < rem <= above(b) + c[b]
+        int hit = -1, hit_above = 0, hit_cnt = 0;
+        int ab = above;
+#pragma unroll
+        for (int b = 3; b >= 0; --b) {
+          if (hit < 0 && ab < rem && rem <= ab + c[b]) {
+            hit = 4 * lane + b;
+            hit_above = ab;
+            hit_cnt = c[b];
+          }
+          ab += c[b];
+        }
+        const uint64_t who = __ballot(hit >= 0);
+        const int src = (int)__builtin_ctzll(who);
+        const int bin = __builtin_amdgcn_readlane(hit, src);
+        rem -= __builtin_amdgcn_readlane(hit_above, src);
+        neq = __builtin_amdgcn_readlane(hit_cnt, src);  // at the last level (1-wide bins): the scores == thr
+        prefix += (uint32_t)bin << sh;
+        nbits = sh;
+      }
+      thr = lo + (int)prefix;
+      ties = rem;  // the larger scores are keep - rem
     }
-    const int v = lo;
-    int greater = 0;
+    // the row as bits, 64 blocks per word: word t = ballot of blocks 64 t .. 64 t + 63, kept by lane t
+    uint64_t myword = 0ull;
+    if (keep == 0 || ties == neq) {
+      // every score >= thr is kept (a missing entry, INT32_MIN, is below any score)
 #pragma unroll
-    for (int t = 0; t < JT; ++t) greater += __popcll(__ballot(v_[t] > v));
-    const int ties = keep - greater;  // equal scores to keep, in ascending j
+      for (int t = 0; t < JT; ++t) {  // (words past the row come out 0)
+        const uint64_t m = __ballot(keep > 0 && v_[t] >= thr);
+        if (lane == t) myword = m;
+      }
+    } else {
+      // only the first `ties` scores equal to thr, in ascending j
+      int seen = 0;
+#pragma unroll
+      for (int t = 0; t < JT; ++t) {
+        const uint64_t eqw = __ballot(v_[t] == thr);  // (past the row: INT32_MIN, never equal)
+        const int rank = seen + __popcll(eqw & below);
+        const uint64_t m = __ballot(v_[t] > thr || (v_[t] == thr && rank < ties));
+        if (lane == t) myword = m;
+        seen += __popcll(eqw);
+      }
+    }
+    if (a.diagonal && lane == (i >> 6)) myword |= 1ull << (i & 63);
+    const int nwords = (mb + 63) >> 6;
+    uint64_t* rw = rbits[w];
+    if (lane < nwords) rw[lane] = myword;
+    asm volatile("" ::: "memory");  // (LDS operations of a wavefront complete in issue order)
+    // Write the row's mb bytes: 16-byte stores of the 16-byte aligned chunks that lie inside the row,
+    // single bytes at its two ends (the neighbouring rows' bytes belong to other wavefronts).
     uint8_t* out = a.mask + ((int64_t)bh * mb + i) * mb;
-    int seen = 0;
-#pragma unroll
-    for (int t = 0; t < JT; ++t) {
-      if (64 * t >= mb) break;
-      const int j = 64 * t + lane;
-      const bool in = v_[t] != INT32_MIN;  // j < mb
-      const bool eq = in && keep > 0 && v_[t] == v;
-      const uint64_t eqw = __ballot(eq);
-      const int rank = seen + __popcll(eqw & below);
-      const bool kept = keep > 0 && in && (v_[t] > v || (eq && rank < ties));
-      const bool diag = a.diagonal && j == i;
-      if (in) out[j] = (kept || diag) ? 1 : 0;
-      seen += __popcll(eqw);
+    const int off0 = (int)((uintptr_t)out & 15);
+    uint8_t* g0 = out - off0;
+    const int span = off0 + mb;
+    for (int c = lane; 16 * c < span; c += 64) {
+      const int b0 = 16 * c;
+      if (b0 >= off0 && b0 + 16 <= span) {
+        const int p0 = b0 - off0;  // row position of the chunk's first byte
+        const int sh = p0 & 63;
+        uint64_t x = rw[p0 >> 6] >> sh;
+        if (sh > 48) x |= rw[(p0 >> 6) + 1] << (64 - sh);
+        const uint32_t bits = (uint32_t)x;
+        // 4 bits -> 4 bytes of 0 / 1: b * (1 + 2^7 + 2^14 + 2^21) puts bit e at bit 8 e (no carries)
+        uint4 v;
+        v.x = ((bits & 0xFu) * 0x204081u) & 0x01010101u;
+        v.y = (((bits >> 4) & 0xFu) * 0x204081u) & 0x01010101u;
+        v.z = (((bits >> 8) & 0xFu) * 0x204081u) & 0x01010101u;
+        v.w = (((bits >> 12) & 0xFu) * 0x204081u) & 0x01010101u;
+        *(uint4*)(g0 + b0) = v;
+      } else {
+        const int x0 = b0 > off0 ? b0 : off0;
+        const int x1 = b0 + 16 < span ? b0 + 16 : span;
+        for (int x = x0; x < x1; ++x) {
+          const int pos = x - off0;
+          g0[x] = (uint8_t)((rw[pos >> 6] >> (pos & 63)) & 1ull);
+        }
+      }
     }
+    asm volatile("" ::: "memory");  // the next row's words are written after these reads
   }
 }
 

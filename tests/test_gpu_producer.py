@@ -65,6 +65,24 @@ def test_producer_ties_and_zero_maximum():
     assert np.all(mask[..., :5] == 1) and not mask[..., 5:].any()
 
 
+@pytest.mark.parametrize("keep", [5, 30, 50, 64])
+def test_producer_partial_ties_at_the_threshold(keep):
+    """Every KV block repeats one of three token rows, so each row's scores take three values about 21
+    times each: the threshold score is tied and only some of its ties are kept (the first in j)."""
+    wl = custom("ties3", heads=2, head_dim=64, block=64, grid=(4, 32, 32), seed=22)
+    q, k, _ = make_qkv(wl)
+    rng = np.random.default_rng(22)
+    mb = wl.mb
+    for h in range(wl.heads):
+        pats = k[0, h, [0, 1, 2]].copy()
+        pick = rng.integers(0, 3, size=mb)
+        for j in range(mb):
+            k[0, h, j * wl.block:(j + 1) * wl.block] = pats[pick[j]]
+    mask, codes = _run(q, k, wl.block, keep, True)
+    assert np.array_equal(codes, _oracle_codes(q, k, wl.block))
+    assert np.array_equal(mask, MP.produce_mask(q, k, wl.block, keep, True))
+
+
 @pytest.mark.parametrize("mb,d,keep", [(1500, 128, 75), (4096, 64, 200), (257, 64, 9)])
 def test_producer_bit_exact_row_widths(mb, d, keep):
     """Heads of 1,500, 4,096 and 257 blocks (ragged last blocks): every width of the selection's
