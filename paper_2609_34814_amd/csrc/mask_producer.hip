@@ -1,25 +1,27 @@
 // Pooled-score top-k block mask for gfx950: a content-dependent producer of the block mask
 // (Sec. II-B: dynamic sparse attention predicts block relevance from pooled Q/K features).
 //
-//   pool_kernel         block means of Q and K: each thread folds 8 channels of one block over
-//                       its tokens in ascending order (IEEE float32, one rounding per addition,
-//                       16-byte loads), then one correctly rounded division by the token count,
-//                       and each block's maximum |mean| (as float bits: non-negative floats order
-//                       like their bit patterns);
-//   head_max_kernel     the per-head maximum over the block maxima (one workgroup per head and
-//                       tensor; a global atomic max per block instead serialised 2,841 updates on
-//                       each of 80 addresses and cost a quarter of the producer's time);
-//   quant_kernel        int8 codes rint(mean * fl32(127 / max)), clamped to [-127, 127];
-//   score_select_kernel one workgroup per 16 query blocks of a head: exact int32 scores
-//                       s_ij = sum_c qcode_i[c] kcode_j[c] with int8 MFMAs
-//                       (v_mfma_i32_16x16x64_i8: 16 KV blocks x the 16 query blocks per
-//                       instruction), 256 KV blocks per pass through a small LDS tile, so
-//                       that each K code row is read once per 16 query blocks; each of the 16
-//                       wavefronts collects one row's scores in registers, finds the k-th
-//                       largest exactly by a radix select over 8-bit digits of the score minus
-//                       the row minimum (one 256-bin LDS histogram per wavefront and digit),
-//                       keeps every larger score, the first equal scores in ascending j up to
-//                       k, and the diagonal if asked, and writes the row.
+// Three roles of one kernel, each taken by whole workgroups of 16 wavefronts:
+//   pooling     block means of Q and K: each thread folds 8 channels of one block over its
+//               tokens in ascending order (IEEE float32, one rounding per addition, 16-byte
+//               loads), then one correctly rounded division by the token count, and each
+//               block's maximum |mean| (as float bits: non-negative floats order like their bit
+//               patterns);
+//   codes       one workgroup per head and tensor: the head's maximum over its block maxima,
+//               then int8 codes rint(mean * fl32(127 / max)), clamped to [-127, 127];
+//   selection   one workgroup per 32 query blocks of a head (16 for rows of more than 3,072
+//               blocks): exact int32 scores s_ij = sum_c qcode_i[c] kcode_j[c] with int8 MFMAs
+//               (v_mfma_i32_16x16x64_i8: 16 KV blocks x 16 query blocks per instruction),
+//               256 KV blocks per pass through a small LDS tile, so that each K code row is
+//               read once per 16 query blocks; each wavefront collects one row's scores in
+//               registers, finds the k-th largest exactly by a radix select over 8-bit digits
+//               of the score minus the row minimum (one 256-bin LDS histogram per wavefront and
+//               digit), keeps every larger score, the first equal scores in ascending j up to
+//               k, and the diagonal if asked, and writes the row.
+// The heads are taken in groups of about 12,000 query blocks, and launch k runs the pooling of
+// group k, the codes of group k - 1 and the selection of group k - 2, so that the memory-bound
+// pooling of one group overlaps the compute-bound selection of another; no workgroup waits for
+// another within a launch.
 // Every step is exact or a single float32 rounding in a fixed order, so the mask is the same bit
 // for bit as a plain implementation of the same definition.
 
@@ -31,45 +33,25 @@
 
 namespace {
 
-constexpr int kPoolThreads = 128;  // (256 took 4% longer: fewer, larger workgroups per CU)
 constexpr int kSelThreads = 1024;  // 16 wavefronts: one 16-KV-block tile each, then one row each
 constexpr int kChunk = 256;        // KV blocks scored per pass (16 wavefronts x 16)
-
-// amax[which][bh] = max over the head's blocks of bmax[which][bh][j]; one workgroup per (which, bh)
-__global__ __launch_bounds__(256) void head_max_kernel(WaProducerLaunch a) {
-  __shared__ uint32_t part[4];
-  const int64_t wh = blockIdx.x;  // which * bh + bh
-  const uint32_t* b = a.bmax + wh * a.mb;
-  uint32_t mx = 0u;
-  for (int j = threadIdx.x; j < a.mb; j += 256) mx = b[j] > mx ? b[j] : mx;
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t u = __shfl_xor(mx, o);
-    mx = u > mx ? u : mx;
-  }
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = mx;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t m = part[0];
-    for (int w = 1; w < 4; ++w) m = part[w] > m ? part[w] : m;
-    a.amax[wh] = m;
-  }
-}
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// grid.x covers bh * mb * (D / 8) threads; grid.y = 0 for Q, 1 for K. The D / 8 threads of one
-// block are consecutive lanes of one wavefront.
+// Pooling role of workgroup wg: threads wg * kSelThreads + tid cover Q, then K, of heads
+// [h0, h0 + nh), D / 8 consecutive threads (lanes of one wavefront) per block.
 template <int D>
-__global__ __launch_bounds__(kPoolThreads) void pool_kernel(WaProducerLaunch a) {
+__device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int nh, int64_t wg) {
   constexpr int G = D / 8;  // 8-channel groups per block
-  const int which = blockIdx.y;
+  const int64_t per = (int64_t)nh * a.mb * G;
+  const int64_t gid = wg * kSelThreads + threadIdx.x;
+  const bool active = gid < 2 * per;
+  const int which = gid < per ? 0 : 1;
   const uint16_t* x = (const uint16_t*)(which ? a.k : a.q);
-  const int64_t gid = (int64_t)blockIdx.x * kPoolThreads + threadIdx.x;
-  const int64_t total = (int64_t)a.bh * a.mb * G;
-  const bool active = gid < total;
-  const int g = (int)(gid % G);
-  const int64_t bj = gid / G;  // bh * mb + j
+  const int64_t rem = gid - which * per;
+  const int g = (int)(rem % G);
+  const int64_t bj = (int64_t)h0 * a.mb + rem / G;  // bh * mb + j
   uint32_t mx = 0u;
   if (active) {
     const int j = (int)(bj % a.mb);
@@ -80,9 +62,13 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(WaProducerLaunch a) 
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     int t = 0;
     for (; t + 8 <= cnt; t += 8) {
+      typedef unsigned nt4 __attribute__((ext_vector_type(4)));
       uint4 v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = *(const uint4*)(p + (int64_t)(t + u) * D);
+      for (int u = 0; u < 8; ++u) {  // read once: streaming loads
+        const nt4 x = __builtin_nontemporal_load((const nt4*)(p + (int64_t)(t + u) * D));
+        v[u] = make_uint4(x[0], x[1], x[2], x[3]);
+      }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         acc[0] += bf16_lo(v[u].x);
@@ -125,23 +111,43 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(WaProducerLaunch a) 
   if (active && g == 0) a.bmax[(int64_t)which * a.bh * a.mb + bj] = mx;
 }
 
-// codes[which][bh][mb][D] = rint(mean * fl32(127 / max)) clamped, 0 when max = 0
+// Codes role of one workgroup: head bh of Q (which = 0) or K (which = 1): the head's maximum block
+// maximum, then codes rint(mean * fl32(127 / max)) clamped to [-127, 127], 0 when max = 0.
 template <int D>
-__global__ __launch_bounds__(256) void quant_kernel(WaProducerLaunch a) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t per = (int64_t)a.bh * a.mb * D;
-  if (i >= 2 * per) return;
-  const int64_t which = i / per;
-  const int64_t bh = (i % per) / ((int64_t)a.mb * D);
-  const float mx = __uint_as_float(a.amax[which * a.bh + bh]);
-  int8_t code = 0;
-  if (mx > 0.f) {
-    const float inv = 127.0f / mx;
-    float r = __builtin_rintf(a.means[i] * inv);
-    r = fminf(fmaxf(r, -127.f), 127.f);
-    code = (int8_t)(int)r;
+__device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which, int64_t bh, uint32_t* part) {
+  const int64_t wh = which * (int64_t)a.bh + bh;
+  const uint32_t* b = a.bmax + wh * a.mb;
+  const int tid = threadIdx.x;
+  uint32_t mx = 0u;
+  for (int j = tid; j < a.mb; j += kSelThreads) mx = b[j] > mx ? b[j] : mx;
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t u = __shfl_xor(mx, o);
+    mx = u > mx ? u : mx;
   }
-  a.codes[i] = code;
+  if ((tid & 63) == 0) part[tid >> 6] = mx;
+  __syncthreads();
+  uint32_t m = part[0];
+  for (int w = 1; w < kSelThreads / 64; ++w) m = part[w] > m ? part[w] : m;
+  if (tid == 0) a.amax[wh] = m;
+  const float fmx = __uint_as_float(m);
+  const float inv = fmx > 0.f ? 127.0f / fmx : 0.f;
+  const float4* src = (const float4*)(a.means + wh * a.mb * D);
+  uint32_t* dst = (uint32_t*)(a.codes + wh * a.mb * D);
+  const int n4 = a.mb * D / 4;
+  for (int e = tid; e < n4; e += kSelThreads) {
+    const float4 v = src[e];
+    uint32_t word = 0u;
+    if (fmx > 0.f) {
+      const float c[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float r = __builtin_rintf(c[q] * inv);
+        r = fminf(fmaxf(r, -127.f), 127.f);
+        word |= (uint32_t)(uint8_t)(int8_t)(int)r << (8 * q);
+      }
+    }
+    dst[e] = word;
+  }
 }
 
 // Query blocks per score_select workgroup: RG groups of 16 (the MFMA's 16 columns), two when the
@@ -152,22 +158,25 @@ struct SelGeom {
   static constexpr int ROWS = 16 * RG;
 };
 
-// One workgroup: query blocks [r0, r0 + ROWS) of head bh. JT (a multiple of kChunk / 64 with
-// 64 JT >= mb) is the number of scores of one row each lane holds.
+// LDS of the selection role
+template <int JT>
+struct SelLds {
+  int32_t sc[SelGeom<JT>::ROWS][kChunk + 1];  // one pass's scores (+1: fewer bank conflicts)
+  int32_t hist[kSelThreads / 64][256];        // one digit histogram per wavefront
+  uint64_t rbits[kSelThreads / 64][JT];       // one row's kept bits per wavefront
+};
+
+// Selection role of one workgroup: query blocks [r0, r0 + ROWS) of head bh. JT (a multiple of
+// kChunk / 64 with 64 JT >= mb) is the number of scores of one row each lane holds.
 template <int D, int JT>
-__global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLaunch a) {
+__device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t bh, int r0, SelLds<JT>& L) {
   typedef int v4i __attribute__((ext_vector_type(4)));
   constexpr int RG = SelGeom<JT>::RG;
   constexpr int ROWS = SelGeom<JT>::ROWS;
   constexpr int KS = D / 64;                      // 64-channel steps of one MFMA each
   constexpr int NCH = JT * 64 / kChunk;           // passes over the KV blocks
   constexpr int CU = kChunk / 64;                 // entries per lane and pass
-  __shared__ int32_t sc[ROWS][kChunk + 1];        // one pass's scores (+1: fewer bank conflicts)
-  __shared__ int32_t hist[kSelThreads / 64][256];  // one digit histogram per wavefront
-  __shared__ uint64_t rbits[kSelThreads / 64][JT];  // one row's kept bits per wavefront
-  const int tiles = (a.mb + ROWS - 1) / ROWS;
-  const int64_t bh = blockIdx.x / tiles;
-  const int r0 = (int)(blockIdx.x % tiles) * ROWS;
+  int32_t (&sc)[ROWS][kChunk + 1] = L.sc;
   const int nr = min(ROWS, a.mb - r0);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -254,7 +263,7 @@ __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLau
     // ascending j); neq: how many scores equal thr
     int thr = lo, ties = keep, neq = mb;  // all scores equal when lo == hi
     if (keep > 0 && lo < hi) {
-      int32_t* h = hist[w];
+      int32_t* h = L.hist[w];
       int nbits = 32 - __builtin_clz((uint32_t)(hi - lo));
       uint32_t prefix = 0u;
       int rem = keep;  // rank of the sought value among the candidates, from the top
@@ -330,7 +339,7 @@ __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLau
     }
     if (a.diagonal && lane == (i >> 6)) myword |= 1ull << (i & 63);
     const int nwords = (mb + 63) >> 6;
-    uint64_t* rw = rbits[w];
+    uint64_t* rw = L.rbits[w];
     if (lane < nwords) rw[lane] = myword;
     asm volatile("" ::: "memory");  // (LDS operations of a wavefront complete in issue order)
     // Write the row's mb bytes: 16-byte stores of the 16-byte aligned chunks that lie inside the row,
@@ -367,36 +376,79 @@ __global__ __launch_bounds__(kSelThreads) void score_select_kernel(WaProducerLau
   }
 }
 
+// One step of the producer's pipeline over head groups: the codes of group k - 1 and the pooling
+// of group k on some workgroups, the selection of group k - 2 on others, in one launch with no
+// dependence between its workgroups. Roles by workgroup index: the first 2 code_nh take the codes,
+// then selection and pooling workgroups alternate in proportion to their counts, so that the
+// memory-bound pooling and the compute-bound selection share the compute units.
+struct ProducerStep {
+  int32_t pool_h0, pool_nh, code_h0, code_nh, sel_h0, sel_nh;
+  int64_t pool_wgs, sel_wgs;
+};
+
 template <int D, int JT>
-hipError_t launch_select_t(const WaProducerLaunch& a, hipStream_t stream) {
-  const dim3 grid((unsigned)(a.bh * ((a.mb + SelGeom<JT>::ROWS - 1) / SelGeom<JT>::ROWS)));
-  hipLaunchKernelGGL((score_select_kernel<D, JT>), grid, dim3(kSelThreads), 0, stream, a);
-  return hipGetLastError();
+__global__ __launch_bounds__(kSelThreads) void producer_step_kernel(WaProducerLaunch a, ProducerStep st) {
+  __shared__ SelLds<JT> lds;
+  const int64_t idx = blockIdx.x;
+  if (idx < 2 * st.code_nh) {
+    codes_role<D>(a, (int)(idx / st.code_nh), st.code_h0 + idx % st.code_nh, (uint32_t*)lds.hist);
+    return;
+  }
+  const int64_t k = idx - 2 * st.code_nh;
+  const int64_t S = st.sel_wgs, T = st.sel_wgs + st.pool_wgs;
+  const int64_t s_before = k * S / T, s_after = (k + 1) * S / T;
+  if (s_after > s_before) {
+    const int tiles = (a.mb + SelGeom<JT>::ROWS - 1) / SelGeom<JT>::ROWS;
+    select_role<D, JT>(a, st.sel_h0 + s_before / tiles, (int)(s_before % tiles) * SelGeom<JT>::ROWS, lds);
+  } else {
+    pool_role<D>(a, st.pool_h0, st.pool_nh, k - s_before);
+  }
 }
 
-template <int D>
-hipError_t launch_select(const WaProducerLaunch& a, hipStream_t stream) {
-  const int jt = (a.mb + kChunk - 1) / kChunk * (kChunk / 64);  // scores per lane, whole passes
-  if (jt <= 16) return launch_select_t<D, 16>(a, stream);
-  if (jt <= 32) return launch_select_t<D, 32>(a, stream);
-  if (jt <= 48) return launch_select_t<D, 48>(a, stream);
-  return launch_select_t<D, WA_MAX_BLOCKS / 64>(a, stream);
+// Query blocks per head group: about 12,000 (four heads of 2,841 blocks). Smaller groups leave
+// too little pooling to overlap a selection with (two heads: +12% call time), larger ones lengthen
+// the launches at both ends of the pipeline, which do not overlap (ten heads: +4%).
+constexpr int kGroupBlocks = 12000;
+
+template <int D, int JT>
+hipError_t launch_all_t(const WaProducerLaunch& a, hipStream_t stream) {
+  const int per_blocks = (kGroupBlocks + a.mb / 2) / a.mb;
+  const int per = per_blocks < 1 ? 1 : (per_blocks > a.bh ? a.bh : per_blocks);
+  const int ng = (a.bh + per - 1) / per;
+  const int tiles = (a.mb + SelGeom<JT>::ROWS - 1) / SelGeom<JT>::ROWS;
+  auto first = [&](int g) { return g * per; };
+  auto count = [&](int g) { return a.bh - g * per < per ? a.bh - g * per : per; };
+  for (int k = 0; k < ng + 2; ++k) {
+    ProducerStep st{};
+    if (k < ng) {
+      st.pool_h0 = first(k);
+      st.pool_nh = count(k);
+      st.pool_wgs = (2ll * st.pool_nh * a.mb * (D / 8) + kSelThreads - 1) / kSelThreads;
+    }
+    if (k >= 1 && k - 1 < ng) {
+      st.code_h0 = first(k - 1);
+      st.code_nh = count(k - 1);
+    }
+    if (k >= 2) {
+      st.sel_h0 = first(k - 2);
+      st.sel_nh = count(k - 2);
+      st.sel_wgs = (int64_t)st.sel_nh * tiles;
+    }
+    const int64_t grid = 2ll * st.code_nh + st.sel_wgs + st.pool_wgs;
+    hipLaunchKernelGGL((producer_step_kernel<D, JT>), dim3((unsigned)grid), dim3(kSelThreads), 0, stream, a, st);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 template <int D>
 hipError_t launch_all(const WaProducerLaunch& a, hipStream_t stream) {
-  const int64_t pool_threads = (int64_t)a.bh * a.mb * (D / 8);
-  const dim3 pgrid((unsigned)((pool_threads + kPoolThreads - 1) / kPoolThreads), 2);
-  const int64_t qn = 2ll * a.bh * a.mb * D;
-  const dim3 qgrid((unsigned)((qn + 255) / 256));
-  hipError_t e;
-  hipLaunchKernelGGL(pool_kernel<D>, pgrid, dim3(kPoolThreads), 0, stream, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(head_max_kernel, dim3((unsigned)(2 * a.bh)), dim3(256), 0, stream, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(quant_kernel<D>, qgrid, dim3(256), 0, stream, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  return launch_select<D>(a, stream);
+  const int jt = (a.mb + kChunk - 1) / kChunk * (kChunk / 64);  // scores per lane, whole passes
+  if (jt <= 16) return launch_all_t<D, 16>(a, stream);
+  if (jt <= 32) return launch_all_t<D, 32>(a, stream);
+  if (jt <= 48) return launch_all_t<D, 48>(a, stream);
+  return launch_all_t<D, WA_MAX_BLOCKS / 64>(a, stream);
 }
 
 }  // namespace
