@@ -220,6 +220,43 @@ __device__ __forceinline__ void for_bits(const uint64_t* words, int nwords, int6
   }
 }
 
+// Threads that share one column (or row) in the one-workgroup form: the largest power of two up to
+// 16 with threads * lines <= NT. They are consecutive lanes of one wavefront, and each takes a
+// contiguous chunk of the line's bit range (or of the compared elements).
+__device__ __forceinline__ int lanes_per_line(int lines) {
+  int t = 1;
+  while (t < 16 && 2 * t * lines <= NT) t *= 2;
+  return t;
+}
+
+// Sum of an int64 over groups of t consecutive lanes (t a power of two up to 64); every lane of a
+// group receives its group's sum.
+__device__ __forceinline__ int64_t group_sum(int64_t v, int t) {
+  for (int o = 1; o < t; o <<= 1) {
+    const int lo = __shfl_xor((int)(uint32_t)(uint64_t)v, o);
+    const int hi = __shfl_xor((int)(uint32_t)((uint64_t)v >> 32), o);
+    v += (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+  }
+  return v;
+}
+
+// Calls f(k) for every set bit k in [b0, b1) of a word-major bitmask line.
+template <typename F>
+__device__ __forceinline__ void for_bits_range(const uint64_t* words, int64_t stride, int line, int b0, int b1,
+                                               F&& f) {
+  if (b0 >= b1) return;
+  for (int w = b0 >> 6; w <= (b1 - 1) >> 6; ++w) {
+    uint64_t word = words[(int64_t)w * stride + line];
+    const int base = w * 64;
+    if (b0 > base) word &= ~0ull << (b0 - base);
+    if (b1 - base < 64) word &= (1ull << (b1 - base)) - 1ull;
+    while (word) {
+      f(base + __ffsll((long long)word) - 1);
+      word &= word - 1;
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------------------------
 // Centred products across many workgroups. One subspace step X -> Z = m * M~ Ys, with
 // Ys = (m * M~^T X) >> sy, runs as two slice kernels (one 256-thread workgroup per 256-column
@@ -233,6 +270,9 @@ __device__ __forceinline__ void for_bits(const uint64_t* words, int nwords, int6
 // does not change any result.
 constexpr int GT = 256;
 constexpr int GW = GT / 64;
+// Heads of at most this many rows are ordered by rank sorts (no barriers), larger ones by bitonic
+// sorts.
+constexpr int kRankSortMax = 512;
 
 __global__ __launch_bounds__(GT) void apply_gather_kernel(WaPermLaunch a) {
   const int h = blockIdx.x / a.slices, s = blockIdx.x % a.slices;
@@ -707,9 +747,21 @@ __device__ void finish_head(const WaPermLaunch& a, Shared& sh, int h, bool degen
   int P = 1;
   while (P < m) P <<= 1;
   int32_t* idx = sh.ys;
-  for (int i = tid; i < P; i += NT) idx[i] = i < m ? i : -1;
-  __syncthreads();
-  if (!degen) {
+  if (m <= kRankSortMax) {
+    // rank sort: a row's position is the number of rows that precede it (a total order)
+    const int t = lanes_per_line(m);
+    const int line = tid / t, sub = tid % t;
+    int64_t r = 0;
+    if (line < m && !degen)
+      for (int j = sub; j < m; j += t) r += angle_less(sh, j, line) ? 1 : 0;
+    r = group_sum(r, t);
+    if (line < m && sub == 0) idx[degen ? line : (int)r] = line;  // degenerate: the identity
+    __syncthreads();
+  } else {
+    for (int i = tid; i < P; i += NT) idx[i] = i < m ? i : -1;
+    __syncthreads();
+  }
+  if (!degen && m > kRankSortMax) {
     for (int k = 2; k <= P; k <<= 1)
       for (int j = k >> 1; j > 0; j >>= 1) {
         for (int t = tid; t < P / 2; t += NT) {
@@ -748,22 +800,36 @@ __device__ void finish_head(const WaPermLaunch& a, Shared& sh, int h, bool degen
     keys[p] = (bucket << 32) | ((0xFFFFull - nz) << 16) | (uint64_t)p;
   }
   __syncthreads();
-  for (int k = 2; k <= P; k <<= 1)
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int t = tid; t < P / 2; t += NT) {
-        const int i = (t / j) * 2 * j + (t % j);
-        const int p = i + j;
-        const uint64_t x = keys[i], y = keys[p];
-        const bool up = (i & k) == 0;
-        if (up ? (y < x) : (x < y)) {
-          keys[i] = y;
-          keys[p] = x;
-        }
-      }
-      __syncthreads();
-    }
   int32_t* fin = sh.xs;  // the built order (the segment map is no longer needed)
-  for (int s = tid; s < m; s += NT) fin[s] = sh.cc[(int)(keys[s] & 0xFFFFull)];
+  if (m <= kRankSortMax) {
+    // rank sort of the (distinct) keys
+    const int t = lanes_per_line(m);
+    const int line = tid / t, sub = tid % t;
+    int64_t r = 0;
+    if (line < m) {
+      const uint64_t kp = keys[line];
+      for (int q = sub; q < m; q += t) r += keys[q] < kp ? 1 : 0;
+    }
+    r = group_sum(r, t);
+    __syncthreads();  // every key is read before the order overwrites the segment map
+    if (line < m && sub == 0) fin[(int)r] = sh.cc[line];
+  } else {
+    for (int k = 2; k <= P; k <<= 1)
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        for (int t = tid; t < P / 2; t += NT) {
+          const int i = (t / j) * 2 * j + (t % j);
+          const int p = i + j;
+          const uint64_t x = keys[i], y = keys[p];
+          const bool up = (i & k) == 0;
+          if (up ? (y < x) : (x < y)) {
+            keys[i] = y;
+            keys[p] = x;
+          }
+        }
+        __syncthreads();
+      }
+    for (int s = tid; s < m; s += NT) fin[s] = sh.cc[(int)(keys[s] & 0xFFFFull)];
+  }
   __syncthreads();
   for (int s = tid; s < m; s += NT) perm[s] = fin[s];
 
@@ -806,70 +872,79 @@ __global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
 }
 
 // The whole permutation of a head in one workgroup, for heads too small to fill the chip with column
-// slices: the same exact integer products as the slice kernels (so the same result), with Ym kept
-// in registers and M Ys scattered into LDS, and X kept in LDS between the steps.
+// slices: the same exact integer products as the slice kernels (so the same result), with X kept in
+// LDS between the steps.
 //   apply: Z = m * M~ Ys, Ys = (m * M~^T X) >> sy, for X in sh.xs; maxy = max |m * M~^T X|.
-//   colbits: the head's column bitmask (held in LDS by the caller); cc: its column counts.
+// Both products are gathers: Ym over each column's rows (column bitmask, held in LDS by the caller),
+// then Z over each row's columns (row bitmask, in LDS when it fits) from Ys in LDS, each line shared
+// by lanes_per_line lanes; no atomics, and every sum is an exact integer. c_line: the column count
+// of the lane's column.
 __device__ void apply_head(const WaPermLaunch& a, Shared& sh, unsigned long long* za, const uint64_t* colbits,
-                           const int32_t (&cc)[PER], int64_t (&zr)[PER][2], uint64_t& maxy) {
+                           const uint64_t* rowbits, int64_t c_line, int64_t (&zr)[PER][2], uint64_t& maxy) {
   const int tid = threadIdx.x;
-  const int m = a.m, n = a.n, mw = (m + 63) / 64;
+  const int m = a.m, n = a.n;
+  const int t = lanes_per_line(m > n ? m : n);
+  const int line = tid / t, sub = tid % t;
   int64_t sx[2] = {0, 0};
   for (int i = tid; i < m; i += NT) {
     sx[0] += sh.xs[2 * i];
     sx[1] += sh.xs[2 * i + 1];
   }
   block_sum<2>(sh, sx);
-  int64_t ym[PER][2];
+  // Ym of column `line`: its rows in this lane's chunk, then the group's sum
+  const int rc = (m + t - 1) / t;
+  int64_t y0 = 0, y1 = 0;
+  if (line < n)
+    for_bits_range(colbits, n, line, min(sub * rc, m), min(sub * rc + rc, m), [&](int i) {
+      y0 += sh.xs[2 * i];
+      y1 += sh.xs[2 * i + 1];
+    });
+  y0 = group_sum(y0, t);
+  y1 = group_sum(y1, t);
+  int64_t ym0 = 0, ym1 = 0;
+  const int64_t c = c_line;
   uint64_t mx = 0;
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int j = tid + k * NT;
-    ym[k][0] = 0;
-    ym[k][1] = 0;
-    if (j < n) {
-      int64_t y0 = 0, y1 = 0;
-      for_bits(colbits, mw, n, j, [&](int i) {
-        y0 += sh.xs[2 * i];
-        y1 += sh.xs[2 * i + 1];
-      });
-      const int64_t c = cc[k];
-      ym[k][0] = (int64_t)m * y0 - c * sx[0];
-      ym[k][1] = (int64_t)m * y1 - c * sx[1];
-      const uint64_t p = uabs64(ym[k][0]), q = uabs64(ym[k][1]);
-      mx = p > mx ? p : mx;
-      mx = q > mx ? q : mx;
-    }
+  if (line < n) {
+    ym0 = (int64_t)m * y0 - c * sx[0];
+    ym1 = (int64_t)m * y1 - c * sx[1];
+    const uint64_t p = uabs64(ym0), q = uabs64(ym1);
+    mx = p > q ? p : q;
   }
   maxy = block_max(sh, mx);
   const int bl = bitlen_u64(maxy);
   const int sy = bl > 30 ? bl - 30 : 0;
-  for (int i = tid; i < 2 * m; i += NT) za[i] = 0ull;
-  __syncthreads();
+  int32_t* ysh = sh.ys;  // Ys (the sort scratch is free during the steps)
   int64_t py[2] = {0, 0};
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int j = tid + k * NT;
-    if (j < n) {
-      const int32_t y0 = (int32_t)(ym[k][0] >> sy), y1 = (int32_t)(ym[k][1] >> sy);
-      const int64_t c = cc[k];
-      py[0] += c * y0;
-      py[1] += c * y1;
-      const unsigned long long u0 = (unsigned long long)(int64_t)y0, u1 = (unsigned long long)(int64_t)y1;
-      for_bits(colbits, mw, n, j, [&](int i) {
-        atomicAdd(&za[2 * i], u0);
-        atomicAdd(&za[2 * i + 1], u1);
-      });
-    }
+  if (line < n && sub == 0) {
+    const int32_t v0 = (int32_t)(ym0 >> sy), v1 = (int32_t)(ym1 >> sy);
+    ysh[2 * line] = v0;
+    ysh[2 * line + 1] = v1;
+    py[0] = c * v0;
+    py[1] = c * v1;
   }
-  block_sum<2>(sh, py);  // its barriers also complete the scatter
+  block_sum<2>(sh, py);  // its barriers also publish Ys
+  // (M Ys) of row `line`
+  const int cr = (n + t - 1) / t;
+  int64_t z0 = 0, z1 = 0;
+  if (line < m)
+    for_bits_range(rowbits, m, line, min(sub * cr, n), min(sub * cr + cr, n), [&](int j) {
+      z0 += ysh[2 * j];
+      z1 += ysh[2 * j + 1];
+    });
+  z0 = group_sum(z0, t);
+  z1 = group_sum(z1, t);
+  if (line < m && sub == 0) {
+    za[2 * line] = (unsigned long long)z0;
+    za[2 * line + 1] = (unsigned long long)z1;
+  }
+  __syncthreads();
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int i = tid + k * NT;
     zr[k][0] = i < m ? (int64_t)m * (int64_t)za[2 * i] - py[0] : 0;
     zr[k][1] = i < m ? (int64_t)m * (int64_t)za[2 * i + 1] - py[1] : 0;
   }
-  __syncthreads();  // every thread has read za before the next step clears it
+  __syncthreads();  // every thread has read za before the next step writes it
 }
 
 __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
@@ -877,6 +952,7 @@ __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
   Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
   unsigned long long* za = reinterpret_cast<unsigned long long*>(smem_raw + sizeof(Shared));  // [2 m]
   uint64_t* cb = reinterpret_cast<uint64_t*>(za + 2 * a.m);  // the head's column bitmask [mw][n]
+  uint64_t* rbl = cb + (size_t)((a.m + 63) / 64) * a.n;     // its row bitmask [nw][m], if a.rows_in_lds
   const int h = blockIdx.x;
   const HeadInit hi = init_head(a, sh, h);
   if (hi.status == HEAD_DONE) return;
@@ -886,15 +962,16 @@ __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
   if (!degen) {
     const Head H = head_of(a, h);
     for (int t = threadIdx.x; t < H.mw * a.n; t += NT) cb[t] = H.colbits[t];
-    int32_t cc[PER];
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int j = threadIdx.x + k * NT;
-      cc[k] = j < a.n ? a.cc[(int64_t)h * a.n + j] : 0;
+    const uint64_t* rows = H.rowbits;
+    if (a.rows_in_lds) {
+      for (int t = threadIdx.x; t < H.nw * a.m; t += NT) rbl[t] = H.rowbits[t];
+      rows = rbl;
     }
+    const int line = threadIdx.x / lanes_per_line(a.m > a.n ? a.m : a.n);
+    const int64_t c_line = line < a.n ? a.cc[(int64_t)h * a.n + line] : 0;
     __syncthreads();
     for (int it = 0; it <= a.iters; ++it) {
-      apply_head(a, sh, za, cb, cc, zr, maxy);
+      apply_head(a, sh, za, cb, rows, c_line, zr, maxy);
       if (it < a.iters && orth(sh, H, zr)) {
         degen = true;
         break;
@@ -924,8 +1001,8 @@ size_t wa_perm_shared_bytes() { return sizeof(Shared); }
 int wa_perm_slices(int n) { return (n + GT - 1) / GT; }
 
 // Heads of at most this many 256-column slices run as one workgroup each (perm_fused_kernel), which
-// replaces the 3 + 3 T launches of the slice kernels (0.21 -> 0.18 ms for 2 heads of 64 blocks,
-// 0.34 -> 0.28 ms for 12 heads of 256); from three slices on, the slices' parallelism wins.
+// replaces the 3 + 3 T launches of the slice kernels (0.21 -> 0.14 ms for 2 heads of 64 blocks,
+// 0.34 -> 0.27 ms for 12 heads of 256); from three slices on, the slices' parallelism wins.
 #ifndef WA_PERM_FUSED_MAX_SLICES
 #define WA_PERM_FUSED_MAX_SLICES 2
 #endif
@@ -947,12 +1024,16 @@ hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   hipError_t e = hipFuncSetAttribute((const void*)apply_scatter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)zsmem);
   if (e != hipSuccess) return e;
-  const size_t fsmem = smem + (size_t)2 * a.m * sizeof(unsigned long long) +
-                       (size_t)((a.m + 63) / 64) * a.n * sizeof(uint64_t);
+  size_t fsmem = smem + (size_t)2 * a.m * sizeof(unsigned long long) +
+                 (size_t)((a.m + 63) / 64) * a.n * sizeof(uint64_t);
   if (!a.stats_only && a.slices <= kFusedMaxSlices && fsmem <= kLdsBytes) {
+    WaPermLaunch f = a;
+    const size_t rows = (size_t)((a.n + 63) / 64) * a.m * sizeof(uint64_t);
+    f.rows_in_lds = fsmem + rows <= kLdsBytes ? 1 : 0;  // the row bitmask too, when it fits
+    if (f.rows_in_lds) fsmem += rows;
     e = hipFuncSetAttribute((const void*)perm_fused_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fsmem);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(perm_fused_kernel, dim3(a.bh), dim3(NT), fsmem, stream, a);
+    hipLaunchKernelGGL(perm_fused_kernel, dim3(a.bh), dim3(NT), fsmem, stream, f);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(perm_init_kernel, dim3(a.bh), dim3(NT), smem, stream, a);
