@@ -95,6 +95,17 @@ def test_producer_bit_exact_row_widths(mb, d, keep):
     assert np.array_equal(mask, MP.produce_mask(q, k, wl.block, keep, True))
 
 
+def test_producer_bit_exact_head_groups():
+    """Two sequences of seven heads of 1,500 blocks: the pipeline takes heads in groups of eight, so
+    the launches see a full group, a short last group, and heads of both sequences in one group."""
+    wl = custom("groups", batch=2, heads=7, head_dim=64, block=64, grid=(1500, 8, 8), seq_len=1500 * 64 - 17,
+                seed=31)
+    q, k, _ = make_qkv(wl)
+    mask, codes = _run(q, k, wl.block, 60, True)
+    assert np.array_equal(codes, _oracle_codes(q, k, wl.block))
+    assert np.array_equal(mask, MP.produce_mask(q, k, wl.block, 60, True))
+
+
 def test_producer_bit_exact_full_size():
     """363,600 tokens, 40 heads, 5% of the blocks per row: every row of every head."""
     wl = PRODUCER_CONFIGS["produced-long-720p-401f"]
