@@ -270,9 +270,10 @@ __device__ __forceinline__ void for_bits_range(const uint64_t* words, int64_t st
 // does not change any result.
 constexpr int GT = 256;
 constexpr int GW = GT / 64;
-// Heads of at most this many rows are ordered by rank sorts (no barriers), larger ones by bitonic
-// sorts.
-constexpr int kRankSortMax = 512;
+// Heads of at most this many rows are ordered by rank sorts (no barriers; four or more lanes per
+// row), larger ones by bitonic sorts (at 394 rows the rank sort's m^2 / 2 compares per lane cost
+// more than the bitonic stages).
+constexpr int kRankSortMax = 256;
 
 __global__ __launch_bounds__(GT) void apply_gather_kernel(WaPermLaunch a) {
   const int h = blockIdx.x / a.slices, s = blockIdx.x % a.slices;
@@ -875,16 +876,18 @@ __global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
 // slices: the same exact integer products as the slice kernels (so the same result), with X kept in
 // LDS between the steps.
 //   apply: Z = m * M~ Ys, Ys = (m * M~^T X) >> sy, for X in sh.xs; maxy = max |m * M~^T X|.
-// Both products are gathers: Ym over each column's rows (column bitmask, held in LDS by the caller),
-// then Z over each row's columns (row bitmask, in LDS when it fits) from Ys in LDS, each line shared
-// by lanes_per_line lanes; no atomics, and every sum is an exact integer. c_line: the column count
-// of the lane's column.
+// Both products walk the column bitmask (held in LDS by the caller), lanes_per_line lanes per column:
+// Ym gathers the column's rows, then M Ys scatters Ys[j] into the column's rows with 64-bit LDS
+// atomics. Walking columns keeps the lanes balanced (row counts are heavy-tailed, column counts are
+// not), and every sum is an exact integer. c_line: the column count of the lane's column.
 __device__ void apply_head(const WaPermLaunch& a, Shared& sh, unsigned long long* za, const uint64_t* colbits,
-                           const uint64_t* rowbits, int64_t c_line, int64_t (&zr)[PER][2], uint64_t& maxy) {
+                           int64_t c_line, int64_t (&zr)[PER][2], uint64_t& maxy) {
   const int tid = threadIdx.x;
   const int m = a.m, n = a.n;
-  const int t = lanes_per_line(m > n ? m : n);
+  const int t = lanes_per_line(n);
   const int line = tid / t, sub = tid % t;
+  const int rc = (m + t - 1) / t;
+  const int r0 = min(sub * rc, m), r1 = min(sub * rc + rc, m);
   int64_t sx[2] = {0, 0};
   for (int i = tid; i < m; i += NT) {
     sx[0] += sh.xs[2 * i];
@@ -892,10 +895,9 @@ __device__ void apply_head(const WaPermLaunch& a, Shared& sh, unsigned long long
   }
   block_sum<2>(sh, sx);
   // Ym of column `line`: its rows in this lane's chunk, then the group's sum
-  const int rc = (m + t - 1) / t;
   int64_t y0 = 0, y1 = 0;
   if (line < n)
-    for_bits_range(colbits, n, line, min(sub * rc, m), min(sub * rc + rc, m), [&](int i) {
+    for_bits_range(colbits, n, line, r0, r1, [&](int i) {
       y0 += sh.xs[2 * i];
       y1 += sh.xs[2 * i + 1];
     });
@@ -910,41 +912,31 @@ __device__ void apply_head(const WaPermLaunch& a, Shared& sh, unsigned long long
     const uint64_t p = uabs64(ym0), q = uabs64(ym1);
     mx = p > q ? p : q;
   }
-  maxy = block_max(sh, mx);
+  for (int i = tid; i < 2 * m; i += NT) za[i] = 0ull;
+  maxy = block_max(sh, mx);  // its barriers also complete the clearing of za
   const int bl = bitlen_u64(maxy);
   const int sy = bl > 30 ? bl - 30 : 0;
-  int32_t* ysh = sh.ys;  // Ys (the sort scratch is free during the steps)
   int64_t py[2] = {0, 0};
-  if (line < n && sub == 0) {
+  if (line < n) {
     const int32_t v0 = (int32_t)(ym0 >> sy), v1 = (int32_t)(ym1 >> sy);
-    ysh[2 * line] = v0;
-    ysh[2 * line + 1] = v1;
-    py[0] = c * v0;
-    py[1] = c * v1;
-  }
-  block_sum<2>(sh, py);  // its barriers also publish Ys
-  // (M Ys) of row `line`
-  const int cr = (n + t - 1) / t;
-  int64_t z0 = 0, z1 = 0;
-  if (line < m)
-    for_bits_range(rowbits, m, line, min(sub * cr, n), min(sub * cr + cr, n), [&](int j) {
-      z0 += ysh[2 * j];
-      z1 += ysh[2 * j + 1];
+    if (sub == 0) {
+      py[0] = c * v0;
+      py[1] = c * v1;
+    }
+    const unsigned long long u0 = (unsigned long long)(int64_t)v0, u1 = (unsigned long long)(int64_t)v1;
+    for_bits_range(colbits, n, line, r0, r1, [&](int i) {
+      atomicAdd(&za[2 * i], u0);
+      atomicAdd(&za[2 * i + 1], u1);
     });
-  z0 = group_sum(z0, t);
-  z1 = group_sum(z1, t);
-  if (line < m && sub == 0) {
-    za[2 * line] = (unsigned long long)z0;
-    za[2 * line + 1] = (unsigned long long)z1;
   }
-  __syncthreads();
+  block_sum<2>(sh, py);  // its barriers also complete the scatter
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int i = tid + k * NT;
     zr[k][0] = i < m ? (int64_t)m * (int64_t)za[2 * i] - py[0] : 0;
     zr[k][1] = i < m ? (int64_t)m * (int64_t)za[2 * i + 1] - py[1] : 0;
   }
-  __syncthreads();  // every thread has read za before the next step writes it
+  __syncthreads();  // every thread has read za before the next step clears it
 }
 
 __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
@@ -952,7 +944,6 @@ __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
   Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
   unsigned long long* za = reinterpret_cast<unsigned long long*>(smem_raw + sizeof(Shared));  // [2 m]
   uint64_t* cb = reinterpret_cast<uint64_t*>(za + 2 * a.m);  // the head's column bitmask [mw][n]
-  uint64_t* rbl = cb + (size_t)((a.m + 63) / 64) * a.n;     // its row bitmask [nw][m], if a.rows_in_lds
   const int h = blockIdx.x;
   const HeadInit hi = init_head(a, sh, h);
   if (hi.status == HEAD_DONE) return;
@@ -962,16 +953,11 @@ __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
   if (!degen) {
     const Head H = head_of(a, h);
     for (int t = threadIdx.x; t < H.mw * a.n; t += NT) cb[t] = H.colbits[t];
-    const uint64_t* rows = H.rowbits;
-    if (a.rows_in_lds) {
-      for (int t = threadIdx.x; t < H.nw * a.m; t += NT) rbl[t] = H.rowbits[t];
-      rows = rbl;
-    }
-    const int line = threadIdx.x / lanes_per_line(a.m > a.n ? a.m : a.n);
+    const int line = threadIdx.x / lanes_per_line(a.n);
     const int64_t c_line = line < a.n ? a.cc[(int64_t)h * a.n + line] : 0;
     __syncthreads();
     for (int it = 0; it <= a.iters; ++it) {
-      apply_head(a, sh, za, cb, rows, c_line, zr, maxy);
+      apply_head(a, sh, za, cb, c_line, zr, maxy);
       if (it < a.iters && orth(sh, H, zr)) {
         degen = true;
         break;
@@ -1024,16 +1010,12 @@ hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   hipError_t e = hipFuncSetAttribute((const void*)apply_scatter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)zsmem);
   if (e != hipSuccess) return e;
-  size_t fsmem = smem + (size_t)2 * a.m * sizeof(unsigned long long) +
-                 (size_t)((a.m + 63) / 64) * a.n * sizeof(uint64_t);
+  const size_t fsmem = smem + (size_t)2 * a.m * sizeof(unsigned long long) +
+                       (size_t)((a.m + 63) / 64) * a.n * sizeof(uint64_t);
   if (!a.stats_only && a.slices <= kFusedMaxSlices && fsmem <= kLdsBytes) {
-    WaPermLaunch f = a;
-    const size_t rows = (size_t)((a.n + 63) / 64) * a.m * sizeof(uint64_t);
-    f.rows_in_lds = fsmem + rows <= kLdsBytes ? 1 : 0;  // the row bitmask too, when it fits
-    if (f.rows_in_lds) fsmem += rows;
     e = hipFuncSetAttribute((const void*)perm_fused_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fsmem);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(perm_fused_kernel, dim3(a.bh), dim3(NT), fsmem, stream, f);
+    hipLaunchKernelGGL(perm_fused_kernel, dim3(a.bh), dim3(NT), fsmem, stream, a);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(perm_init_kernel, dim3(a.bh), dim3(NT), smem, stream, a);

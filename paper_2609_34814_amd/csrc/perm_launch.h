@@ -38,7 +38,6 @@ struct WaPermLaunch {
   int32_t* seg_start;       // [bh][n_xcd+1], nullable
   int32_t bh, m, n, slices;
   int32_t wave, n_xcd, iters, skip_mode, stats_only;
-  int32_t rows_in_lds;      // set by the launcher: the one-workgroup form holds the row bitmask in LDS
   int32_t block, head_dim;
   uint64_t seed;
   wa_skip_profile prof;
