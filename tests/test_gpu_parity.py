@@ -58,10 +58,13 @@ def test_fp64_arithmetic_is_ieee_exact():
 
 
 def test_xcc_round_robin_dispatch():
+    """Workgroups are dealt to the eight XCDs round-robin. The XCD of workgroup 0 depends on the dispatches
+    before (the deal continues across launches), so the check allows a rotation; the attention kernel
+    reads its XCD from the hardware register and does not rely on either."""
     ids = _w().xcc_probe(8 * 4096).cpu().numpy()
     assert set(np.unique(ids)) == set(range(8))
-    frac = float((ids == (np.arange(ids.size) % 8)).mean())
-    print(f"workgroups on XCD g mod 8: {frac:.4f}")
+    frac = float((ids == ((np.arange(ids.size) + int(ids[0])) % 8)).mean())
+    print(f"workgroups on XCD (g + {int(ids[0])}) mod 8: {frac:.4f}")
     assert frac == 1.0
 
 
