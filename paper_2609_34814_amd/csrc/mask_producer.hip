@@ -33,19 +33,19 @@
 
 namespace {
 
-constexpr int kSelThreads = 1024;  // 16 wavefronts: one 16-KV-block tile each, then one row each
+constexpr int kThreads = 1024;  // every role: 16 wavefronts (selection: one 16-KV-block tile each, then rows)
 constexpr int kChunk = 256;        // KV blocks scored per pass (16 wavefronts x 16)
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// Pooling role of workgroup wg: threads wg * kSelThreads + tid cover Q, then K, of heads
+// Pooling role of workgroup wg: threads wg * kThreads + tid cover Q, then K, of heads
 // [h0, h0 + nh), D / 8 consecutive threads (lanes of one wavefront) per block.
 template <int D>
 __device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int nh, int64_t wg) {
   constexpr int G = D / 8;  // 8-channel groups per block
   const int64_t per = (int64_t)nh * a.mb * G;
-  const int64_t gid = wg * kSelThreads + threadIdx.x;
+  const int64_t gid = wg * kThreads + threadIdx.x;
   const bool active = gid < 2 * per;
   const int which = gid < per ? 0 : 1;
   const uint16_t* x = (const uint16_t*)(which ? a.k : a.q);
@@ -119,7 +119,7 @@ __device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which,
   const uint32_t* b = a.bmax + wh * a.mb;
   const int tid = threadIdx.x;
   uint32_t mx = 0u;
-  for (int j = tid; j < a.mb; j += kSelThreads) mx = b[j] > mx ? b[j] : mx;
+  for (int j = tid; j < a.mb; j += kThreads) mx = b[j] > mx ? b[j] : mx;
   for (int o = 32; o > 0; o >>= 1) {
     const uint32_t u = __shfl_xor(mx, o);
     mx = u > mx ? u : mx;
@@ -127,14 +127,14 @@ __device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which,
   if ((tid & 63) == 0) part[tid >> 6] = mx;
   __syncthreads();
   uint32_t m = part[0];
-  for (int w = 1; w < kSelThreads / 64; ++w) m = part[w] > m ? part[w] : m;
+  for (int w = 1; w < kThreads / 64; ++w) m = part[w] > m ? part[w] : m;
   if (tid == 0) a.amax[wh] = m;
   const float fmx = __uint_as_float(m);
   const float inv = fmx > 0.f ? 127.0f / fmx : 0.f;
   const float4* src = (const float4*)(a.means + wh * a.mb * D);
   uint32_t* dst = (uint32_t*)(a.codes + wh * a.mb * D);
   const int n4 = a.mb * D / 4;
-  for (int e = tid; e < n4; e += kSelThreads) {
+  for (int e = tid; e < n4; e += kThreads) {
     const float4 v = src[e];
     uint32_t word = 0u;
     if (fmx > 0.f) {
@@ -162,8 +162,8 @@ struct SelGeom {
 template <int JT>
 struct SelLds {
   int32_t sc[SelGeom<JT>::ROWS][kChunk + 1];  // one pass's scores (+1: fewer bank conflicts)
-  int32_t hist[kSelThreads / 64][256];        // one digit histogram per wavefront
-  uint64_t rbits[kSelThreads / 64][JT];       // one row's kept bits per wavefront
+  int32_t hist[kThreads / 64][256];        // one digit histogram per wavefront
+  uint64_t rbits[kThreads / 64][JT];       // one row's kept bits per wavefront
 };
 
 // Selection role of one workgroup: query blocks [r0, r0 + ROWS) of head bh. JT (a multiple of
@@ -387,7 +387,7 @@ struct ProducerStep {
 };
 
 template <int D, int JT>
-__global__ __launch_bounds__(kSelThreads) void producer_step_kernel(WaProducerLaunch a, ProducerStep st) {
+__global__ __launch_bounds__(kThreads) void producer_step_kernel(WaProducerLaunch a, ProducerStep st) {
   __shared__ SelLds<JT> lds;
   const int64_t idx = blockIdx.x;
   if (idx < 2 * st.code_nh) {
@@ -423,7 +423,7 @@ hipError_t launch_all_t(const WaProducerLaunch& a, hipStream_t stream) {
     if (k < ng) {
       st.pool_h0 = first(k);
       st.pool_nh = count(k);
-      st.pool_wgs = (2ll * st.pool_nh * a.mb * (D / 8) + kSelThreads - 1) / kSelThreads;
+      st.pool_wgs = (2ll * st.pool_nh * a.mb * (D / 8) + kThreads - 1) / kThreads;
     }
     if (k >= 1 && k - 1 < ng) {
       st.code_h0 = first(k - 1);
@@ -435,7 +435,7 @@ hipError_t launch_all_t(const WaProducerLaunch& a, hipStream_t stream) {
       st.sel_wgs = (int64_t)st.sel_nh * tiles;
     }
     const int64_t grid = 2ll * st.code_nh + st.sel_wgs + st.pool_wgs;
-    hipLaunchKernelGGL((producer_step_kernel<D, JT>), dim3((unsigned)grid), dim3(kSelThreads), 0, stream, a, st);
+    hipLaunchKernelGGL((producer_step_kernel<D, JT>), dim3((unsigned)grid), dim3(kThreads), 0, stream, a, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
