@@ -572,6 +572,14 @@ def run_producer(args) -> int:
     hbm_bytes = 2.0 * b_ * h_ * n * d * 2 + float(b_ * h_ * mb * mb)
     nnz = int(md.sum(dtype=torch.int64).item())
     log(f"producer: {prod_ms:.3f} ms, keep {keep} + diagonal, nnz {nnz} ({nnz / (b_ * h_ * mb * mb):.4f})")
+    roof = {"bound": "hbm", "achieved": hbm_bytes / (prod_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": hbm_bytes / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": hbm_bytes}
+    if args.producer_only:
+        print(json.dumps({"mode": "producer", "workload": wl.name, "keep": keep, "diagonal": True,
+                          "density": nnz / (b_ * h_ * mb * mb), "producer_ms": prod_ms,
+                          "producer_calls": args.warmup + args.steps, "producer_roofline": roof, "path": {}}),
+              flush=True)
+        return 0
 
     perm_ws = torch.empty(W.perm_workspace_size(shape), dtype=torch.uint8, device="cuda")
     attn_ws = torch.empty(W.attn_vt_workspace_size(shape), dtype=torch.uint8, device="cuda")
@@ -613,10 +621,7 @@ def run_producer(args) -> int:
         log(f"{variant}: step {step_ms:.2f} ms, attention {attn_ms:.2f} ms")
     print(json.dumps({
         "mode": "producer", "workload": wl.name, "keep": keep, "diagonal": True, "density": nnz / (b_ * h_ * mb * mb),
-        "producer_ms": prod_ms, "producer_calls": args.warmup + args.steps,
-        "producer_roofline": {"bound": "hbm", "achieved": hbm_bytes / (prod_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
-                              "unit": "GB/s", "frac": hbm_bytes / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                              "algorithmic_bytes": hbm_bytes},
+        "producer_ms": prod_ms, "producer_calls": args.warmup + args.steps, "producer_roofline": roof,
         "path": res}), flush=True)
     return 0
 
@@ -705,6 +710,8 @@ def main() -> int:
     ap.add_argument("--producer", action="store_true",
                     help="time the pooled-score top-k mask producer and the path on its mask (JSON line)")
     ap.add_argument("--producer-density", type=float, default=0.05, help="kept blocks per row / M_B")
+    ap.add_argument("--producer-only", action="store_true",
+                    help="with --producer: time the producer alone, not the path on its mask")
     ap.add_argument("--sweep-command", default="", help="command line recorded in the sweep summary")
     args = ap.parse_args()
 
