@@ -153,7 +153,7 @@ struct SelGeom {
 // LDS of the selection role
 template <int JT>
 struct SelLds {
-  int32_t sc[SelGeom<JT>::ROWS][kChunk + 1];  // one pass's scores (+1: fewer bank conflicts)
+  int32_t sc[2][SelGeom<JT>::ROWS][kChunk + 1];  // scores of two passes in turn (+1: fewer bank conflicts)
   int32_t hist[kThreads / 64][256];        // one digit histogram per wavefront
   uint64_t rbits[kThreads / 64][JT];       // one row's kept bits per wavefront
 };
@@ -168,7 +168,6 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
   constexpr int KS = D / 64;                      // 64-channel steps of one MFMA each
   constexpr int NCH = JT * 64 / kChunk;           // passes over the KV blocks
   constexpr int CU = kChunk / 64;                 // entries per lane and pass
-  int32_t (&sc)[ROWS][kChunk + 1] = L.sc;
   const int nr = min(ROWS, a.mb - r0);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -212,7 +211,10 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
       for (int st = 0; st < KS; ++st) acc[g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ka[st], qb[g][st], acc[g], 0, 0, 0);
     }
     if (c + 1 < NCH) load_k(c + 1, ka);
-    // each 16 x 16 result: lane l holds KV rows 4 (l / 16) + e, query column l mod 16 of its group
+    // each 16 x 16 result: lane l holds KV rows 4 (l / 16) + e, query column l mod 16 of its group.
+    // Passes alternate between two tiles: the barrier of pass c + 1 (every wavefront has collected
+    // pass c) orders the reads of pass c before pass c + 2 overwrites that tile.
+    int32_t (&sc)[ROWS][kChunk + 1] = L.sc[c & 1];
 #pragma unroll
     for (int g = 0; g < RG; ++g)
 #pragma unroll
@@ -225,7 +227,6 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
         const int j = c * kChunk + 64 * u + lane;
         val[g][c * CU + u] = j < mb ? sc[w + 16 * g][64 * u + lane] : INT32_MIN;
       }
-    __syncthreads();  // every row is collected before the next pass overwrites the tile
   }
   const int keep = a.keep < mb ? a.keep : mb;
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
