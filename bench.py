@@ -298,7 +298,7 @@ def summarize_producer_trace(rows, line, out_md: str, command_note: str) -> None
     for r in rows:
         short = r["Name"].replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
         avg = float(r["AverageNs"]) / 1e6
-        if "producer_step_kernel" in r["Name"]:  # several launches per call
+        if "producer_kernel" in r["Name"] or "producer_init_kernel" in r["Name"]:  # two launches per call
             prod_ms += float(r["TotalDurationNs"]) / 1e6 / calls
             launches += int(r["Calls"])
         if short.startswith("at::") or "elementwise" in short or "reduce_kernel" in short:
@@ -310,7 +310,7 @@ def summarize_producer_trace(rows, line, out_md: str, command_note: str) -> None
               f"bench.py (HIP events around wa_produce_block_mask, same run): {line['producer_ms']:.3f} ms; "
               f"{rf['achieved']:.0f} GB/s of {rf['algorithmic_bytes'] / 1e9:.2f} GB algorithmic bytes "
               f"(Q and K read once, mask written) = {100 * rf['frac']:.1f}% of 8 TB/s.",
-              f"rocprofv3: the producer's {launches // calls} pipeline launches per call take {prod_ms:.3f} ms "
+              f"rocprofv3: the producer's {launches // calls} launches per call take {prod_ms:.3f} ms "
               f"per call ({calls} calls).", "",
               "Path on the produced mask (step = permutation if built + compaction + attention):", ""]
     for v, r in line["path"].items():

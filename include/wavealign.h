@@ -204,7 +204,9 @@ wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* sh
                                 uint8_t* mask, int8_t* codes, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes needed by wa_produce_block_mask: float32 block means, per-block and
- * per-head maxima of Q and K, and their int8 codes. */
+ * per-head maxima of Q and K, their int8 codes, and the call's work queue (64 + 4*B*H
+ * uint32 counters and flags, cleared by the call itself). Calls that share a workspace
+ * must not overlap. */
 wa_status wa_mask_producer_workspace_size(const wa_shape* shape, size_t* bytes);
 
 /* Workspace bytes needed by wa_sparse_attn: the scheduler state (queue counters,

@@ -73,7 +73,7 @@ wa_status check_shape(const wa_shape* s, Dims* out) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 struct ProducerWs {
-  size_t means, amax, bmax, codes, total;
+  size_t means, amax, bmax, codes, queue, total;
 };
 
 ProducerWs producer_ws_layout(const Dims& d) {
@@ -83,6 +83,7 @@ ProducerWs producer_ws_layout(const Dims& d) {
   w.amax = off; off = align_up(off + (size_t)2 * d.bh * 4);
   w.bmax = off; off = align_up(off + (size_t)2 * d.bh * d.mb * 4);
   w.codes = off; off = align_up(off + (size_t)2 * d.bh * d.mb * d.d);
+  w.queue = off; off = align_up(off + (size_t)wa_producer_queue_words(d.bh) * 4);
   w.total = off;
   return w;
 }
@@ -360,6 +361,7 @@ wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* sh
   a.bmax = (uint32_t*)(base + L.bmax);
   a.codes = codes ? codes : (int8_t*)(base + L.codes);
   a.mask = mask;
+  a.queue = (uint32_t*)(base + L.queue);
   a.bh = (int32_t)d.bh; a.mb = d.mb; a.seq_len = d.n; a.block = d.blk; a.head_dim = d.d;
   a.keep = keep; a.diagonal = diagonal ? 1 : 0;
   hipError_t e = wa_launch_producer(a, (hipStream_t)stream);

@@ -1,27 +1,30 @@
 // Pooled-score top-k block mask for gfx950: a content-dependent producer of the block mask
 // (Sec. II-B: dynamic sparse attention predicts block relevance from pooled Q/K features).
 //
-// Three roles of one kernel, each taken by whole workgroups of 16 wavefronts:
+// Three roles in one persistent kernel (one workgroup of 16 wavefronts per compute unit, taking
+// items from one queue):
 //   pooling     block means of Q and K: each thread folds 8 channels of one block over its
 //               tokens in ascending order (IEEE float32, one rounding per addition, 16-byte
 //               loads), then one correctly rounded division by the token count, and each
 //               block's maximum |mean| (as float bits: non-negative floats order like their bit
-//               patterns);
-//   codes       one workgroup per head and tensor: the head's maximum over its block maxima,
-//               then int8 codes rint(mean * fl32(127 / max)), clamped to [-127, 127];
-//   selection   one workgroup per 32 query blocks of a head (16 for rows of more than 3,072
-//               blocks): exact int32 scores s_ij = sum_c qcode_i[c] kcode_j[c] with int8 MFMAs
+//               patterns); an item is 64 blocks;
+//   codes       per head and tensor, by the workgroup that pooled its last blocks: the head's
+//               maximum over its block maxima, then int8 codes rint(mean * fl32(127 / max)),
+//               clamped to [-127, 127];
+//   selection   an item is 32 query blocks of a head (16 for rows of more than 3,072 blocks):
+//               exact int32 scores s_ij = sum_c qcode_i[c] kcode_j[c] with int8 MFMAs
 //               (v_mfma_i32_16x16x64_i8: 16 KV blocks x 16 query blocks per instruction),
 //               256 KV blocks per pass through a small LDS tile, so that each K code row is
 //               read once per 16 query blocks; each wavefront collects one row's scores in
 //               registers, finds the k-th largest exactly by a radix select over 8-bit digits
-//               of the score minus the row minimum (one 256-bin LDS histogram per wavefront and
+//               of the score minus a floor under it (one 256-bin LDS histogram per wavefront and
 //               digit), keeps every larger score, the first equal scores in ascending j up to
 //               k, and the diagonal if asked, and writes the row.
-// The heads are taken in groups of about 12,000 query blocks, and launch k runs the pooling of
-// group k, the codes of group k - 1 and the selection of group k - 2, so that the memory-bound
-// pooling of one group overlaps the compute-bound selection of another; no workgroup waits for
-// another within a launch.
+// The heads are taken in groups of about 12,000 query blocks; step k of the queue holds the
+// pooling of group k and the selection of group k - 2, interleaved, so that the memory-bound
+// pooling of one group overlaps the compute-bound selection of another. A selection item waits
+// for the codes of its head, whose pooling was queued two steps earlier. One launch replaces
+// the earlier one launch per step, each of which ended with a partly idle chip.
 // Every step is exact or a single float32 rounding in a fixed order, so the mask is the same bit
 // for bit as a plain implementation of the same definition.
 
@@ -33,11 +36,25 @@
 
 namespace {
 
+// Workgroup barrier that waits only for this wavefront's LDS operations (a full __syncthreads also
+// waits for every global load in flight, which would drain the K loads issued passes ahead); the
+// compiler may not move memory accesses across it.
+#define WA_LDS_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
+
 constexpr int kThreads = 1024;  // every role: 16 wavefronts (selection: one 16-KV-block tile each, then rows)
 constexpr int kChunk = 256;        // KV blocks scored per pass (16 wavefronts x 16)
 // Channels folded per pooling thread: 8 (one 16-byte load per token). 4 (8-byte loads, twice the
 // threads) took 1.93 ms per call against 1.79, 16 (two loads per token) 2.67.
 constexpr int kPoolCh = 8;
+
+// Stores that other workgroups of the same launch read (block means and maxima, head maxima,
+// codes): device-scope atomic stores, which gfx950 writes through to the level every XCD sees, so
+// that publishing them takes only a wait for their completion rather than a write-back of the
+// whole L2 (the release fence on this multi-XCD chip).
+template <typename T>
+__device__ __forceinline__ void dev_store(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
@@ -45,13 +62,13 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 // Pooling role of workgroup wg: threads wg * kThreads + tid cover Q, then K, of heads [h0, h0 + nh),
 // D / kPoolCh consecutive threads (lanes of one wavefront) per block, each folding kPoolCh channels.
 template <int D>
-__device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int nh, int64_t wg) {
+__device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int nh, int64_t wg, int tid) {
   constexpr int CH = kPoolCh;
   constexpr int G = D / CH;       // channel groups per block
   constexpr int U = 64 / CH;      // tokens per round of loads (128 bytes in flight per thread)
   typedef unsigned vec __attribute__((ext_vector_type(CH / 2)));
   const int64_t per = (int64_t)nh * a.mb * G;
-  const int64_t gid = wg * kThreads + threadIdx.x;
+  const int64_t gid = wg * kThreads + tid;
   const bool active = gid < 2 * per;
   const int which = gid < per ? 0 : 1;
   const uint16_t* x = (const uint16_t*)(which ? a.k : a.q);
@@ -85,13 +102,14 @@ __device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int
     }
     for (; t < cnt; ++t) fold(*(const vec*)(p + (int64_t)t * D));
     const float c = (float)cnt;
-    float* out = a.means + ((int64_t)which * a.bh * a.mb + bj) * D + CH * g;
+    uint64_t* out = (uint64_t*)(a.means + ((int64_t)which * a.bh * a.mb + bj) * D + CH * g);
 #pragma unroll
-    for (int e = 0; e < CH; ++e) {
-      const float m = acc[e] / c;
-      out[e] = m;
-      const uint32_t b = __float_as_uint(fabsf(m));
-      mx = b > mx ? b : mx;
+    for (int e = 0; e < CH; e += 2) {
+      const float m0 = acc[e] / c, m1 = acc[e + 1] / c;
+      dev_store(out + e / 2, (uint64_t)__float_as_uint(m0) | ((uint64_t)__float_as_uint(m1) << 32));
+      const uint32_t b0 = __float_as_uint(fabsf(m0)), b1 = __float_as_uint(fabsf(m1));
+      mx = b0 > mx ? b0 : mx;
+      mx = b1 > mx ? b1 : mx;
     }
   }
   // maximum over the G lanes of this block (every lane takes part)
@@ -100,16 +118,16 @@ __device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int
     const uint32_t u = __shfl_xor(mx, o);
     mx = u > mx ? u : mx;
   }
-  if (active && g == 0) a.bmax[(int64_t)which * a.bh * a.mb + bj] = mx;
+  if (active && g == 0) dev_store(a.bmax + (int64_t)which * a.bh * a.mb + bj, mx);
 }
 
 // Codes role of one workgroup: head bh of Q (which = 0) or K (which = 1): the head's maximum block
 // maximum, then codes rint(mean * fl32(127 / max)) clamped to [-127, 127], 0 when max = 0.
 template <int D>
-__device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which, int64_t bh, uint32_t* part) {
+__device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which, int64_t bh, uint32_t* part,
+                                           int tid) {
   const int64_t wh = which * (int64_t)a.bh + bh;
   const uint32_t* b = a.bmax + wh * a.mb;
-  const int tid = threadIdx.x;
   uint32_t mx = 0u;
   for (int j = tid; j < a.mb; j += kThreads) mx = b[j] > mx ? b[j] : mx;
   for (int o = 32; o > 0; o >>= 1) {
@@ -120,7 +138,7 @@ __device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which,
   __syncthreads();
   uint32_t m = part[0];
   for (int w = 1; w < kThreads / 64; ++w) m = part[w] > m ? part[w] : m;
-  if (tid == 0) a.amax[wh] = m;
+  if (tid == 0) dev_store(a.amax + wh, m);
   const float fmx = __uint_as_float(m);
   const float inv = fmx > 0.f ? 127.0f / fmx : 0.f;
   const float4* src = (const float4*)(a.means + wh * a.mb * D);
@@ -138,9 +156,13 @@ __device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which,
         word |= (uint32_t)(uint8_t)(int8_t)(int)r << (8 * q);
       }
     }
-    dst[e] = word;
+    dev_store(dst + e, word);
   }
 }
+
+// Bytes per Q code row in LDS: 128 + 16, so that the 16 rows one MFMA operand read takes lie in
+// distinct banks.
+constexpr int kQsStride = 144;
 
 // Query blocks per score_select workgroup: RG groups of 16 (the MFMA's 16 columns), two when the
 // rows' scores (2 JT registers) leave room for four wavefronts per SIMD, else one.
@@ -154,6 +176,7 @@ struct SelGeom {
 template <int JT>
 struct SelLds {
   int32_t sc[2][SelGeom<JT>::ROWS][kChunk + 1];  // scores of two passes in turn (+1: fewer bank conflicts)
+  __attribute__((aligned(16))) int8_t qs[SelGeom<JT>::ROWS][kQsStride];  // the rows' Q codes (head_dim <= 128)
   int32_t hist[kThreads / 64][256];        // one digit histogram per wavefront
   uint64_t rbits[kThreads / 64][JT];       // one row's kept bits per wavefront
 };
@@ -161,7 +184,7 @@ struct SelLds {
 // Selection role of one workgroup: query blocks [r0, r0 + ROWS) of head bh. JT (a multiple of
 // kChunk / 64 with 64 JT >= mb) is the number of scores of one row each lane holds.
 template <int D, int JT>
-__device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t bh, int r0, SelLds<JT>& L) {
+__device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t bh, int r0, SelLds<JT>& L, int tid) {
   typedef int v4i __attribute__((ext_vector_type(4)));
   constexpr int RG = SelGeom<JT>::RG;
   constexpr int ROWS = SelGeom<JT>::ROWS;
@@ -169,7 +192,6 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
   constexpr int NCH = JT * 64 / kChunk;           // passes over the KV blocks
   constexpr int CU = kChunk / 64;                 // entries per lane and pass
   const int nr = min(ROWS, a.mb - r0);
-  const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int mb = a.mb;
@@ -178,29 +200,30 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
   const v4i zero = {0, 0, 0, 0};
   // MFMA operands: lane l holds bytes [16 (l / 16), +16) of each 64-channel step of one code row,
   // row l mod 16 (the same channel split for both operands, so each product pairs equal channels).
-  // B of group g: the Q codes of query block r0 + 16 g + l mod 16 (zero past the head).
-  v4i qb[RG][KS];
-#pragma unroll
-  for (int g = 0; g < RG; ++g) {
-    const int qr = r0 + 16 * g + (lane & 15);
-#pragma unroll
-    for (int st = 0; st < KS; ++st)
-      qb[g][st] = qr < mb ? *(const v4i*)(qc + (int64_t)qr * D + 64 * st + 16 * (lane >> 4)) : zero;
+  // B of group g: the Q codes of query block r0 + 16 g + l mod 16 (zero past the head), staged in
+  // LDS once and read there before each product (registers are the scarce resource here).
+  for (int e = tid; e < ROWS * (D / 16); e += kThreads) {
+    const int row = e / (D / 16), col = e % (D / 16);
+    const int qr = r0 + row;
+    *(v4i*)&L.qs[row][16 * col] = qr < mb ? *(const v4i*)(qc + (int64_t)qr * D + 16 * col) : zero;
   }
   // A of pass c: the K codes of KV block c kChunk + 16 w + l mod 16 (zero past the head), loaded
-  // one pass ahead
+  // one pass ahead. Only the passes that reach past the head check (the last one, and on short
+  // heads the ones after it).
   auto load_k = [&](int c, v4i (&ka)[KS]) {
     const int kv = c * kChunk + 16 * w + (lane & 15);
+    const bool in = (c + 1) * kChunk <= mb || kv < mb;
 #pragma unroll
     for (int st = 0; st < KS; ++st)
-      ka[st] = kv < mb ? *(const v4i*)(kc + (int64_t)kv * D + 64 * st + 16 * (lane >> 4)) : zero;
+      ka[st] = in ? *(const v4i*)(kc + (int64_t)kv * D + 64 * st + 16 * (lane >> 4)) : zero;
   };
   // the rows' scores: entry t of lane l is KV block 64 t + l; entries past the row hold INT32_MIN
-  // and never count. Wavefront w collects query blocks r0 + w + 16 g. (NCH passes cover the row
-  // exactly: kChunk (NCH - 1) < mb <= kChunk NCH, so every entry is written by its pass.)
+  // and never count. Wavefront w collects query blocks r0 + w + 16 g. (mb <= kChunk NCH, so every
+  // entry of the row is written by its pass.)
   int32_t val[RG][JT];
   v4i ka[KS];
   load_k(0, ka);
+  WA_LDS_BARRIER();  // the Q codes are in LDS
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     v4i acc[RG];
@@ -208,7 +231,10 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
     for (int g = 0; g < RG; ++g) {
       acc[g] = zero;
 #pragma unroll
-      for (int st = 0; st < KS; ++st) acc[g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ka[st], qb[g][st], acc[g], 0, 0, 0);
+      for (int st = 0; st < KS; ++st) {
+        const v4i qb = *(const v4i*)&L.qs[16 * g + (lane & 15)][64 * st + 16 * (lane >> 4)];
+        acc[g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ka[st], qb, acc[g], 0, 0, 0);
+      }
     }
     if (c + 1 < NCH) load_k(c + 1, ka);
     // each 16 x 16 result: lane l holds KV rows 4 (l / 16) + e, query column l mod 16 of its group.
@@ -219,13 +245,14 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
     for (int g = 0; g < RG; ++g)
 #pragma unroll
       for (int e = 0; e < 4; ++e) sc[16 * g + (lane & 15)][16 * w + 4 * (lane >> 4) + e] = acc[g][e];
-    __syncthreads();
+    WA_LDS_BARRIER();
 #pragma unroll
     for (int g = 0; g < RG; ++g)
 #pragma unroll
       for (int u = 0; u < CU; ++u) {
         const int j = c * kChunk + 64 * u + lane;
-        val[g][c * CU + u] = j < mb ? sc[w + 16 * g][64 * u + lane] : INT32_MIN;
+        const int x = sc[w + 16 * g][64 * u + lane];  // (past the head: a product with zero codes)
+        val[g][c * CU + u] = (c + 1) * kChunk <= mb || j < mb ? x : INT32_MIN;
       }
   }
   const int keep = a.keep < mb ? a.keep : mb;
@@ -248,16 +275,38 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
     }
     lo = __builtin_amdgcn_readfirstlane(lo);
     hi = __builtin_amdgcn_readfirstlane(hi);
-    // The keep-th largest score, digit by digit of u = s - lo (0 <= u <= hi - lo < 2^23): at each
-    // level the wavefront counts its candidates (entries whose higher digits equal the prefix found
-    // so far) in 256 bins of the next 8 bits, and the bin holding the kept-th largest candidate fixes
-    // those bits. Three levels resolve any row.
+    // A floor under the keep-th largest score: each lane splits its entries into three groups
+    // (t mod 3) and takes the smallest of the three group maxima; the floor is the smallest of
+    // those over the lanes whose groups all hold a score. Every such group has a score at or above
+    // the floor, so when the groups number at least keep, so is the keep-th largest score; the
+    // search below then counts only the scores at or above it (about a quarter of the row at 5%
+    // density), and the histogram atomics stop piling up on the crowded middle bins.
+    int base = lo;
+    if (keep > 0 && keep <= 3 * 64 && lo < hi) {
+      int g0 = INT32_MIN, g1 = INT32_MIN, g2 = INT32_MIN;
+#pragma unroll
+      for (int t = 0; t < JT; t += 3) {
+        g0 = max(g0, v_[t]);
+        if (t + 1 < JT) g1 = max(g1, v_[t + 1]);
+        if (t + 2 < JT) g2 = max(g2, v_[t + 2]);
+      }
+      const bool full = g0 != INT32_MIN && g1 != INT32_MIN && g2 != INT32_MIN;
+      const int n_full = __popcll(__ballot(full));
+      int f = full ? min(g0, min(g1, g2)) : INT32_MAX;
+      for (int o = 32; o > 0; o >>= 1) f = min(f, __shfl_xor(f, o));
+      f = __builtin_amdgcn_readfirstlane(f);
+      if (3 * n_full >= keep && f < hi) base = f;
+    }
+    // The keep-th largest score, digit by digit of u = s - base (0 <= u <= hi - base < 2^23): at
+    // each level the wavefront counts its candidates (entries whose higher digits equal the prefix
+    // found so far) in 256 bins of the next 8 bits, and the bin holding the kept-th largest
+    // candidate fixes those bits. Three levels resolve any row.
     // thr: the keep-th largest score; ties: how many scores equal to thr are kept (the first ones in
     // ascending j); neq: how many scores equal thr
     int thr = lo, ties = keep, neq = mb;  // all scores equal when lo == hi
     if (keep > 0 && lo < hi) {
       int32_t* h = L.hist[w];
-      int nbits = 32 - __builtin_clz((uint32_t)(hi - lo));
+      int nbits = 32 - __builtin_clz((uint32_t)(hi - base));
       uint32_t prefix = 0u;
       int rem = keep;  // rank of the sought value among the candidates, from the top
       while (nbits > 0) {
@@ -268,8 +317,9 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
         asm volatile("" ::: "memory");
 #pragma unroll
         for (int t = 0; t < JT; ++t) {
-          // below the prefix u wraps past 2^nbits; a missing entry (INT32_MIN) lands near 2^31
-          const uint32_t u = (uint32_t)v_[t] - (uint32_t)lo - prefix;
+          // below the floor or the prefix u wraps past 2^nbits; a missing entry (INT32_MIN) lands
+          // near 2^31
+          const uint32_t u = (uint32_t)v_[t] - (uint32_t)base - prefix;
           if ((u >> nbits) == 0u) atomicAdd(&h[u >> sh], 1);
         }
         asm volatile("" ::: "memory");
@@ -306,7 +356,7 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
         prefix += (uint32_t)bin << sh;
         nbits = sh;
       }
-      thr = lo + (int)prefix;
+      thr = base + (int)prefix;
       ties = rem;  // the larger scores are keep - rem
     }
     // the row as bits, 64 blocks per word: word t = ballot of blocks 64 t .. 64 t + 63, kept by lane t
@@ -369,70 +419,156 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
   }
 }
 
-// One step of the producer's pipeline over head groups: the codes of group k - 1 and the pooling
-// of group k on some workgroups, the selection of group k - 2 on others, in one launch with no
-// dependence between its workgroups. Roles by workgroup index: the first 2 code_nh take the codes,
-// then selection and pooling workgroups alternate in proportion to their counts, so that the
-// memory-bound pooling and the compute-bound selection share the compute units.
-struct ProducerStep {
-  int32_t pool_h0, pool_nh, code_h0, code_nh, sel_h0, sel_nh;
-  int64_t pool_wgs, sel_wgs;
+// Queue words of one call (workspace, cleared by producer_init_kernel at the start of every call):
+//   [0]                          the next item;
+//   [1]                          set if a wait for codes ran out (see producer_kernel: it cannot);
+//   [kQueueDone + x]             blocks of x = which * bh + head pooled so far (which: 0 Q, 1 K);
+//   [kQueueDone + 2 bh + x]      nonzero once the codes of x are written.
+constexpr int kQueueDone = 64;
+// Sleeps of about 0.25 us between looks at a flag before a wait gives up (about one second).
+constexpr uint32_t kWaitLimit = 1u << 22;
+
+__global__ __launch_bounds__(256) void producer_init_kernel(uint32_t* queue, int64_t words) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < words; e += (int64_t)gridDim.x * 256) queue[e] = 0u;
+}
+
+// The call's work as one sequence of items, taken in order from the queue by resident
+// workgroups. Step k (k = 0 .. ng + 1) holds the pooling items of head group k and the
+// selection items of group k - 2, interleaved in proportion to their counts, so that the
+// memory-bound pooling of one group overlaps the compute-bound selection of another.
+struct ProducerPlan {
+  int32_t per, ng, tiles;
+  int64_t pool_full, pool_last;  // pooling items of a full group and of the last group
+  int64_t total;                 // items of all steps
 };
 
 template <int D, int JT>
-__global__ __launch_bounds__(kThreads) void producer_step_kernel(WaProducerLaunch a, ProducerStep st) {
+__global__ __launch_bounds__(kThreads) void producer_kernel(WaProducerLaunch a, ProducerPlan pl) {
+  constexpr int ROWS = SelGeom<JT>::ROWS;
+  constexpr int G = D / kPoolCh;
   __shared__ SelLds<JT> lds;
-  const int64_t idx = blockIdx.x;
-  if (idx < 2 * st.code_nh) {
-    codes_role<D>(a, (int)(idx / st.code_nh), st.code_h0 + idx % st.code_nh, (uint32_t*)lds.hist);
-    return;
-  }
-  const int64_t k = idx - 2 * st.code_nh;
-  const int64_t S = st.sel_wgs, T = st.sel_wgs + st.pool_wgs;
-  const int64_t s_before = k * S / T, s_after = (k + 1) * S / T;
-  if (s_after > s_before) {
-    const int tiles = (a.mb + SelGeom<JT>::ROWS - 1) / SelGeom<JT>::ROWS;
-    select_role<D, JT>(a, st.sel_h0 + s_before / tiles, (int)(s_before % tiles) * SelGeom<JT>::ROWS, lds);
-  } else {
-    pool_role<D>(a, st.pool_h0, st.pool_nh, k - s_before);
+  __shared__ int64_t s_item;
+  __shared__ int32_t s_nrec, s_rec[kThreads / G];
+  uint32_t* const ready = a.queue + kQueueDone + 2 * (int64_t)a.bh;
+  for (;;) {
+    // the thread index as a value the compiler cannot see through: what the roles derive from it
+    // is recomputed per item instead of being hoisted out of this loop and held in registers
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    __syncthreads();  // the previous item is finished everywhere
+    if (tid == 0) {
+      s_item = (int64_t)atomicAdd(a.queue, 1u);
+      s_nrec = 0;
+    }
+    __syncthreads();
+    int64_t r = s_item;
+    if (r >= pl.total) break;
+    // step k of the item and its place r in that step
+    int k = 0;
+    int64_t P = 0, S = 0;
+    for (; k < pl.ng + 2; ++k) {
+      P = k < pl.ng ? (k == pl.ng - 1 ? pl.pool_last : pl.pool_full) : 0;
+      S = k >= 2 ? (int64_t)min(pl.per, a.bh - (k - 2) * pl.per) * pl.tiles : 0;
+      if (r < P + S) break;
+      r -= P + S;
+    }
+    if (k == pl.ng + 2) break;  // (not reached: the steps hold exactly pl.total items)
+    const int64_t s_before = r * S / (P + S), s_after = (r + 1) * S / (P + S);
+    if (s_after > s_before) {
+      // selection: wait until the codes of its head are written. The pooling of the head's group
+      // came two steps earlier in the queue, so every item it needs was taken by a workgroup that
+      // is running and never waits; the bound only turns an impossible hang into an error.
+      const int head = (k - 2) * pl.per + (int)(s_before / pl.tiles);
+      if (tid == 0) {
+        uint32_t n = 0;
+        while (!(__hip_atomic_load(ready + head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &&
+                 __hip_atomic_load(ready + a.bh + head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+          __builtin_amdgcn_s_sleep(8);
+          if (++n == kWaitLimit) {
+            atomicOr(a.queue + 1, 1u);
+            break;
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the codes another workgroup wrote
+      }
+      __syncthreads();
+      select_role<D, JT>(a, head, (int)(s_before % pl.tiles) * ROWS, lds, tid);
+      continue;
+    }
+    // pooling of items r - s_before of group k
+    const int h0 = k * pl.per, nh = min(pl.per, a.bh - h0);
+    const int64_t idx = r - s_before;
+    pool_role<D>(a, h0, nh, idx, tid);
+    // publish: every wavefront's means and maxima (device-scope stores) have completed, then count
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) {
+      // the item's blocks, by (tensor, head): blocks [b0, b1) of the group's 2 nh mb, in runs of one head
+      const int64_t b0 = idx * (kThreads / G);
+      const int64_t b1 = min(b0 + kThreads / G, 2ll * nh * a.mb);
+      for (int64_t b = b0; b < b1;) {
+        const int64_t x = b / a.mb;  // which * nh + local head
+        const int64_t e = min(b1, (x + 1) * a.mb);
+        const uint32_t cnt = (uint32_t)(e - b);
+        const int which = (int)(x / nh);
+        const int64_t wh = (int64_t)which * a.bh + h0 + x % nh;
+        if (atomicAdd(a.queue + kQueueDone + wh, cnt) + cnt == (uint32_t)a.mb) s_rec[s_nrec++] = (int32_t)wh;
+        b = e;
+      }
+      if (s_nrec > 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other workgroups' means
+    }
+    __syncthreads();
+    // the workgroup that pooled the last blocks of a head and tensor writes its codes
+    const int nrec = s_nrec;
+    for (int q = 0; q < nrec; ++q) {
+      const int wh = s_rec[q];
+      codes_role<D>(a, wh / a.bh, wh % a.bh, (uint32_t*)lds.hist, tid);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the codes (device-scope stores) are complete
+      __syncthreads();
+      if (tid == 0) dev_store(ready + wh, 1u);
+    }
   }
 }
 
-// Query blocks per head group: about 12,000 (four heads of 2,841 blocks). Smaller groups leave
-// too little pooling to overlap a selection with (two heads: +12% call time), larger ones lengthen
-// the launches at both ends of the pipeline, which do not overlap (ten heads: +4%).
+// Query blocks per head group: about 12,000 (four heads of 2,841 blocks). Two-head groups took
+// 1.78 ms per call against 1.74 for four (measured before the stores were made device-scope),
+// one-head groups 2.06 ms: selections then reach their head before its codes are written.
 constexpr int kGroupBlocks = 12000;
+
+int producer_resident_cus() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
 
 template <int D, int JT>
 hipError_t launch_all_t(const WaProducerLaunch& a, hipStream_t stream) {
   const int per_blocks = (kGroupBlocks + a.mb / 2) / a.mb;
-  const int per = per_blocks < 1 ? 1 : (per_blocks > a.bh ? a.bh : per_blocks);
-  const int ng = (a.bh + per - 1) / per;
-  const int tiles = (a.mb + SelGeom<JT>::ROWS - 1) / SelGeom<JT>::ROWS;
-  auto first = [&](int g) { return g * per; };
-  auto count = [&](int g) { return a.bh - g * per < per ? a.bh - g * per : per; };
-  for (int k = 0; k < ng + 2; ++k) {
-    ProducerStep st{};
-    if (k < ng) {
-      st.pool_h0 = first(k);
-      st.pool_nh = count(k);
-      st.pool_wgs = (2ll * st.pool_nh * a.mb * (D / kPoolCh) + kThreads - 1) / kThreads;
-    }
-    if (k >= 1 && k - 1 < ng) {
-      st.code_h0 = first(k - 1);
-      st.code_nh = count(k - 1);
-    }
-    if (k >= 2) {
-      st.sel_h0 = first(k - 2);
-      st.sel_nh = count(k - 2);
-      st.sel_wgs = (int64_t)st.sel_nh * tiles;
-    }
-    const int64_t grid = 2ll * st.code_nh + st.sel_wgs + st.pool_wgs;
-    hipLaunchKernelGGL((producer_step_kernel<D, JT>), dim3((unsigned)grid), dim3(kThreads), 0, stream, a, st);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  ProducerPlan pl{};
+  pl.per = per_blocks < 1 ? 1 : (per_blocks > a.bh ? a.bh : per_blocks);
+  pl.ng = (a.bh + pl.per - 1) / pl.per;
+  pl.tiles = (a.mb + SelGeom<JT>::ROWS - 1) / SelGeom<JT>::ROWS;
+  constexpr int G = D / kPoolCh;
+  auto pool_items = [&](int nh) { return (2ll * nh * a.mb * G + kThreads - 1) / kThreads; };
+  const int last = a.bh - (pl.ng - 1) * pl.per;
+  pl.pool_full = pool_items(pl.per);
+  pl.pool_last = pool_items(last);
+  pl.total = (pl.ng - 1) * pl.pool_full + pl.pool_last + (int64_t)a.bh * pl.tiles;
+  const int64_t words = wa_producer_queue_words(a.bh);
+  const int64_t init_wgs = (words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024;
+  hipLaunchKernelGGL(producer_init_kernel, dim3((unsigned)init_wgs), dim3(256), 0, stream, a.queue, words);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t cus = producer_resident_cus();
+  const int64_t grid = pl.total < cus ? pl.total : cus;
+  hipLaunchKernelGGL((producer_kernel<D, JT>), dim3((unsigned)grid), dim3(kThreads), 0, stream, a, pl);
+  return hipGetLastError();
 }
 
 template <int D>
