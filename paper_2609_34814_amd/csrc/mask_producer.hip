@@ -46,6 +46,7 @@ constexpr int kChunk = 256;        // KV blocks scored per pass (16 wavefronts x
 // Channels folded per pooling thread: 8 (one 16-byte load per token). 4 (8-byte loads, twice the
 // threads) took 1.93 ms per call against 1.79, 16 (two loads per token) 2.67.
 constexpr int kPoolCh = 8;
+static_assert(kPoolCh == 8, "the pooling role stages its 8 means per lane as two float4");
 
 // Stores that other workgroups of the same launch read (block means and maxima, head maxima,
 // codes): device-scope atomic stores, which gfx950 writes through to the level every XCD sees, so
@@ -61,8 +62,12 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 
 // Pooling role of workgroup wg: threads wg * kThreads + tid cover Q, then K, of heads [h0, h0 + nh),
 // D / kPoolCh consecutive threads (lanes of one wavefront) per block, each folding kPoolCh channels.
+// stage: 2 KB of LDS private to the wavefront, through which its means are regrouped so that each
+// store instruction writes 512 contiguous bytes (the stores go through to memory, so partly
+// filled lines would be written more than once).
 template <int D>
-__device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int nh, int64_t wg, int tid) {
+__device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int nh, int64_t wg, int tid,
+                                          float* stage) {
   constexpr int CH = kPoolCh;
   constexpr int G = D / CH;       // channel groups per block
   constexpr int U = 64 / CH;      // tokens per round of loads (128 bytes in flight per thread)
@@ -102,14 +107,33 @@ __device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int
     }
     for (; t < cnt; ++t) fold(*(const vec*)(p + (int64_t)t * D));
     const float c = (float)cnt;
-    uint64_t* out = (uint64_t*)(a.means + ((int64_t)which * a.bh * a.mb + bj) * D + CH * g);
 #pragma unroll
-    for (int e = 0; e < CH; e += 2) {
-      const float m0 = acc[e] / c, m1 = acc[e + 1] / c;
-      dev_store(out + e / 2, (uint64_t)__float_as_uint(m0) | ((uint64_t)__float_as_uint(m1) << 32));
-      const uint32_t b0 = __float_as_uint(fabsf(m0)), b1 = __float_as_uint(fabsf(m1));
-      mx = b0 > mx ? b0 : mx;
-      mx = b1 > mx ? b1 : mx;
+    for (int e = 0; e < CH; ++e) {
+      acc[e] = acc[e] / c;
+      const uint32_t b = __float_as_uint(fabsf(acc[e]));
+      mx = b > mx ? b : mx;
+    }
+    // lane l's channels are floats [8 l, 8 l + 8) of the wavefront's 512 (its 64 / G blocks in order)
+    float4* st = (float4*)(stage + CH * (tid & 63));
+    st[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    st[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  }
+  asm volatile("" ::: "memory");  // (a wavefront's LDS operations complete in issue order)
+  {
+    // store k: floats [128 k + 2 l, +2) of the wavefront, block (128 k + 2 l) / D of its blocks
+    const int lane = tid & 63;
+    const int64_t lb0 = (wg * kThreads + (tid & ~63)) / G;  // the wavefront's first block
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int f = 128 * k + 2 * lane;
+      const int64_t lb = lb0 + f / D;
+      if (lb < 2ll * nh * a.mb) {
+        const int wb = lb < (int64_t)nh * a.mb ? 0 : 1;
+        const int64_t b_ = (int64_t)h0 * a.mb + lb - (int64_t)wb * nh * a.mb;
+        const float2 v = *(const float2*)(stage + f);
+        dev_store((uint64_t*)(a.means + ((int64_t)wb * a.bh * a.mb + b_) * D + f % D),
+                  (uint64_t)__float_as_uint(v.x) | ((uint64_t)__float_as_uint(v.y) << 32));
+      }
     }
   }
   // maximum over the G lanes of this block (every lane takes part)
@@ -180,6 +204,8 @@ struct SelLds {
   int32_t hist[kThreads / 64][256];        // one digit histogram per wavefront
   uint64_t rbits[kThreads / 64][JT];       // one row's kept bits per wavefront
 };
+
+static_assert(sizeof(SelLds<64>::sc) >= kThreads / 64 * 2048, "pooling stages 2 KB per wavefront in the score tile");
 
 // Selection role of one workgroup: query blocks [r0, r0 + ROWS) of head bh. JT (a multiple of
 // kChunk / 64 with 64 JT >= mb) is the number of scores of one row each lane holds.
@@ -498,7 +524,7 @@ __global__ __launch_bounds__(kThreads) void producer_kernel(WaProducerLaunch a, 
     // pooling of items r - s_before of group k
     const int h0 = k * pl.per, nh = min(pl.per, a.bh - h0);
     const int64_t idx = r - s_before;
-    pool_role<D>(a, h0, nh, idx, tid);
+    pool_role<D>(a, h0, nh, idx, tid, (float*)&lds.sc[0][0][0] + 512 * (tid >> 6));
     // publish: every wavefront's means and maxima (device-scope stores) have completed, then count
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
