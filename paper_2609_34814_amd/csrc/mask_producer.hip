@@ -16,8 +16,8 @@
 //               (v_mfma_i32_16x16x64_i8: 16 KV blocks x 16 query blocks per instruction),
 //               256 KV blocks per pass through a small LDS tile, so that each K code row is
 //               read once per 16 query blocks; each wavefront collects one row's scores in
-//               registers, finds the k-th largest exactly by a radix select over 8-bit digits
-//               of the score minus a floor under it (one 256-bin LDS histogram per wavefront and
+//               registers, finds the k-th largest exactly by a radix select over 10-bit digits
+//               of the score minus a floor under it (one 1,024-bin LDS histogram per wavefront and
 //               digit), keeps every larger score, the first equal scores in ascending j up to
 //               k, and the diagonal if asked, and writes the row.
 // The heads are taken in groups of about 12,000 query blocks; step k of the queue holds the
@@ -59,6 +59,44 @@ __device__ __forceinline__ void dev_store(T* p, T v) {
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Lane moves through DPP (a few cycles, where a lane shuffle is an LDS round trip): lanes that the
+// control leaves without a source, or that the row mask excludes, take `old`.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp32(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROW_MASK, 0xf, false);
+}
+// Minimum and maximum over the wavefront: xor 1 and 2 within quads, the half-row and row mirrors,
+// then the broadcasts of lanes 15 and 31 into the rows above, which leave the result in lane 63.
+__device__ __forceinline__ int wave_min(int v) {
+  v = min(v, dpp32<0xB1, 0xf>(INT32_MAX, v));
+  v = min(v, dpp32<0x4E, 0xf>(INT32_MAX, v));
+  v = min(v, dpp32<0x141, 0xf>(INT32_MAX, v));
+  v = min(v, dpp32<0x140, 0xf>(INT32_MAX, v));
+  v = min(v, dpp32<0x142, 0xa>(INT32_MAX, v));
+  v = min(v, dpp32<0x143, 0xc>(INT32_MAX, v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+__device__ __forceinline__ int wave_max(int v) {
+  v = max(v, dpp32<0xB1, 0xf>(INT32_MIN, v));
+  v = max(v, dpp32<0x4E, 0xf>(INT32_MIN, v));
+  v = max(v, dpp32<0x141, 0xf>(INT32_MIN, v));
+  v = max(v, dpp32<0x140, 0xf>(INT32_MIN, v));
+  v = max(v, dpp32<0x142, 0xa>(INT32_MIN, v));
+  v = max(v, dpp32<0x143, 0xc>(INT32_MIN, v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+// Inclusive prefix sum over the lanes: shifts by 1, 2, 4 and 8 within each row of 16, then the
+// broadcasts of lane 15 into rows 1 and 3 and of lane 31 into rows 2 and 3.
+__device__ __forceinline__ int lane_prefix_sum(int x) {
+  x += dpp32<0x111, 0xf>(0, x);  // row_shr:1
+  x += dpp32<0x112, 0xf>(0, x);  // row_shr:2
+  x += dpp32<0x114, 0xf>(0, x);  // row_shr:4
+  x += dpp32<0x118, 0xf>(0, x);  // row_shr:8
+  x += dpp32<0x142, 0xa>(0, x);  // row_bcast:15
+  x += dpp32<0x143, 0xc>(0, x);  // row_bcast:31
+  return x;
+}
 
 // Pooling role of workgroup wg: threads wg * kThreads + tid cover Q, then K, of heads [h0, h0 + nh),
 // D / kPoolCh consecutive threads (lanes of one wavefront) per block, each folding kPoolCh channels.
@@ -136,12 +174,15 @@ __device__ __forceinline__ void pool_role(const WaProducerLaunch& a, int h0, int
       }
     }
   }
-  // maximum over the G lanes of this block (every lane takes part)
-#pragma unroll
-  for (int o = G / 2; o > 0; o >>= 1) {
-    const uint32_t u = __shfl_xor(mx, o);
-    mx = u > mx ? u : mx;
-  }
+  // maximum over the G lanes of this block (every lane takes part; non-negative float bits compare
+  // like integers): xor 1 and 2 within quads, the half-row mirror, and for 16 lanes the row mirror
+  static_assert(G == 8 || G == 16, "a block's lanes are half a DPP row or a whole one");
+  int m = (int)mx;
+  m = max(m, dpp32<0xB1, 0xf>(0, m));
+  m = max(m, dpp32<0x4E, 0xf>(0, m));
+  m = max(m, dpp32<0x141, 0xf>(0, m));
+  if (G == 16) m = max(m, dpp32<0x140, 0xf>(0, m));
+  mx = (uint32_t)m;
   if (active && g == 0) dev_store(a.bmax + (int64_t)which * a.bh * a.mb + bj, mx);
 }
 
@@ -154,10 +195,7 @@ __device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which,
   const uint32_t* b = a.bmax + wh * a.mb;
   uint32_t mx = 0u;
   for (int j = tid; j < a.mb; j += kThreads) mx = b[j] > mx ? b[j] : mx;
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t u = __shfl_xor(mx, o);
-    mx = u > mx ? u : mx;
-  }
+  mx = (uint32_t)wave_max((int)mx);  // (non-negative float bits compare like integers)
   if ((tid & 63) == 0) part[tid >> 6] = mx;
   __syncthreads();
   uint32_t m = part[0];
@@ -196,12 +234,18 @@ struct SelGeom {
   static constexpr int ROWS = 16 * RG;
 };
 
+// Digits of the radix select: 10 bits (1,024 bins, 16 per lane), so that two levels resolve the
+// score ranges of 16 to 19 bits seen in practice (8-bit digits took three passes over the row).
+constexpr int kDigitBits = 10;
+constexpr int kBins = 1 << kDigitBits;
+constexpr int kBinsPerLane = kBins / 64;
+
 // LDS of the selection role
 template <int JT>
 struct SelLds {
   int32_t sc[2][SelGeom<JT>::ROWS][kChunk + 1];  // scores of two passes in turn (+1: fewer bank conflicts)
   __attribute__((aligned(16))) int8_t qs[SelGeom<JT>::ROWS][kQsStride];  // the rows' Q codes (head_dim <= 128)
-  int32_t hist[kThreads / 64][256];        // one digit histogram per wavefront
+  __attribute__((aligned(16))) int32_t hist[kThreads / 64][kBins];  // one digit histogram per wavefront
   uint64_t rbits[kThreads / 64][JT];       // one row's kept bits per wavefront
 };
 
@@ -295,12 +339,8 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
       lo = min(lo, v_[t] == INT32_MIN ? INT32_MAX : v_[t]);
       hi = max(hi, v_[t]);
     }
-    for (int o = 32; o > 0; o >>= 1) {
-      lo = min(lo, __shfl_xor(lo, o));
-      hi = max(hi, __shfl_xor(hi, o));
-    }
-    lo = __builtin_amdgcn_readfirstlane(lo);
-    hi = __builtin_amdgcn_readfirstlane(hi);
+    lo = wave_min(lo);
+    hi = wave_max(hi);
     // A floor under the keep-th largest score: each lane splits its entries into three groups
     // (t mod 3) and takes the smallest of the three group maxima; the floor is the smallest of
     // those over the lanes whose groups all hold a score. Every such group has a score at or above
@@ -318,15 +358,13 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
       }
       const bool full = g0 != INT32_MIN && g1 != INT32_MIN && g2 != INT32_MIN;
       const int n_full = __popcll(__ballot(full));
-      int f = full ? min(g0, min(g1, g2)) : INT32_MAX;
-      for (int o = 32; o > 0; o >>= 1) f = min(f, __shfl_xor(f, o));
-      f = __builtin_amdgcn_readfirstlane(f);
+      const int f = wave_min(full ? min(g0, min(g1, g2)) : INT32_MAX);
       if (3 * n_full >= keep && f < hi) base = f;
     }
     // The keep-th largest score, digit by digit of u = s - base (0 <= u <= hi - base < 2^23): at
     // each level the wavefront counts its candidates (entries whose higher digits equal the prefix
-    // found so far) in 256 bins of the next 8 bits, and the bin holding the kept-th largest
-    // candidate fixes those bits. Three levels resolve any row.
+    // found so far) in kBins bins of the next kDigitBits bits, and the bin holding the kept-th
+    // largest candidate fixes those bits. Two levels resolve a range below 2^20, three any.
     // thr: the keep-th largest score; ties: how many scores equal to thr are kept (the first ones in
     // ascending j); neq: how many scores equal thr
     int thr = lo, ties = keep, neq = mb;  // all scores equal when lo == hi
@@ -336,9 +374,13 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
       uint32_t prefix = 0u;
       int rem = keep;  // rank of the sought value among the candidates, from the top
       while (nbits > 0) {
-        const int sh = nbits > 8 ? nbits - 8 : 0;
+        const int sh = nbits > kDigitBits ? nbits - kDigitBits : 0;
+        typedef int v4i_t __attribute__((ext_vector_type(4)));
+        // lane l holds bins [kBinsPerLane (63 - l), +kBinsPerLane): the bins above a lane's are
+        // those of the lanes below it, so a prefix sum over the lanes counts them
+        v4i_t* h4 = (v4i_t*)(h + kBinsPerLane * (63 - lane));
 #pragma unroll
-        for (int b = 0; b < 4; ++b) h[4 * lane + b] = 0;
+        for (int q = 0; q < kBinsPerLane / 4; ++q) h4[q] = v4i_t{0, 0, 0, 0};
         // (the wavefront's LDS operations complete in issue order; these fences keep that order)
         asm volatile("" ::: "memory");
 #pragma unroll
@@ -349,26 +391,29 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
           if ((u >> nbits) == 0u) atomicAdd(&h[u >> sh], 1);
         }
         asm volatile("" ::: "memory");
-        int c[4];
+        int c[kBinsPerLane];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) c[b] = h[4 * lane + b];
-        asm volatile("" ::: "memory");
-        // candidates in the bins above this lane's four: suffix sum over the lanes
-        const int tot = c[0] + c[1] + c[2] + c[3];
-        int acc = tot;  // inclusive suffix sum: this lane and the lanes above it
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int x = __shfl_down(acc, o);
-          if (lane + o < 64) acc += x;
+        for (int q = 0; q < kBinsPerLane / 4; ++q) {
+          const v4i_t x = h4[q];
+          c[4 * q] = x[0];
+          c[4 * q + 1] = x[1];
+          c[4 * q + 2] = x[2];
+          c[4 * q + 3] = x[3];
         }
-        const int above = acc - tot;
-        // bin 4 lane + b holds the rem-th largest candidate when above(b) < rem <= above(b) + c[b]
+        asm volatile("" ::: "memory");
+        // candidates in the bins above this lane's: a prefix sum over the lanes
+        int tot = 0;
+#pragma unroll
+        for (int b = 0; b < kBinsPerLane; ++b) tot += c[b];
+        const int above = lane_prefix_sum(tot) - tot;
+        // bin kBinsPerLane (63 - lane) + b holds the rem-th largest candidate when
+        // above(b) < rem <= above(b) + c[b]
         int hit = -1, hit_above = 0, hit_cnt = 0;
         int ab = above;
 #pragma unroll
-        for (int b = 3; b >= 0; --b) {
+        for (int b = kBinsPerLane - 1; b >= 0; --b) {
           if (hit < 0 && ab < rem && rem <= ab + c[b]) {
-            hit = 4 * lane + b;
+            hit = kBinsPerLane * (63 - lane) + b;
             hit_above = ab;
             hit_cnt = c[b];
           }
