@@ -106,6 +106,19 @@ def test_producer_bit_exact_head_groups():
     assert np.array_equal(mask, MP.produce_mask(q, k, wl.block, 60, True))
 
 
+@pytest.mark.parametrize("batch,heads,d,blk,seq,keep", [(3, 37, 64, 64, 300, 2), (2, 100, 128, 128, 100, 1)])
+def test_producer_bit_exact_many_short_heads(batch, heads, d, blk, seq, keep):
+    """Heads of 5 blocks (ragged) and of a single block: one pooling item of the queue covers the blocks of
+    up to 64 heads of one tensor, so one workgroup writes the codes of many heads (64 at once with one
+    block per head and d 128, as many as an item holds), and one head group holds every head."""
+    wl = custom(f"short{heads}", batch=batch, heads=heads, head_dim=d, block=blk, grid=(1, 1, seq), seq_len=seq,
+                seed=40 + heads)
+    q, k, _ = make_qkv(wl)
+    mask, codes = _run(q, k, wl.block, keep, True)
+    assert np.array_equal(codes, _oracle_codes(q, k, wl.block))
+    assert np.array_equal(mask, MP.produce_mask(q, k, wl.block, keep, True))
+
+
 def test_producer_bit_exact_full_size():
     """363,600 tokens, 40 heads, 5% of the blocks per row: every row of every head."""
     wl = PRODUCER_CONFIGS["produced-long-720p-401f"]
