@@ -37,14 +37,15 @@
 namespace {
 
 // Workgroup barrier that waits only for this wavefront's LDS operations (a full __syncthreads also
-// waits for every global load in flight, which would drain the K loads issued passes ahead); the
-// compiler may not move memory accesses across it.
+// waits for every global load in flight, which would drain the K-code load issued for the next
+// pass); the compiler may not move memory accesses across it.
 #define WA_LDS_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
 constexpr int kThreads = 1024;  // every role: 16 wavefronts (selection: one 16-KV-block tile each, then rows)
 constexpr int kChunk = 256;        // KV blocks scored per pass (16 wavefronts x 16)
 // Channels folded per pooling thread: 8 (one 16-byte load per token). 4 (8-byte loads, twice the
-// threads) took 1.93 ms per call against 1.79, 16 (two loads per token) 2.67.
+// threads) took 1.93 ms per call against 1.79, 16 (two loads per token) 2.67 (measured when the
+// pipeline took one launch per step).
 constexpr int kPoolCh = 8;
 static_assert(kPoolCh == 8, "the pooling role stages its 8 means per lane as two float4");
 
@@ -226,7 +227,7 @@ __device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which,
 // distinct banks.
 constexpr int kQsStride = 144;
 
-// Query blocks per score_select workgroup: RG groups of 16 (the MFMA's 16 columns), two when the
+// Query blocks per selection item: RG groups of 16 (the MFMA's 16 columns), two when the
 // rows' scores (2 JT registers) leave room for four wavefronts per SIMD, else one.
 template <int JT>
 struct SelGeom {
@@ -240,7 +241,8 @@ constexpr int kDigitBits = 10;
 constexpr int kBins = 1 << kDigitBits;
 constexpr int kBinsPerLane = kBins / 64;
 
-// LDS of the selection role
+// LDS of the kernel: the selection role's tiles; a pooling item stages its means in the score tile
+// and the codes take their partial maxima from the histograms (items never overlap in a workgroup)
 template <int JT>
 struct SelLds {
   int32_t sc[2][SelGeom<JT>::ROWS][kChunk + 1];  // scores of two passes in turn (+1: fewer bank conflicts)
