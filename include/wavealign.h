@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define WA_ABI_VERSION 2
+#define WA_ABI_VERSION 3
 #define WA_MAX_BLOCKS 4096
 
 typedef enum wa_status {
@@ -185,6 +185,13 @@ wa_status wa_check_perm_workspace_size(const wa_shape* shape, size_t* bytes);
 wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* row_ptr, int32_t* col_idx,
                           void* stream);
 
+/* Status word of wa_produce_block_mask (device int32, nullable): zeroed by the call; bit 1
+ * is set if a selection item's wait for the codes of its head ran out. The call takes its
+ * items from a queue in which every such wait depends only on items taken earlier by running
+ * workgroups that never wait, so the bit cannot be set; if it were, the mask is not valid.
+ * Readable once the stream has passed the call. */
+enum { WA_PRODUCE_WAIT_EXPIRED = 1 };
+
 /* Pooled-score top-k block mask: a content-dependent producer of the mask the path
  * consumes (Sec. II-B: dynamic sparse attention predicts block relevance from pooled
  * Q/K features). Per head:
@@ -199,9 +206,11 @@ wa_status wa_compact_mask(const uint8_t* mask, const wa_shape* shape, int32_t* r
  *   keep      >= 0; values >= N_B keep every block
  *   mask      out uint8 [B][H][M_B][N_B], 1 = kept
  *   codes     out int8 [2][B][H][M_B][d] (Q codes, then K codes), nullable
+ *   status    out int32 device word (WA_PRODUCE_WAIT_EXPIRED), nullable, 4-byte aligned
  *   workspace >= wa_mask_producer_workspace_size(shape), 256-byte aligned. */
 wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* shape, int32_t keep, int32_t diagonal,
-                                uint8_t* mask, int8_t* codes, void* workspace, size_t workspace_bytes, void* stream);
+                                uint8_t* mask, int8_t* codes, int32_t* status, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 /* Workspace bytes needed by wa_produce_block_mask: float32 block means, per-block and
  * per-head maxima of Q and K, their int8 codes, and the call's work queue (64 + 4*B*H

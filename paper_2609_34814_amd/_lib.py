@@ -18,6 +18,7 @@ WA_ERR_HIP = -6
 WA_SKIP_AUTO, WA_SKIP_NEVER, WA_SKIP_ALWAYS = 0, 1, 2
 FLAG_FITS_CACHE, FLAG_LITTLE_WORK, FLAG_LOCAL, FLAG_UNSTRUCTURED, FLAG_DEGENERATE, FLAG_IDENTITY = 1, 2, 4, 8, 16, 64
 WA_ATTN_BAD_PERM, WA_ATTN_BAD_KV_INDEX = 1, 2
+WA_PRODUCE_WAIT_EXPIRED = 1
 WA_HEADS_IN_ORDER, WA_HEADS_INTERLEAVED = 0, 1
 WA_NOALLOC_SCRATCH_BYTES = 4 * 1024 * 1024
 
@@ -65,7 +66,7 @@ _SIGNATURES = {
     "wa_check_perm_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
     "wa_check_perm": (c_int32, [c_void_p, POINTER(WaShape), c_void_p, c_void_p, c_size_t, c_void_p]),
     "wa_produce_block_mask": (c_int32, [c_void_p, c_void_p, POINTER(WaShape), c_int32, c_int32, c_void_p, c_void_p,
-                                        c_void_p, c_size_t, c_void_p]),
+                                        c_void_p, c_void_p, c_size_t, c_void_p]),
     "wa_attn_workspace_size": (c_int32, [POINTER(WaShape), POINTER(c_size_t)]),
     "wa_sparse_attn": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(WaShape),
                                  c_float, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),

@@ -190,8 +190,9 @@ def mask_producer_workspace_size(shape: L.WaShape) -> int:
 
 def produce_block_mask(q: torch.Tensor, k: torch.Tensor, *, block: int, keep: int, diagonal: bool = True,
                        out: Optional[torch.Tensor] = None, codes_out: Optional[torch.Tensor] = None,
-                       workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Pooled-score top-k block mask uint8 [B][H][M_B][M_B] from q, k bf16 [B][H][N][d]."""
+                       workspace: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Pooled-score top-k block mask uint8 [B][H][M_B][M_B] from q, k bf16 [B][H][N][d]. ``status``: an int32
+    device tensor of one element the call zeroes and sets WA_PRODUCE_WAIT_EXPIRED in (nullable)."""
     lib = L.load()
     for t, nm in ((q, "q"), (k, "k")):
         _dev(t, nm)
@@ -207,11 +208,14 @@ def produce_block_mask(q: torch.Tensor, k: torch.Tensor, *, block: int, keep: in
         raise ValueError("out must be a uint8 tensor of B*H*M_B*M_B elements")
     if codes_out is not None and (codes_out.dtype != torch.int8 or codes_out.numel() < 2 * b * h * mb * d):
         raise ValueError("codes_out must be an int8 tensor of 2*B*H*M_B*d elements")
+    if status is not None and (status.dtype != torch.int32 or status.numel() < 1):
+        raise ValueError("status must be an int32 tensor of at least one element")
     need = mask_producer_workspace_size(shape)
     if workspace is None or workspace.numel() < need:
         workspace = _workspace(need, q.device)
     L.check(lib.wa_produce_block_mask(_ptr(q), _ptr(k), ctypes.byref(shape), int(keep), 1 if diagonal else 0,
-                                      _ptr(mask), _ptr(codes_out), _ptr(workspace), workspace.numel(), _stream()))
+                                      _ptr(mask), _ptr(codes_out), _ptr(status), _ptr(workspace), workspace.numel(),
+                                      _stream()))
     return mask
 
 

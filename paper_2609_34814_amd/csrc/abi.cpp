@@ -342,7 +342,8 @@ wa_status wa_mask_producer_workspace_size(const wa_shape* shape, size_t* bytes) 
 }
 
 wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* shape, int32_t keep, int32_t diagonal,
-                                uint8_t* mask, int8_t* codes, void* workspace, size_t workspace_bytes, void* stream) {
+                                uint8_t* mask, int8_t* codes, int32_t* status, void* workspace,
+                                size_t workspace_bytes, void* stream) {
   Dims d;
   wa_status s = check_shape(shape, &d);
   if (s != WA_OK) return s;
@@ -350,6 +351,7 @@ wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* sh
   if (keep < 0) return fail(WA_ERR_INVALID_ARG, "keep %d is negative", keep);
   if (!aligned(q, 16) || !aligned(k, 16)) return fail(WA_ERR_ALIGNMENT, "q and k must be 16-byte aligned");
   if (codes && !aligned(codes, 16)) return fail(WA_ERR_ALIGNMENT, "codes must be 16-byte aligned");
+  if (status && !aligned(status, 4)) return fail(WA_ERR_ALIGNMENT, "status must be 4-byte aligned");
   const ProducerWs L = producer_ws_layout(d);
   s = check_ws(workspace, workspace_bytes, L.total);
   if (s != WA_OK) return s;
@@ -362,6 +364,7 @@ wa_status wa_produce_block_mask(const void* q, const void* k, const wa_shape* sh
   a.codes = codes ? codes : (int8_t*)(base + L.codes);
   a.mask = mask;
   a.queue = (uint32_t*)(base + L.queue);
+  a.status = status;
   a.bh = (int32_t)d.bh; a.mb = d.mb; a.seq_len = d.n; a.block = d.blk; a.head_dim = d.d;
   a.keep = keep; a.diagonal = diagonal ? 1 : 0;
   hipError_t e = wa_launch_producer(a, (hipStream_t)stream);

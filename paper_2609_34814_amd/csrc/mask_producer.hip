@@ -494,15 +494,17 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
 
 // Queue words of one call (workspace, cleared by producer_init_kernel at the start of every call):
 //   [0]                          the next item;
-//   [1]                          set if a wait for codes ran out (see producer_kernel: it cannot);
+//   [1]                          set if a wait for codes ran out (see producer_kernel: it cannot;
+//                                the call's status word reports it too);
 //   [kQueueDone + x]             blocks of x = which * bh + head pooled so far (which: 0 Q, 1 K);
 //   [kQueueDone + 2 bh + x]      nonzero once the codes of x are written.
 constexpr int kQueueDone = 64;
 // Sleeps of about 0.25 us between looks at a flag before a wait gives up (about one second).
 constexpr uint32_t kWaitLimit = 1u << 22;
 
-__global__ __launch_bounds__(256) void producer_init_kernel(uint32_t* queue, int64_t words) {
+__global__ __launch_bounds__(256) void producer_init_kernel(uint32_t* queue, int64_t words, int32_t* status) {
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < words; e += (int64_t)gridDim.x * 256) queue[e] = 0u;
+  if (status && blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
 
 // The call's work as one sequence of items, taken in order from the queue by resident
@@ -559,6 +561,7 @@ __global__ __launch_bounds__(kThreads) void producer_kernel(WaProducerLaunch a, 
           __builtin_amdgcn_s_sleep(8);
           if (++n == kWaitLimit) {
             atomicOr(a.queue + 1, 1u);
+            if (a.status) atomicOr(a.status, WA_PRODUCE_WAIT_EXPIRED);
             break;
           }
         }
@@ -635,7 +638,8 @@ hipError_t launch_all_t(const WaProducerLaunch& a, hipStream_t stream) {
   pl.total = (pl.ng - 1) * pl.pool_full + pl.pool_last + (int64_t)a.bh * pl.tiles;
   const int64_t words = wa_producer_queue_words(a.bh);
   const int64_t init_wgs = (words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024;
-  hipLaunchKernelGGL(producer_init_kernel, dim3((unsigned)init_wgs), dim3(256), 0, stream, a.queue, words);
+  hipLaunchKernelGGL(producer_init_kernel, dim3((unsigned)init_wgs), dim3(256), 0, stream, a.queue, words,
+                     a.status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t cus = producer_resident_cus();

@@ -13,6 +13,7 @@ struct WaProducerLaunch {
   int8_t* codes;      // [2][bh][mb][head_dim]: int8 codes of Q, then K
   uint8_t* mask;      // out [bh][mb][mb]
   uint32_t* queue;    // workspace [wa_producer_queue_words(bh)]: the work queue and its flags
+  int32_t* status;    // out, nullable: WA_PRODUCE_WAIT_EXPIRED
   int32_t bh, mb, seq_len, block, head_dim, keep, diagonal;
 };
 

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_version_and_strings():
     lib = _lib()
-    assert lib.wa_abi_version() == 2
+    assert lib.wa_abi_version() == 3
     for code in (0, -1, -2, -3, -4, -6):
         assert lib.wa_status_string(code)
     p = L.WaSkipProfile()
@@ -49,6 +49,15 @@ def test_version_and_strings():
     for name, _ in L.WaSkipProfile._fields_:
         assert getattr(p, name) == getattr(ref, name), name
     assert lib.wa_default_skip_profile(None) == L.WA_ERR_INVALID_ARG
+
+
+def test_status_bits_match_the_header():
+    """The status-word bits the binding names are the header's."""
+    text = open(HEADER).read()
+    for name in ("WA_ATTN_BAD_PERM", "WA_ATTN_BAD_KV_INDEX", "WA_PRODUCE_WAIT_EXPIRED"):
+        m = re.search(rf"\b{name}\s*=\s*(\d+)", text)
+        assert m, name
+        assert int(m.group(1)) == getattr(L, name), name
 
 
 FAKE = ctypes.c_void_p(1 << 20)   # never dereferenced: every call below fails validation first
@@ -158,13 +167,14 @@ def test_produce_block_mask_validation():
     assert lib.wa_mask_producer_workspace_size(ctypes.byref(s), ctypes.byref(ws_n)) == 0
     b, h, mb, d = s.batch, s.heads, -(-s.seq_len // s.block), s.head_dim
     assert ws_n.value >= 2 * b * h * mb * d * 5
-    args = dict(q=FAKE, k=FAKE, keep=8, mask=FAKE, codes=None, ws=ctypes.c_void_p(1 << 24), ws_bytes=ws_n.value)
+    args = dict(q=FAKE, k=FAKE, keep=8, mask=FAKE, codes=None, status=None, ws=ctypes.c_void_p(1 << 24),
+                ws_bytes=ws_n.value)
 
     def call(**kw):
         a = dict(args)
         a.update(kw)
         return lib.wa_produce_block_mask(a["q"], a["k"], ctypes.byref(s), a["keep"], 1, a["mask"], a["codes"],
-                                         a["ws"], a["ws_bytes"], None)
+                                         a["status"], a["ws"], a["ws_bytes"], None)
 
     assert call(q=None) == L.WA_ERR_INVALID_ARG
     assert call(k=None) == L.WA_ERR_INVALID_ARG
@@ -172,10 +182,11 @@ def test_produce_block_mask_validation():
     assert call(keep=-1) == L.WA_ERR_INVALID_ARG
     assert call(q=ctypes.c_void_p((1 << 20) + 2)) == L.WA_ERR_ALIGNMENT
     assert call(codes=ctypes.c_void_p((1 << 20) + 8)) == L.WA_ERR_ALIGNMENT
+    assert call(status=ctypes.c_void_p((1 << 20) + 2)) == L.WA_ERR_ALIGNMENT
     assert call(ws=None) == L.WA_ERR_INVALID_ARG
     assert call(ws_bytes=ws_n.value - 1) == L.WA_ERR_WORKSPACE
     bad = L.WaShape(1, 1, 100, 96, 64)
-    assert lib.wa_produce_block_mask(FAKE, FAKE, ctypes.byref(bad), 4, 1, FAKE, None, ctypes.c_void_p(1 << 24),
+    assert lib.wa_produce_block_mask(FAKE, FAKE, ctypes.byref(bad), 4, 1, FAKE, None, None, ctypes.c_void_p(1 << 24),
                                      1 << 30, None) == L.WA_ERR_UNSUPPORTED
 
 

@@ -35,8 +35,10 @@ def _run(q, k, blk, keep, diagonal):
     b_, h_, n, d = q.shape
     mb = -(-n // blk)
     codes = torch.empty((2, b_, h_, mb, d), dtype=torch.int8, device="cuda")
-    mask = _w().produce_block_mask(qd, kd, block=blk, keep=keep, diagonal=diagonal, codes_out=codes)
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")  # the call clears it
+    mask = _w().produce_block_mask(qd, kd, block=blk, keep=keep, diagonal=diagonal, codes_out=codes, status=status)
     torch.cuda.synchronize()
+    assert int(status.item()) == 0  # no selection's wait for codes ran out
     return mask.cpu().numpy(), codes.cpu().numpy()
 
 
