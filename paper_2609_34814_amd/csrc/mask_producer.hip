@@ -41,8 +41,15 @@ namespace {
 // pass); the compiler may not move memory accesses across it.
 #define WA_LDS_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
-constexpr int kThreads = 1024;  // every role: 16 wavefronts (selection: one 16-KV-block tile each, then rows)
-constexpr int kChunk = 256;        // KV blocks scored per pass (16 wavefronts x 16)
+// Threads per workgroup, every role: 16 wavefronts, one workgroup per CU. 512 (two per CU, so that a
+// pooling and a selection item can share one; 16-row selection items) took 1.64 ms per call
+// against 1.52: the scoring passes then serve half as many rows each.
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+constexpr int kWgPerCu = 1024 / kThreads;  // resident workgroups per compute unit (four wavefronts per SIMD)
+constexpr int kChunk = 256;        // KV blocks scored per pass
+constexpr int kKvTiles = kChunk / 16 / kWaves;  // 16-KV-block MFMA tiles per wavefront and pass
+static_assert(kKvTiles >= 1 && kKvTiles * 16 * kWaves == kChunk, "a pass splits into whole tiles");
 // Channels folded per pooling thread: 8 (one 16-byte load per token). 4 (8-byte loads, twice the
 // threads) took 1.93 ms per call against 1.79, 16 (two loads per token) 2.67 (measured when the
 // pipeline took one launch per step).
@@ -227,12 +234,13 @@ __device__ __forceinline__ void codes_role(const WaProducerLaunch& a, int which,
 // distinct banks.
 constexpr int kQsStride = 144;
 
-// Query blocks per selection item: RG groups of 16 (the MFMA's 16 columns), two when the
-// rows' scores (2 JT registers) leave room for four wavefronts per SIMD, else one.
+// Query blocks per selection item: RPW rows per wavefront (two when their scores, 2 JT registers,
+// leave room for four wavefronts per SIMD, else one), in QG groups of the MFMA's 16 columns.
 template <int JT>
 struct SelGeom {
-  static constexpr int RG = JT <= 48 ? 2 : 1;
-  static constexpr int ROWS = 16 * RG;
+  static constexpr int RPW = JT <= 48 ? 2 : 1;
+  static constexpr int ROWS = kWaves * RPW;
+  static constexpr int QG = (ROWS + 15) / 16;
 };
 
 // Digits of the radix select: 10 bits (1,024 bins, 16 per lane), so that two levels resolve the
@@ -245,8 +253,8 @@ constexpr int kBinsPerLane = kBins / 64;
 // and the codes take their partial maxima from the histograms (items never overlap in a workgroup)
 template <int JT>
 struct SelLds {
-  int32_t sc[2][SelGeom<JT>::ROWS][kChunk + 1];  // scores of two passes in turn (+1: fewer bank conflicts)
-  __attribute__((aligned(16))) int8_t qs[SelGeom<JT>::ROWS][kQsStride];  // the rows' Q codes (head_dim <= 128)
+  int32_t sc[2][16 * SelGeom<JT>::QG][kChunk + 1];  // scores of two passes in turn (+1: fewer bank conflicts)
+  __attribute__((aligned(16))) int8_t qs[16 * SelGeom<JT>::QG][kQsStride];  // the rows' Q codes (d <= 128)
   __attribute__((aligned(16))) int32_t hist[kThreads / 64][kBins];  // one digit histogram per wavefront
   uint64_t rbits[kThreads / 64][JT];       // one row's kept bits per wavefront
 };
@@ -258,8 +266,9 @@ static_assert(sizeof(SelLds<64>::sc) >= kThreads / 64 * 2048, "pooling stages 2 
 template <int D, int JT>
 __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t bh, int r0, SelLds<JT>& L, int tid) {
   typedef int v4i __attribute__((ext_vector_type(4)));
-  constexpr int RG = SelGeom<JT>::RG;
+  constexpr int RPW = SelGeom<JT>::RPW;
   constexpr int ROWS = SelGeom<JT>::ROWS;
+  constexpr int QG = SelGeom<JT>::QG;
   constexpr int KS = D / 64;                      // 64-channel steps of one MFMA each
   constexpr int NCH = JT * 64 / kChunk;           // passes over the KV blocks
   constexpr int CU = kChunk / 64;                 // entries per lane and pass
@@ -272,68 +281,78 @@ __device__ __forceinline__ void select_role(const WaProducerLaunch& a, int64_t b
   const v4i zero = {0, 0, 0, 0};
   // MFMA operands: lane l holds bytes [16 (l / 16), +16) of each 64-channel step of one code row,
   // row l mod 16 (the same channel split for both operands, so each product pairs equal channels).
-  // B of group g: the Q codes of query block r0 + 16 g + l mod 16 (zero past the head), staged in
-  // LDS once and read there before each product (registers are the scarce resource here).
-  for (int e = tid; e < ROWS * (D / 16); e += kThreads) {
+  // B of group g: the Q codes of query block r0 + 16 g + l mod 16 (zero past the item or the
+  // head), staged in LDS once and read there before each product (registers are the scarce
+  // resource here).
+  for (int e = tid; e < 16 * QG * (D / 16); e += kThreads) {
     const int row = e / (D / 16), col = e % (D / 16);
     const int qr = r0 + row;
-    *(v4i*)&L.qs[row][16 * col] = qr < mb ? *(const v4i*)(qc + (int64_t)qr * D + 16 * col) : zero;
+    *(v4i*)&L.qs[row][16 * col] =
+        row < ROWS && qr < mb ? *(const v4i*)(qc + (int64_t)qr * D + 16 * col) : zero;
   }
-  // A of pass c: the K codes of KV block c kChunk + 16 w + l mod 16 (zero past the head), loaded
-  // one pass ahead. Only the passes that reach past the head check (the last one, and on short
-  // heads the ones after it).
-  auto load_k = [&](int c, v4i (&ka)[KS]) {
-    const int kv = c * kChunk + 16 * w + (lane & 15);
-    const bool in = (c + 1) * kChunk <= mb || kv < mb;
+  // A of tile tt of pass c: the K codes of KV block c kChunk + 16 (kKvTiles w + tt) + l mod 16 (zero
+  // past the head), loaded one pass ahead. Only the passes that reach past the head check (the
+  // last one, and on short heads the ones after it).
+  auto load_k = [&](int c, v4i (&ka)[kKvTiles][KS]) {
 #pragma unroll
-    for (int st = 0; st < KS; ++st)
-      ka[st] = in ? *(const v4i*)(kc + (int64_t)kv * D + 64 * st + 16 * (lane >> 4)) : zero;
+    for (int tt = 0; tt < kKvTiles; ++tt) {
+      const int kv = c * kChunk + 16 * (kKvTiles * w + tt) + (lane & 15);
+      const bool in = (c + 1) * kChunk <= mb || kv < mb;
+#pragma unroll
+      for (int st = 0; st < KS; ++st)
+        ka[tt][st] = in ? *(const v4i*)(kc + (int64_t)kv * D + 64 * st + 16 * (lane >> 4)) : zero;
+    }
   };
   // the rows' scores: entry t of lane l is KV block 64 t + l; entries past the row hold INT32_MIN
-  // and never count. Wavefront w collects query blocks r0 + w + 16 g. (mb <= kChunk NCH, so every
-  // entry of the row is written by its pass.)
-  int32_t val[RG][JT];
-  v4i ka[KS];
+  // and never count. Wavefront w collects query blocks r0 + w + kWaves r. (mb <= kChunk NCH, so
+  // every entry of the row is written by its pass.)
+  int32_t val[RPW][JT];
+  v4i ka[kKvTiles][KS];
   load_k(0, ka);
   WA_LDS_BARRIER();  // the Q codes are in LDS
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    v4i acc[RG];
+    v4i acc[kKvTiles][QG];
 #pragma unroll
-    for (int g = 0; g < RG; ++g) {
-      acc[g] = zero;
+    for (int tt = 0; tt < kKvTiles; ++tt)
 #pragma unroll
-      for (int st = 0; st < KS; ++st) {
-        const v4i qb = *(const v4i*)&L.qs[16 * g + (lane & 15)][64 * st + 16 * (lane >> 4)];
-        acc[g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ka[st], qb, acc[g], 0, 0, 0);
+      for (int g = 0; g < QG; ++g) {
+        acc[tt][g] = zero;
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+          const v4i qb = *(const v4i*)&L.qs[16 * g + (lane & 15)][64 * st + 16 * (lane >> 4)];
+          acc[tt][g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ka[tt][st], qb, acc[tt][g], 0, 0, 0);
+        }
       }
-    }
     if (c + 1 < NCH) load_k(c + 1, ka);
     // each 16 x 16 result: lane l holds KV rows 4 (l / 16) + e, query column l mod 16 of its group.
     // Passes alternate between two tiles: the barrier of pass c + 1 (every wavefront has collected
     // pass c) orders the reads of pass c before pass c + 2 overwrites that tile.
-    int32_t (&sc)[ROWS][kChunk + 1] = L.sc[c & 1];
+    int32_t (&sc)[16 * QG][kChunk + 1] = L.sc[c & 1];
 #pragma unroll
-    for (int g = 0; g < RG; ++g)
+    for (int tt = 0; tt < kKvTiles; ++tt)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sc[16 * g + (lane & 15)][16 * w + 4 * (lane >> 4) + e] = acc[g][e];
+      for (int g = 0; g < QG; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          sc[16 * g + (lane & 15)][16 * (kKvTiles * w + tt) + 4 * (lane >> 4) + e] = acc[tt][g][e];
     WA_LDS_BARRIER();
 #pragma unroll
-    for (int g = 0; g < RG; ++g)
+    for (int r = 0; r < RPW; ++r)
 #pragma unroll
       for (int u = 0; u < CU; ++u) {
         const int j = c * kChunk + 64 * u + lane;
-        const int x = sc[w + 16 * g][64 * u + lane];  // (past the head: a product with zero codes)
-        val[g][c * CU + u] = (c + 1) * kChunk <= mb || j < mb ? x : INT32_MIN;
+        const int x = sc[w + kWaves * r][64 * u + lane];  // (past the head: a product with zero codes)
+        val[r][c * CU + u] = (c + 1) * kChunk <= mb || j < mb ? x : INT32_MIN;
       }
   }
   const int keep = a.keep < mb ? a.keep : mb;
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
-  for (int g = 0; g < RG; ++g) {
-    if (w + 16 * g >= nr) break;
-    const int i = r0 + w + 16 * g;
-    const int32_t (&v_)[JT] = val[g];
+  for (int r = 0; r < RPW; ++r) {
+    if (w + kWaves * r >= nr) break;
+    const int i = r0 + w + kWaves * r;
+    const int32_t (&v_)[JT] = val[r];
     // (a score is at most 128 x 127 x 127 in magnitude, so INT32_MIN marks exactly the missing entries)
     int lo = INT32_MAX, hi = INT32_MIN;
 #pragma unroll
@@ -518,7 +537,8 @@ struct ProducerPlan {
 };
 
 template <int D, int JT>
-__global__ __launch_bounds__(kThreads) void producer_kernel(WaProducerLaunch a, ProducerPlan pl) {
+// (launch bounds: four wavefronts per SIMD, so 128 registers per lane and kWgPerCu workgroups per CU)
+__global__ __launch_bounds__(kThreads, 4) void producer_kernel(WaProducerLaunch a, ProducerPlan pl) {
   constexpr int ROWS = SelGeom<JT>::ROWS;
   constexpr int G = D / kPoolCh;
   __shared__ SelLds<JT> lds;
@@ -642,8 +662,8 @@ hipError_t launch_all_t(const WaProducerLaunch& a, hipStream_t stream) {
                      a.status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t cus = producer_resident_cus();
-  const int64_t grid = pl.total < cus ? pl.total : cus;
+  const int64_t slots = (int64_t)producer_resident_cus() * kWgPerCu;
+  const int64_t grid = pl.total < slots ? pl.total : slots;
   hipLaunchKernelGGL((producer_kernel<D, JT>), dim3((unsigned)grid), dim3(kThreads), 0, stream, a, pl);
   return hipGetLastError();
 }
