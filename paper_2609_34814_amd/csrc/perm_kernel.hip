@@ -143,6 +143,37 @@ struct Head {
   int m, n, nw, mw;
 };
 
+// Cholesky factor of the 2 x 2 Gram matrix g of a block Z (exact sums of its entries shifted to 24
+// bits): r11, r12, r22, and whether the second column keeps a direction of its own (its residual u
+// above G22 2^-30). One IEEE fp64 rounding per operation, no contraction.
+struct Chol {
+  double r11, r12, r22;
+  bool rank2;
+};
+__device__ __forceinline__ Chol chol2(const int64_t (&g)[3]) {
+  const double G11 = (double)g[0], G12 = (double)g[1], G22 = (double)g[2];
+  Chol c;
+  c.r11 = __builtin_sqrt(G11);
+  c.r12 = G12 / c.r11;
+  const double u = G22 - c.r12 * c.r12;
+  c.rank2 = u > G22 * 0x1p-30;
+  c.r22 = c.rank2 ? __builtin_sqrt(u) : 0.0;
+  return c;
+}
+
+// Row (x0, x1) of the orthonormal factor X = Z R^-1 in 2^30 fixed point, from the row of Z shifted
+// right by the Gram shift (z0s, z1s); the second entry is 0 when Z has rank one.
+__device__ __forceinline__ void orth_row(const Chol& c, int64_t z0s, int64_t z1s, int32_t& x0, int32_t& x1) {
+  const double q0 = (double)z0s / c.r11;
+  x0 = (int32_t)__builtin_rint(q0 * 1073741824.0);
+  if (c.rank2) {
+    const double q1 = ((double)z1s - c.r12 * q0) / c.r22;
+    x1 = (int32_t)__builtin_rint(q1 * 1073741824.0);
+  } else {
+    x1 = 0;
+  }
+}
+
 // Cholesky-QR of Z (thread-owned rows i = tid + k NT, zr[k]) into sh.xs; true if degenerate.
 __device__ bool orth(Shared& sh, const Head& H, const int64_t (&zr)[PER][2]) {
   const int tid = threadIdx.x;
@@ -169,32 +200,18 @@ __device__ bool orth(Shared& sh, const Head& H, const int64_t (&zr)[PER][2]) {
   block_sum<3>(sh, g);
   if (g[0] == 0) return true;
   if (tid == 0) {
-    const double G11 = (double)g[0], G12 = (double)g[1], G22 = (double)g[2];
-    const double r11 = __builtin_sqrt(G11);
-    const double r12 = G12 / r11;
-    const double u = G22 - r12 * r12;
-    const bool rank2 = u > G22 * 0x1p-30;
-    sh.dbl[0] = r11;
-    sh.dbl[1] = r12;
-    sh.dbl[2] = rank2 ? __builtin_sqrt(u) : 0.0;
-    sh.i32[0] = rank2 ? 1 : 0;
+    const Chol c = chol2(g);
+    sh.dbl[0] = c.r11;
+    sh.dbl[1] = c.r12;
+    sh.dbl[2] = c.r22;
+    sh.i32[0] = c.rank2 ? 1 : 0;
   }
   __syncthreads();
-  const double r11 = sh.dbl[0], r12 = sh.dbl[1], r22 = sh.dbl[2];
-  const bool rank2 = sh.i32[0] != 0;
+  const Chol c = {sh.dbl[0], sh.dbl[1], sh.dbl[2], sh.i32[0] != 0};
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int i = tid + k * NT;
-    if (i < H.m) {
-      const double q0 = (double)(zr[k][0] >> s) / r11;
-      sh.xs[2 * i] = (int32_t)__builtin_rint(q0 * 1073741824.0);
-      if (rank2) {
-        const double q1 = ((double)(zr[k][1] >> s) - r12 * q0) / r22;
-        sh.xs[2 * i + 1] = (int32_t)__builtin_rint(q1 * 1073741824.0);
-      } else {
-        sh.xs[2 * i + 1] = 0;
-      }
-    }
+    if (i < H.m) orth_row(c, zr[k][0] >> s, zr[k][1] >> s, sh.xs[2 * i], sh.xs[2 * i + 1]);
   }
   __syncthreads();
   return false;
@@ -967,6 +984,255 @@ __global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
   finish_head(a, sh, h, degen, hi.nnz, hi.sum_c2, hi.flags, maxy, zr, hi.adj_and, hi.adj_or);
 }
 
+// ---------------------------------------------------------------------------------------------
+// The whole permutation of a head in one workgroup, with both centred products on the matrix cores.
+//
+// An integer v with |v| < 2^31 - 2^23 is the sum of its four balanced base-256 digits,
+// v = sum_b d_b 256^b with d_b in [-128, 127] (d_0 is the low byte read as a signed byte, then
+// v <- (v - d_0) / 256, exactly, and so on). So M^T X = sum_b 256^b (M^T D_b), where D_b holds digit
+// b of every entry of X: each term is a product of a 0/1 matrix and an int8 matrix, whose int32
+// sums are exact (at most 1024 * 128 in magnitude), and the terms are combined exactly in int64.
+// One v_mfma_i32_16x16x64_i8 takes 64 rows of 16 columns of M: A = the eight digit rows (two
+// columns of X, four digits each; rows 8-15 zero), B = the 16 columns' bits. Lane l supplies bits
+// [16 (l / 16), +16) of the 64-bit word of line 16 t + l mod 16, expanded to one byte per bit, and
+// the digits of the same 16 rows; it receives digit rows 4 (l / 16) .. +3 of that line, so lanes
+// 0-15 hold the line's product with the first column of X and lanes 16-31 with the second. M Ys
+// reads the row words the same way. The products are the same integers as the sparse sums of the
+// sliced form, so the result is the same bit for bit; what this form removes is the latency of the
+// sparse walks and their LDS atomics.
+constexpr int kMfmaMax = NT;  // rows and columns of the heads built in this form: one row or column a thread
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+struct MfmaLds {
+  int8_t xd[8][kMfmaMax];    // digit rows of X: row 4 k + b holds digit b of column k (zero past m)
+  int8_t yd[8][kMfmaMax];    // the same for Ys (zero past n)
+  int64_t v[2 * kMfmaMax];   // Ym of the first product, then Z of the second: [line][column of X]
+  int32_t cc[kMfmaMax];      // column counts
+  int64_t red[2][4][NWAVE];  // wavefront partials of the reductions, two alternating slot sets
+};
+constexpr size_t kMfmaLdsOffset = (sizeof(Shared) + 15) & ~(size_t)15;
+
+// 16 bits -> 16 bytes of 0 or 1: byte t = bit t (each nibble spread by one 24-bit multiply)
+__device__ __forceinline__ v4i bits_to_bytes(uint32_t b) {
+  v4i r;
+  r[0] = (int)(((b & 0xFu) * 0x204081u) & 0x01010101u);
+  r[1] = (int)((((b >> 4) & 0xFu) * 0x204081u) & 0x01010101u);
+  r[2] = (int)((((b >> 8) & 0xFu) * 0x204081u) & 0x01010101u);
+  r[3] = (int)((((b >> 12) & 0xFu) * 0x204081u) & 0x01010101u);
+  return r;
+}
+
+// Balanced base-256 digits of v into digit rows row0 .. row0 + 3, column idx.
+__device__ __forceinline__ void put_digits(int8_t (*d)[kMfmaMax], int row0, int idx, int32_t v) {
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int8_t db = (int8_t)(uint8_t)(uint32_t)v;
+    d[row0 + b][idx] = db;
+    v = (v - (int32_t)db) >> 8;  // exact: v - db is a multiple of 256
+  }
+}
+
+// Scheduling fence between the phases of the matrix-core form: no instruction moves across it. Left
+// alone, the compiler interleaves the phases (the products, the reductions, the fp64 Cholesky factor)
+// in a way that made the kernel three times slower than the same code with these fences.
+#define WA_PHASE_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// Sum over the 16 lanes of each DPP row (quad exchanges, then the half-row and row mirrors); every
+// lane of the row receives the row's total.
+__device__ __forceinline__ int64_t row16_sum(int64_t v) {
+  uint64_t u = (uint64_t)v;
+  u += dpp64<0xB1, 0xf>(u);   // quad_perm [1,0,3,2]
+  u += dpp64<0x4E, 0xf>(u);   // quad_perm [2,3,0,1]
+  u += dpp64<0x141, 0xf>(u);  // row_half_mirror
+  u += dpp64<0x140, 0xf>(u);  // row_mirror
+  return (int64_t)u;
+}
+__device__ __forceinline__ uint64_t row16_max(uint64_t v) {
+  v = max64(v, dpp64<0xB1, 0xf>(v));
+  v = max64(v, dpp64<0x4E, 0xf>(v));
+  v = max64(v, dpp64<0x141, 0xf>(v));
+  v = max64(v, dpp64<0x140, 0xf>(v));
+  return v;
+}
+
+// Exact int64 sums of K values (or the maximum of one) over the workgroup, returned to every thread:
+// each wavefront reduces its lanes, parks its partial in LDS, and after the barrier lanes 0-15 of
+// every wavefront read the NWAVE partials (one read each) and reduce them within their DPP row.
+// Consecutive reductions alternate between the two slot sets (buf), so a wavefront that writes the
+// partials of the next reduction never overwrites ones that another is still reading. One barrier,
+// which also publishes every LDS write made before the call.
+static_assert(NWAVE == 16, "the partials are reduced within one 16-lane DPP row");
+template <int K>
+__device__ __forceinline__ void wg_sum(int64_t (*red)[4][NWAVE], int buf, int64_t (&v)[K]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  WA_PHASE_FENCE();
+#pragma unroll
+  for (int k = 0; k < K; ++k) v[k] = wave_sum(v[k]);
+  if (lane == 0)
+#pragma unroll
+    for (int k = 0; k < K; ++k) red[buf][k][w] = v[k];
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int64_t p = lane < NWAVE ? red[buf][k][lane] : 0;
+    const int64_t t = row16_sum(p);
+    v[k] = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)((uint64_t)t >> 32), 0) << 32) |
+                     (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(uint64_t)t, 0));
+  }
+  WA_PHASE_FENCE();
+}
+__device__ __forceinline__ uint64_t wg_max(int64_t (*red)[4][NWAVE], int buf, uint64_t v) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  WA_PHASE_FENCE();
+  v = wave_max(v);
+  if (lane == 0) red[buf][0][w] = (int64_t)v;
+  __syncthreads();
+  const uint64_t t = row16_max(lane < NWAVE ? (uint64_t)red[buf][0][lane] : 0ull);
+  const uint64_t r = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(t >> 32), 0) << 32) |
+                     (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)t, 0);
+  WA_PHASE_FENCE();
+  return r;
+}
+
+// Exact products of the digit rows dg with the bitmask of `lines` lines (word s of line j at
+// bits16[4 (s lines + j) .. +3], `words` words a line). The wavefront takes the 16-line tiles
+// w, w + NWAVE, ...; for each, f(line, column, value) is called in lanes 0-31 with the product of
+// line 16 tile + l mod 16 with column l / 16 of the digit block (line may lie past `lines`).
+template <typename F>
+__device__ __forceinline__ void mfma_product(const int8_t (*dg)[kMfmaMax], const uint16_t* bits16, int lines,
+                                             int words, F&& f) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 15, q = lane >> 4;
+  const v4i zero = {0, 0, 0, 0};
+  constexpr int CH = 4;  // words whose bits are loaded together
+  WA_PHASE_FENCE();
+  for (int tile = w; 16 * tile < lines; tile += NWAVE) {
+    const int line = 16 * tile + r;
+    v4i acc = zero;
+    for (int s0 = 0; s0 < words; s0 += CH) {
+      uint32_t bt[CH];
+#pragma unroll
+      for (int u = 0; u < CH; ++u)
+        bt[u] = s0 + u < words && line < lines ? bits16[((int64_t)(s0 + u) * lines + line) * 4 + q] : 0u;
+#pragma unroll
+      for (int u = 0; u < CH; ++u) {
+        if (s0 + u < words) {
+          const v4i av = r < 8 ? *(const v4i*)&dg[r][64 * (s0 + u) + 16 * q] : zero;
+          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bits_to_bytes(bt[u]), acc, 0, 0, 0);
+        }
+      }
+    }
+    if (q < 2) f(line, q, (int64_t)acc[0] + 256ll * acc[1] + 65536ll * acc[2] + 16777216ll * acc[3]);
+  }
+  WA_PHASE_FENCE();
+}
+
+__global__ __launch_bounds__(NT) void perm_mfma_kernel(WaPermLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
+  MfmaLds& L = *reinterpret_cast<MfmaLds*>(smem_raw + kMfmaLdsOffset);
+  const int h = blockIdx.x;
+  const HeadInit hi = init_head(a, sh, h);
+  if (hi.status == HEAD_DONE) return;
+  bool degen = hi.status == HEAD_DEGENERATE;
+  int64_t zr[PER][2] = {};
+  uint64_t maxy = 0;
+  if (!degen) {
+    const int tid = threadIdx.x;  // row tid (QR) and column tid (Ys) of the head
+    const int m = a.m, n = a.n;
+    const int64_t mm = m;
+    const Head H = head_of(a, h);
+    const uint16_t* cb16 = reinterpret_cast<const uint16_t*>(H.colbits);
+    const uint16_t* rb16 = reinterpret_cast<const uint16_t*>(H.rowbits);
+    // digit rows start at zero (their padding past m and n stays zero); X of the seeded start
+    for (int e = tid; e < 8 * kMfmaMax / 4; e += NT) {
+      reinterpret_cast<int32_t*>(L.xd)[e] = 0;
+      reinterpret_cast<int32_t*>(L.yd)[e] = 0;
+    }
+    L.cc[tid] = tid < n ? a.cc[(int64_t)h * n + tid] : 0;
+    __syncthreads();
+    int64_t sx[2] = {0, 0};  // 1^T X
+    if (tid < m) {
+      const int32_t x0 = sh.xs[2 * tid], x1 = sh.xs[2 * tid + 1];
+      put_digits(L.xd, 0, tid, x0);
+      put_digits(L.xd, 4, tid, x1);
+      sx[0] = x0;
+      sx[1] = x1;
+    }
+    int rb = 0;                      // reductions so far (selects the slot set)
+    wg_sum<2>(L.red, rb++ & 1, sx);  // its barrier also publishes the digits
+    for (int it = 0; it <= a.iters; ++it) {
+      // ---- Ym = m M^T X - c (1^T X), and max |Ym| ----
+      uint64_t mx = 0;
+      mfma_product(L.xd, cb16, n, H.mw, [&](int j, int k, int64_t ya) {
+        if (j < n) {
+          const int64_t y = mm * ya - (int64_t)L.cc[j] * (k == 0 ? sx[0] : sx[1]);
+          L.v[2 * j + k] = y;
+          mx = max64(mx, uabs64(y));
+        }
+      });
+      maxy = wg_max(L.red, rb++ & 1, mx);  // its barrier also publishes Ym
+      const int bly = bitlen_u64(maxy);
+      const int sy = bly > 30 ? bly - 30 : 0;
+      // ---- Ys = Ym >> sy as digit rows, and c^T Ys ----
+      int64_t py[2] = {0, 0};
+      if (tid < n) {
+        const int32_t v0 = (int32_t)(L.v[2 * tid] >> sy), v1 = (int32_t)(L.v[2 * tid + 1] >> sy);
+        put_digits(L.yd, 0, tid, v0);
+        put_digits(L.yd, 4, tid, v1);
+        py[0] = (int64_t)L.cc[tid] * v0;
+        py[1] = (int64_t)L.cc[tid] * v1;
+      }
+      wg_sum<2>(L.red, rb++ & 1, py);  // its barrier also publishes the Ys digits (Ym is read)
+      // ---- Z = m M Ys - 1 (c^T Ys), and max |Z| ----
+      uint64_t mz = 0;
+      mfma_product(L.yd, rb16, m, H.nw, [&](int i, int k, int64_t za) {
+        if (i < m) {
+          const int64_t z = mm * za - (k == 0 ? py[0] : py[1]);
+          L.v[2 * i + k] = z;
+          mz = max64(mz, uabs64(z));
+        }
+      });
+      mz = wg_max(L.red, rb++ & 1, mz);  // its barrier also publishes Z
+      int64_t z0 = 0, z1 = 0;
+      if (tid < m) {
+        z0 = L.v[2 * tid];
+        z1 = L.v[2 * tid + 1];
+      }
+      if (it == a.iters) {  // the last product: Rayleigh-Ritz in the finishing phases
+        zr[0][0] = z0;
+        zr[0][1] = z1;
+        break;
+      }
+      // ---- Cholesky-QR: X = Z R^-1 ----
+      const int blz = bitlen_u64(mz);
+      const int s = blz > 24 ? blz - 24 : 0;
+      const int64_t z0s = z0 >> s, z1s = z1 >> s;
+      int64_t g[3] = {z0s * z0s, z0s * z1s, z1s * z1s};
+      wg_sum<3>(L.red, rb++ & 1, g);
+      if (g[0] == 0) {  // uniform: every thread holds the same sums
+        degen = true;
+        break;
+      }
+      const Chol c = chol2(g);
+      sx[0] = 0;
+      sx[1] = 0;
+      if (tid < m) {
+        int32_t x0, x1;
+        orth_row(c, z0s, z1s, x0, x1);
+        sh.xs[2 * tid] = x0;
+        sh.xs[2 * tid + 1] = x1;
+        put_digits(L.xd, 0, tid, x0);
+        put_digits(L.xd, 4, tid, x1);
+        sx[0] = x0;
+        sx[1] = x1;
+      }
+      wg_sum<2>(L.red, rb++ & 1, sx);  // its barrier also publishes X and its digits
+    }
+  }
+  finish_head(a, sh, h, degen, hi.nnz, hi.sum_c2, hi.flags, maxy, zr, hi.adj_and, hi.adj_or);
+}
+
 // Arithmetic self-check: the fp64 operations the permutation relies on, evaluated on the GPU.
 __global__ void fp64_probe_kernel(const double* a, const double* b, const int64_t* c, double* out, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -994,6 +1260,10 @@ int wa_perm_slices(int n) { return (n + GT - 1) / GT; }
 #endif
 constexpr int kFusedMaxSlices = WA_PERM_FUSED_MAX_SLICES;
 constexpr size_t kLdsBytes = 160 * 1024;  // LDS of one gfx950 workgroup
+#ifndef WA_PERM_MFMA_FORM_MAX
+#define WA_PERM_MFMA_FORM_MAX 1024
+#endif
+constexpr int kMfmaFormMax = WA_PERM_MFMA_FORM_MAX;
 
 // Launch sequence on one stream: init; iters x (gather, scatter, orth); gather, scatter, finish; or
 // the fused kernel alone. The statistics-only form runs init alone.
@@ -1010,6 +1280,14 @@ hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   hipError_t e = hipFuncSetAttribute((const void*)apply_scatter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)zsmem);
   if (e != hipSuccess) return e;
+  const size_t msmem = kMfmaLdsOffset + sizeof(MfmaLds);
+  if (!a.stats_only && a.m <= kMfmaFormMax && a.n <= kMfmaFormMax) {
+    static_assert(kMfmaFormMax <= kMfmaMax, "the matrix-core form holds at most kMfmaMax lines");
+    e = hipFuncSetAttribute((const void*)perm_mfma_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(perm_mfma_kernel, dim3(a.bh), dim3(NT), msmem, stream, a);
+    return hipGetLastError();
+  }
   const size_t fsmem = smem + (size_t)2 * a.m * sizeof(unsigned long long) +
                        (size_t)((a.m + 63) / 64) * a.n * sizeof(uint64_t);
   if (!a.stats_only && a.slices <= kFusedMaxSlices && fsmem <= kLdsBytes) {
