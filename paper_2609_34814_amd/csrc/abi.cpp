@@ -148,14 +148,14 @@ const wa_skip_profile kDefaultProfile = {
     96.0 * 1024.0 * 1024.0,  // cache_bytes: K/V per head below which reordering did not pay (the shared
                              // 256 MiB last-level cache holds it next to the streamed Q, O and V^T)
     0.5,                     // gain_ns_per_block: attention time saved per kept block where it paid
-    8419.0,                  // ovh_ns_fixed    } permutation time per head of more than 512 blocks (the
-    4.39,                    // ovh_ns_per_row  } sliced form), amortised over concurrent heads,
-    0.0547,                  // ovh_ns_per_nnz  } least-squares fit over the sweep (worst residual 14%)
+    11575.0,                 // ovh_ns_fixed    } permutation time per head of more than 1024 blocks (the
+    2.96,                    // ovh_ns_per_row  } sliced form), amortised over concurrent heads,
+    0.0565,                  // ovh_ns_per_nnz  } least-squares fit over the sweep (worst residual 11%)
     0.2,                     // j_max: adjacent rows of raster-local heads share 23-40% of their blocks
     0.05,                    // eta_min
-    512.0,                   // fused_max_blocks: heads built by one workgroup (at most two 256-column slices)
-    1297.0,                  // ovh_fused_ns_fixed   } the one-workgroup form's time per head, fitted alone
-    16.88,                   // ovh_fused_ns_per_row } (worst residual 3%)
+    1024.0,                  // fused_max_blocks: heads built by one workgroup (the matrix-core form)
+    1199.0,                  // ovh_fused_ns_fixed   } the one-workgroup form's time per head, fitted alone
+    10.70,                   // ovh_fused_ns_per_row } (worst residual 6%)
     0.0,                     // ovh_fused_ns_per_nnz }
 };
 

@@ -5,14 +5,13 @@
 //      distinct columns, adjacent-row overlap, sum c_j^2);
 //   1  skip cases 1-3 (fits in cache, too little work, already local);
 //   2  matrix-free centred subspace iteration in exact fixed point: the centred
-//      products are integer sums over the set bits of the packed mask plus the
-//      rank-one centring corrections scaled by m (Alg. 1), spread over one
-//      workgroup per 256-column slice of every head; the 2-column QR is a
-//      Cholesky-QR of the exactly summed Gram matrix (one IEEE fp64 rounding per
-//      operation, no contraction); then Rayleigh-Ritz with one Jacobi rotation
-//      and a canonical column sign;
+//      products are exact integer products of the packed mask with X (or Ys)
+//      plus the rank-one centring corrections scaled by m (Alg. 1); the
+//      2-column QR is a Cholesky-QR of the exactly summed Gram matrix (one IEEE
+//      fp64 rounding per operation, no contraction); then Rayleigh-Ritz with
+//      one Jacobi rotation and a canonical column sign;
 //   3  skip case 4 (the rank-2 embedding keeps too little of ||M~||_F^2);
-//   4  Stage 1: bitonic sort of the rows by polar angle (Eq. 4) with an exact
+//   4  Stage 1: sort of the rows by polar angle (Eq. 4) with an exact
 //      integer comparator (half-plane class, then the sign of the cross product,
 //      then the row index);
 //   5  Stage 2: the order is cut into n_xcd contiguous segments of equal work
@@ -21,13 +20,17 @@
 //      (bucket, -n_i, position) keys sorts every bucket by descending n_i,
 //      stably. The segment table is an output: the attention kernel runs
 //      segment x on XCD x.
-// Phases 0-1 and the first QR run in perm_init_kernel, each further QR in
-// orth_step_kernel and phases 3-5 in perm_finish_kernel (one 1024-thread
-// workgroup per head each); the centred products run in apply_gather_kernel and
-// apply_scatter_kernel. Per-head state between the kernels lives in the
-// workspace. Every sum is an exact integer, so neither the order of parallel
-// reductions nor the slicing matters and the result is reproducible bit for bit.
-// Supports m, n <= 4096.
+// Two forms, both exact, so the same result bit for bit:
+//   * heads of at most 1024 rows and columns: perm_mfma_kernel, one 1024-thread workgroup per head
+//     and one launch for all heads; the centred products are int8 matrix-core products of the
+//     mask bits with the base-256 digits of X and Ys (see the kernel);
+//   * larger heads: phases 0-1 and the first QR in perm_init_kernel, each further QR in
+//     orth_step_kernel and phases 3-5 in perm_finish_kernel (one 1024-thread workgroup per head
+//     each); the centred products as sparse sums over the set bits in apply_gather_kernel and
+//     apply_scatter_kernel, one workgroup per 256-column slice of every head. Per-head state
+//     between the kernels lives in the workspace.
+// Every sum is an exact integer, so neither the order of parallel reductions nor the slicing nor the
+// form matters. Supports m, n <= 4096.
 
 #pragma clang fp contract(off)
 
@@ -257,23 +260,6 @@ __device__ __forceinline__ int64_t group_sum(int64_t v, int t) {
   return v;
 }
 
-// Calls f(k) for every set bit k in [b0, b1) of a word-major bitmask line.
-template <typename F>
-__device__ __forceinline__ void for_bits_range(const uint64_t* words, int64_t stride, int line, int b0, int b1,
-                                               F&& f) {
-  if (b0 >= b1) return;
-  for (int w = b0 >> 6; w <= (b1 - 1) >> 6; ++w) {
-    uint64_t word = words[(int64_t)w * stride + line];
-    const int base = w * 64;
-    if (b0 > base) word &= ~0ull << (b0 - base);
-    if (b1 - base < 64) word &= (1ull << (b1 - base)) - 1ull;
-    while (word) {
-      f(base + __ffsll((long long)word) - 1);
-      word &= word - 1;
-    }
-  }
-}
-
 // ---------------------------------------------------------------------------------------------
 // Centred products across many workgroups. One subspace step X -> Z = m * M~ Ys, with
 // Ys = (m * M~^T X) >> sy, runs as two slice kernels (one 256-thread workgroup per 256-column
@@ -472,16 +458,23 @@ __device__ void compute_segments(Shared& sh, const int32_t* row_nnz, int m, int 
   const int lo = min(tid * per, m), hi = min(lo + per, m);
   int32_t local = 0;
   for (int p = lo; p < hi; ++p) local += row_nnz[sh.cc[p]] + 1;
-  sh.part[tid] = local;
-  __syncthreads();
-  for (int off = 1; off < NT; off <<= 1) {
-    const int32_t v = tid >= off ? sh.part[tid - off] : 0;
-    __syncthreads();
-    sh.part[tid] += v;
-    __syncthreads();
+  // prefix sums of the thread totals: within the wavefront by lane shifts, then over the wavefront totals
+  const int lane = tid & 63, w = tid >> 6;
+  int32_t incl = local;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
   }
-  const int64_t total = sh.part[NT - 1];
-  int32_t run = tid > 0 ? sh.part[tid - 1] : 0;   // W_lo
+  if (lane == 63) sh.part[w] = incl;
+  __syncthreads();
+  int32_t before = 0, sum = 0;
+  for (int i = 0; i < NWAVE; ++i) {
+    const int32_t t = sh.part[i];
+    before += i < w ? t : 0;
+    sum += t;
+  }
+  const int64_t total = sum;
+  int32_t run = before + incl - local;   // W_lo
   int32_t* segof = sh.xs;
   for (int p = lo; p < hi; ++p) {
     const int64_t x = ((int64_t)n_xcd * run) / total;
@@ -889,101 +882,6 @@ __global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
   finish_head(a, sh, h, degen, S->nnz, S->sum_c2, S->flags, S->maxy, zr, S->adj_and, S->adj_or);
 }
 
-// The whole permutation of a head in one workgroup, for heads too small to fill the chip with column
-// slices: the same exact integer products as the slice kernels (so the same result), with X kept in
-// LDS between the steps.
-//   apply: Z = m * M~ Ys, Ys = (m * M~^T X) >> sy, for X in sh.xs; maxy = max |m * M~^T X|.
-// Both products walk the column bitmask (held in LDS by the caller), lanes_per_line lanes per column:
-// Ym gathers the column's rows, then M Ys scatters Ys[j] into the column's rows with 64-bit LDS
-// atomics. Walking columns keeps the lanes balanced (row counts are heavy-tailed, column counts are
-// not), and every sum is an exact integer. c_line: the column count of the lane's column.
-__device__ void apply_head(const WaPermLaunch& a, Shared& sh, unsigned long long* za, const uint64_t* colbits,
-                           int64_t c_line, int64_t (&zr)[PER][2], uint64_t& maxy) {
-  const int tid = threadIdx.x;
-  const int m = a.m, n = a.n;
-  const int t = lanes_per_line(n);
-  const int line = tid / t, sub = tid % t;
-  const int rc = (m + t - 1) / t;
-  const int r0 = min(sub * rc, m), r1 = min(sub * rc + rc, m);
-  int64_t sx[2] = {0, 0};
-  for (int i = tid; i < m; i += NT) {
-    sx[0] += sh.xs[2 * i];
-    sx[1] += sh.xs[2 * i + 1];
-  }
-  block_sum<2>(sh, sx);
-  // Ym of column `line`: its rows in this lane's chunk, then the group's sum
-  int64_t y0 = 0, y1 = 0;
-  if (line < n)
-    for_bits_range(colbits, n, line, r0, r1, [&](int i) {
-      y0 += sh.xs[2 * i];
-      y1 += sh.xs[2 * i + 1];
-    });
-  y0 = group_sum(y0, t);
-  y1 = group_sum(y1, t);
-  int64_t ym0 = 0, ym1 = 0;
-  const int64_t c = c_line;
-  uint64_t mx = 0;
-  if (line < n) {
-    ym0 = (int64_t)m * y0 - c * sx[0];
-    ym1 = (int64_t)m * y1 - c * sx[1];
-    const uint64_t p = uabs64(ym0), q = uabs64(ym1);
-    mx = p > q ? p : q;
-  }
-  for (int i = tid; i < 2 * m; i += NT) za[i] = 0ull;
-  maxy = block_max(sh, mx);  // its barriers also complete the clearing of za
-  const int bl = bitlen_u64(maxy);
-  const int sy = bl > 30 ? bl - 30 : 0;
-  int64_t py[2] = {0, 0};
-  if (line < n) {
-    const int32_t v0 = (int32_t)(ym0 >> sy), v1 = (int32_t)(ym1 >> sy);
-    if (sub == 0) {
-      py[0] = c * v0;
-      py[1] = c * v1;
-    }
-    const unsigned long long u0 = (unsigned long long)(int64_t)v0, u1 = (unsigned long long)(int64_t)v1;
-    for_bits_range(colbits, n, line, r0, r1, [&](int i) {
-      atomicAdd(&za[2 * i], u0);
-      atomicAdd(&za[2 * i + 1], u1);
-    });
-  }
-  block_sum<2>(sh, py);  // its barriers also complete the scatter
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int i = tid + k * NT;
-    zr[k][0] = i < m ? (int64_t)m * (int64_t)za[2 * i] - py[0] : 0;
-    zr[k][1] = i < m ? (int64_t)m * (int64_t)za[2 * i + 1] - py[1] : 0;
-  }
-  __syncthreads();  // every thread has read za before the next step clears it
-}
-
-__global__ __launch_bounds__(NT) void perm_fused_kernel(WaPermLaunch a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-  Shared& sh = *reinterpret_cast<Shared*>(smem_raw);
-  unsigned long long* za = reinterpret_cast<unsigned long long*>(smem_raw + sizeof(Shared));  // [2 m]
-  uint64_t* cb = reinterpret_cast<uint64_t*>(za + 2 * a.m);  // the head's column bitmask [mw][n]
-  const int h = blockIdx.x;
-  const HeadInit hi = init_head(a, sh, h);
-  if (hi.status == HEAD_DONE) return;
-  bool degen = hi.status == HEAD_DEGENERATE;
-  int64_t zr[PER][2] = {};
-  uint64_t maxy = 0;
-  if (!degen) {
-    const Head H = head_of(a, h);
-    for (int t = threadIdx.x; t < H.mw * a.n; t += NT) cb[t] = H.colbits[t];
-    const int line = threadIdx.x / lanes_per_line(a.n);
-    const int64_t c_line = line < a.n ? a.cc[(int64_t)h * a.n + line] : 0;
-    __syncthreads();
-    for (int it = 0; it <= a.iters; ++it) {
-      apply_head(a, sh, za, cb, c_line, zr, maxy);
-      if (it < a.iters && orth(sh, H, zr)) {
-        degen = true;
-        break;
-      }
-    }
-  }
-  finish_head(a, sh, h, degen, hi.nnz, hi.sum_c2, hi.flags, maxy, zr, hi.adj_and, hi.adj_or);
-}
-
 // ---------------------------------------------------------------------------------------------
 // The whole permutation of a head in one workgroup, with both centred products on the matrix cores.
 //
@@ -1252,21 +1150,14 @@ size_t wa_perm_shared_bytes() { return sizeof(Shared); }
 
 int wa_perm_slices(int n) { return (n + GT - 1) / GT; }
 
-// Heads of at most this many 256-column slices run as one workgroup each (perm_fused_kernel), which
-// replaces the 3 + 3 T launches of the slice kernels (0.21 -> 0.14 ms for 2 heads of 64 blocks,
-// 0.34 -> 0.27 ms for 12 heads of 256); from three slices on, the slices' parallelism wins.
-#ifndef WA_PERM_FUSED_MAX_SLICES
-#define WA_PERM_FUSED_MAX_SLICES 2
-#endif
-constexpr int kFusedMaxSlices = WA_PERM_FUSED_MAX_SLICES;
-constexpr size_t kLdsBytes = 160 * 1024;  // LDS of one gfx950 workgroup
-#ifndef WA_PERM_MFMA_FORM_MAX
-#define WA_PERM_MFMA_FORM_MAX 1024
-#endif
-constexpr int kMfmaFormMax = WA_PERM_MFMA_FORM_MAX;
+// Heads of at most this many rows and columns are built by perm_mfma_kernel (one launch, one workgroup
+// a head); larger ones by the slice kernels (3 + 3 T launches), whose column slices spread a head over
+// the whole chip.
+constexpr int kMfmaFormMax = kMfmaMax;
+static_assert(kMfmaLdsOffset + sizeof(MfmaLds) <= 160 * 1024, "the matrix-core form fits one workgroup's LDS");
 
-// Launch sequence on one stream: init; iters x (gather, scatter, orth); gather, scatter, finish; or
-// the fused kernel alone. The statistics-only form runs init alone.
+// Launch sequence on one stream: the matrix-core kernel alone; or init, iters x (gather, scatter,
+// orth), gather, scatter, finish. The statistics-only form runs init alone.
 hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   if (a.bh <= 0) return hipSuccess;
   if (a.slices != wa_perm_slices(a.n) || a.m > MAXB || a.n > MAXB) return hipErrorInvalidValue;
@@ -1282,18 +1173,9 @@ hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const size_t msmem = kMfmaLdsOffset + sizeof(MfmaLds);
   if (!a.stats_only && a.m <= kMfmaFormMax && a.n <= kMfmaFormMax) {
-    static_assert(kMfmaFormMax <= kMfmaMax, "the matrix-core form holds at most kMfmaMax lines");
     e = hipFuncSetAttribute((const void*)perm_mfma_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(perm_mfma_kernel, dim3(a.bh), dim3(NT), msmem, stream, a);
-    return hipGetLastError();
-  }
-  const size_t fsmem = smem + (size_t)2 * a.m * sizeof(unsigned long long) +
-                       (size_t)((a.m + 63) / 64) * a.n * sizeof(uint64_t);
-  if (!a.stats_only && a.slices <= kFusedMaxSlices && fsmem <= kLdsBytes) {
-    e = hipFuncSetAttribute((const void*)perm_fused_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fsmem);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(perm_fused_kernel, dim3(a.bh), dim3(NT), fsmem, stream, a);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(perm_init_kernel, dim3(a.bh), dim3(NT), smem, stream, a);

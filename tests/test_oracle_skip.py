@@ -90,13 +90,14 @@ def test_little_work_uses_the_cost_curve_of_the_form_that_builds_the_head():
     for m, want in ((512, S.FLAG_LITTLE_WORK), (513, 0)):
         st = S.head_stats(np.eye(m, dtype=np.uint8))
         assert S.tier1_flags(st, prof, 128, 128) == want, m
-    # the saving is compared strictly: equal costs keep the reordering
+    # the saving is compared strictly: equal costs keep the reordering (a head of the sliced form)
     st = S.head_stats(np.eye(600, dtype=np.uint8))
     even = S.SkipProfile(cache_bytes=0.0, gain_ns_per_block=1.0, j_max=2.0, ovh_ns_fixed=600.0,
-                         ovh_ns_per_row=0.0, ovh_ns_per_nnz=0.0)
+                         ovh_ns_per_row=0.0, ovh_ns_per_nnz=0.0, fused_max_blocks=512.0)
     assert S.tier1_flags(st, even, 128, 128) == 0
     assert S.tier1_flags(st, S.SkipProfile(cache_bytes=0.0, gain_ns_per_block=1.0, j_max=2.0,
-                                           ovh_ns_fixed=600.5, ovh_ns_per_row=0.0, ovh_ns_per_nnz=0.0),
+                                           ovh_ns_fixed=600.5, ovh_ns_per_row=0.0, ovh_ns_per_nnz=0.0,
+                                           fused_max_blocks=512.0),
                          128, 128) == S.FLAG_LITTLE_WORK
 
 
