@@ -190,6 +190,26 @@ def test_permutation_bit_exact_bench_layout(name, mode):
     _perm_case(wl, make_mask(wl, threads=16), wave=_w().wave_size(wl.head_dim, wl.block) * 8, n_xcd=1, mode=mode)
 
 
+# Heads of at most 1024 blocks are built by the matrix-core form (one workgroup per head, 16-line MFMA
+# tiles over 64-row mask words), larger ones by the sliced form: sizes at the tile and word edges and at
+# the switch between the forms, where skip case 2 also changes its overhead line.
+@pytest.mark.parametrize("blocks", [16, 17, 63, 65, 1024, 1025])
+@pytest.mark.parametrize("mode,profile", [(S.SKIP_NEVER, None), (S.SKIP_AUTO, _SMALL_CACHE)],
+                         ids=["never", "auto-small-cache"])
+def test_permutation_bit_exact_form_boundaries(blocks, mode, profile):
+    wl = custom(f"edge{blocks}", heads=2, head_dim=64, block=64, grid=(max(1, blocks // 16), 16, 64),
+                seq_len=blocks * 64 - 13, rule=dict(kind="radius", rt=1, rs=2, g=2), seed=20 + blocks)
+    assert wl.mb == blocks
+    _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=mode, profile=profile)
+
+
+@pytest.mark.parametrize("blocks", [1024, 1025])
+def test_permutation_bit_exact_form_boundaries_random(blocks):
+    wl = custom(f"edge-random{blocks}", heads=1, head_dim=64, block=64, grid=(blocks // 16, 16, 64),
+                seq_len=blocks * 64, rule=dict(kind="bernoulli", p=0.1), seed=40 + blocks)
+    _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=S.SKIP_NEVER)
+
+
 @pytest.mark.parametrize("n_xcd,wave,seed", [(1, 132, 5), (2, 7, 99), (8, 1, 3)])
 def test_permutation_bit_exact_params(n_xcd, wave, seed):
     wl = CONFIGS["wan1.3b-480p-81f"]
