@@ -649,13 +649,14 @@ def summarize_sweep(jsonl: str, out_md: str, command_note: str) -> None:
                      f"{r['gain_step']:.3f} | {r['gain_attn']:.3f} | {r['auto']['step']:.2f} "
                      f"({r['auto']['identity_heads']}/{r['heads']}) | {r['auto_vs_best']:.3f} | {cases or '-'} |")
     # calibration of the skip rule's cost model (case 2): the permutation's time per head, amortised
-    # over the heads that run concurrently, as a linear function of M_B and the head's kept blocks,
-    # fitted separately for the two forms that build it (one workgroup per head up to 1024 blocks,
-    # column slices above); and the attention time saved per kept block by the reordered order
+    # over the heads that run concurrently, as a linear function of M_B (both forms multiply the whole
+    # bit mask on the matrix cores, so the head's kept blocks do not enter), fitted separately for the
+    # two forms that build it (one workgroup per head up to 1024 blocks, many workgroups per head
+    # above); and the attention time saved per kept block by the reordered order
     lines += ["", "Overhead model fitted to the permutation times above (least squares, per head = step share / "
               "heads), one line per form that builds the permutation:"]
     for form, sel, cols in (("one workgroup per head (M_B <= 1024)", lambda r: r["mb"] <= 1024, 2),
-                            ("column slices (M_B > 1024)", lambda r: r["mb"] > 1024, 3)):
+                            ("sliced, many workgroups per head (M_B > 1024)", lambda r: r["mb"] > 1024, 2)):
         rs = [r for r in recs if sel(r)]
         if len(rs) < cols:
             continue

@@ -62,14 +62,14 @@ SKIP_AUTO, SKIP_NEVER, SKIP_ALWAYS = 0, 1, 2
 class SkipProfile:
     cache_bytes: float = 96.0 * 1024 * 1024
     gain_ns_per_block: float = 0.5
-    ovh_ns_fixed: float = 11575.0
-    ovh_ns_per_row: float = 2.96
-    ovh_ns_per_nnz: float = 0.0565
+    ovh_ns_fixed: float = -3000.0
+    ovh_ns_per_row: float = 11.06
+    ovh_ns_per_nnz: float = 0.0
     j_max: float = 0.2
     eta_min: float = 0.05
     fused_max_blocks: float = 1024.0
-    ovh_fused_ns_fixed: float = 1199.0
-    ovh_fused_ns_per_row: float = 10.70
+    ovh_fused_ns_fixed: float = 1184.0
+    ovh_fused_ns_per_row: float = 10.50
     ovh_fused_ns_per_nnz: float = 0.0
 
 

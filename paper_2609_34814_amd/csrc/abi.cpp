@@ -89,7 +89,7 @@ ProducerWs producer_ws_layout(const Dims& d) {
 }
 
 struct PermWs {
-  size_t rowbits, colbits, row_nnz, col_cnt, head_stats, xg, ym, part, psy, state, total;
+  size_t rowbits, colbits, row_nnz, col_cnt, head_stats, xg, ym, z, state, total;
   int slices;
 };
 
@@ -105,8 +105,7 @@ PermWs perm_ws_layout(const Dims& d) {
   w.head_stats = off; off = align_up(off + (size_t)d.bh * 6 * 8);
   w.xg = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 4);
   w.ym = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 8);
-  w.part = off; off = align_up(off + (size_t)d.bh * w.slices * d.mb * 2 * 8);
-  w.psy = off; off = align_up(off + (size_t)d.bh * w.slices * 2 * 8);
+  w.z = off; off = align_up(off + (size_t)d.bh * d.mb * 2 * 8);
   w.state = off; off = align_up(off + (size_t)d.bh * sizeof(PermState));
   w.total = off;
   return w;
@@ -118,8 +117,7 @@ void perm_ws_pointers(WaPermLaunch& a, const PermWs& L, char* base) {
   a.cc = (int32_t*)(base + L.col_cnt);
   a.xg = (int32_t*)(base + L.xg);
   a.ym = (int64_t*)(base + L.ym);
-  a.part = (int64_t*)(base + L.part);
-  a.psy = (int64_t*)(base + L.psy);
+  a.z = (int64_t*)(base + L.z);
   a.state = (PermState*)(base + L.state);
   a.slices = L.slices;
 }
@@ -148,14 +146,14 @@ const wa_skip_profile kDefaultProfile = {
     96.0 * 1024.0 * 1024.0,  // cache_bytes: K/V per head below which reordering did not pay (the shared
                              // 256 MiB last-level cache holds it next to the streamed Q, O and V^T)
     0.5,                     // gain_ns_per_block: attention time saved per kept block where it paid
-    11575.0,                 // ovh_ns_fixed    } permutation time per head of more than 1024 blocks (the
-    2.96,                    // ovh_ns_per_row  } sliced form), amortised over concurrent heads,
-    0.0565,                  // ovh_ns_per_nnz  } least-squares fit over the sweep (worst residual 11%)
+    -3000.0,                 // ovh_ns_fixed    } permutation time per head of more than 1024 blocks (the
+    11.06,                   // ovh_ns_per_row  } sliced form), amortised over concurrent heads, least-
+    0.0,                     // ovh_ns_per_nnz  } squares fit over 1,547-4,079 blocks (worst residual 11%)
     0.2,                     // j_max: adjacent rows of raster-local heads share 23-40% of their blocks
     0.05,                    // eta_min
     1024.0,                  // fused_max_blocks: heads built by one workgroup (the matrix-core form)
-    1199.0,                  // ovh_fused_ns_fixed   } the one-workgroup form's time per head, fitted alone
-    10.70,                   // ovh_fused_ns_per_row } (worst residual 6%)
+    1184.0,                  // ovh_fused_ns_fixed   } the one-workgroup form's time per head, fitted alone
+    10.50,                   // ovh_fused_ns_per_row } (worst residual 3%)
     0.0,                     // ovh_fused_ns_per_nnz }
 };
 

@@ -26,9 +26,9 @@
 //     mask bits with the base-256 digits of X and Ys (see the kernel);
 //   * larger heads: phases 0-1 and the first QR in perm_init_kernel, each further QR in
 //     orth_step_kernel and phases 3-5 in perm_finish_kernel (one 1024-thread workgroup per head
-//     each); the centred products as sparse sums over the set bits in apply_gather_kernel and
-//     apply_scatter_kernel, one workgroup per 256-column slice of every head. Per-head state
-//     between the kernels lives in the workspace.
+//     each); the centred products, with the same matrix-core products, in mfma_gather_kernel and
+//     mfma_scatter_kernel, one workgroup per 128 lines of every head. Per-head state between the
+//     kernels lives in the workspace.
 // Every sum is an exact integer, so neither the order of parallel reductions nor the slicing nor the
 // form matters. Supports m, n <= 4096.
 
@@ -220,26 +220,6 @@ __device__ bool orth(Shared& sh, const Head& H, const int64_t (&zr)[PER][2]) {
   return false;
 }
 
-// Calls f(k) for every set bit k of a word-major bitmask line (words[w * stride + line] for
-// w < nwords), reading the words eight at a time so that the loads are in flight together.
-template <typename F>
-__device__ __forceinline__ void for_bits(const uint64_t* words, int nwords, int64_t stride, int line, F&& f) {
-  constexpr int CH = 8;
-  for (int v0 = 0; v0 < nwords; v0 += CH) {
-    uint64_t wd[CH];
-#pragma unroll
-    for (int t = 0; t < CH; ++t) wd[t] = v0 + t < nwords ? words[(int64_t)(v0 + t) * stride + line] : 0ull;
-#pragma unroll
-    for (int t = 0; t < CH; ++t) {
-      uint64_t word = wd[t];
-      while (word) {
-        f((v0 + t) * 64 + __ffsll((long long)word) - 1);
-        word &= word - 1;
-      }
-    }
-  }
-}
-
 // Threads that share one column (or row) in the one-workgroup form: the largest power of two up to
 // 16 with threads * lines <= NT. They are consecutive lanes of one wavefront, and each takes a
 // contiguous chunk of the line's bit range (or of the compared elements).
@@ -260,154 +240,19 @@ __device__ __forceinline__ int64_t group_sum(int64_t v, int t) {
   return v;
 }
 
-// ---------------------------------------------------------------------------------------------
-// Centred products across many workgroups. One subspace step X -> Z = m * M~ Ys, with
-// Ys = (m * M~^T X) >> sy, runs as two slice kernels (one 256-thread workgroup per 256-column
-// slice of every head, one lane per column) and the per-head orth kernel:
-//   gather:  Ym[j] = m * sum_{i in column j} X[i] - c_j * sum_i X[i]; atomic max of |Ym| per head;
-//   scatter: Ys[j] = Ym[j] >> sy; the slice's share of M Ys, scattered into LDS with 64-bit LDS
-//            atomics, and of sum_j c_j Ys[j], both written out as partial sums;
-//   orth:    Z[i] = m * (sum of the partials of row i) - (sum of the partial c.Ys sums).
-// Column counts are far more even than the heavy-tailed row counts, so one lane per column keeps
-// the lanes of a wavefront balanced in both halves. Every sum is an exact integer, so the slicing
-// does not change any result.
-constexpr int GT = 256;
-constexpr int GW = GT / 64;
 // Heads of at most this many rows are ordered by rank sorts (no barriers; four or more lanes per
 // row), larger ones by bitonic sorts (at 394 rows the rank sort's m^2 / 2 compares per lane cost
 // more than the bitonic stages).
 constexpr int kRankSortMax = 256;
 
-__global__ __launch_bounds__(GT) void apply_gather_kernel(WaPermLaunch a) {
-  const int h = blockIdx.x / a.slices, s = blockIdx.x % a.slices;
-  if (!a.state[h].active) return;
-  __shared__ __attribute__((aligned(16))) int32_t xs[2 * MAXB];
-  __shared__ int64_t red[GW][2];
-  __shared__ uint64_t redm[GW];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int m = a.m, n = a.n, mw = (m + 63) / 64;
-  const int2* xg = reinterpret_cast<const int2*>(a.xg) + (int64_t)h * m;
-  int64_t sx0 = 0, sx1 = 0;
-  for (int i = tid; i < m; i += GT) {
-    const int2 x = xg[i];
-    xs[2 * i] = x.x;
-    xs[2 * i + 1] = x.y;
-    sx0 += x.x;
-    sx1 += x.y;
-  }
-  sx0 = wave_sum(sx0);
-  sx1 = wave_sum(sx1);
-  if (lane == 0) {
-    red[w][0] = sx0;
-    red[w][1] = sx1;
-  }
-  __syncthreads();
-  sx0 = 0;
-  sx1 = 0;
-#pragma unroll
-  for (int k = 0; k < GW; ++k) {
-    sx0 += red[k][0];
-    sx1 += red[k][1];
-  }
-  const int j = s * GT + tid;
-  uint64_t mx = 0;
-  if (j < n) {
-    int64_t y0 = 0, y1 = 0;
-    for_bits(a.colbits + (int64_t)h * n * mw, mw, n, j, [&](int i) {
-      const int2 x = *(const int2*)&xs[2 * i];
-      y0 += x.x;
-      y1 += x.y;
-    });
-    const int64_t c = a.cc[(int64_t)h * n + j];
-    y0 = (int64_t)m * y0 - c * sx0;
-    y1 = (int64_t)m * y1 - c * sx1;
-    int64_t* out = a.ym + ((int64_t)h * n + j) * 2;
-    out[0] = y0;
-    out[1] = y1;
-    const uint64_t p = uabs64(y0), q = uabs64(y1);
-    mx = p > q ? p : q;
-  }
-  mx = wave_max(mx);
-  if (lane == 0) redm[w] = mx;
-  __syncthreads();
-  if (tid == 0) {
-    for (int k = 1; k < GW; ++k) mx = redm[k] > mx ? redm[k] : mx;
-    if (mx) atomicMax((unsigned long long*)&a.state[h].maxy, (unsigned long long)mx);
-  }
-}
-
-__global__ __launch_bounds__(GT) void apply_scatter_kernel(WaPermLaunch a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-  unsigned long long* za = reinterpret_cast<unsigned long long*>(smem_raw);  // [2 m]
-  __shared__ int64_t red[GW][2];
-  const int h = blockIdx.x / a.slices, s = blockIdx.x % a.slices;
-  if (!a.state[h].active) return;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int m = a.m, n = a.n, mw = (m + 63) / 64;
-  const int bl = bitlen_u64(a.state[h].maxy);
-  const int sy = bl > 30 ? bl - 30 : 0;
-  for (int i = tid; i < 2 * m; i += GT) za[i] = 0ull;
-  __syncthreads();
-  const int j = s * GT + tid;
-  int64_t p0 = 0, p1 = 0;
-  if (j < n) {
-    const int64_t* yj = a.ym + ((int64_t)h * n + j) * 2;
-    const int32_t y0 = (int32_t)(yj[0] >> sy), y1 = (int32_t)(yj[1] >> sy);
-    const int64_t c = a.cc[(int64_t)h * n + j];
-    p0 = c * y0;
-    p1 = c * y1;
-    const unsigned long long u0 = (unsigned long long)(int64_t)y0, u1 = (unsigned long long)(int64_t)y1;
-    for_bits(a.colbits + (int64_t)h * n * mw, mw, n, j, [&](int i) {
-      atomicAdd(&za[2 * i], u0);
-      atomicAdd(&za[2 * i + 1], u1);
-    });
-  }
-  p0 = wave_sum(p0);
-  p1 = wave_sum(p1);
-  if (lane == 0) {
-    red[w][0] = p0;
-    red[w][1] = p1;
-  }
-  __syncthreads();  // also completes the scatter
-  const int64_t slot = (int64_t)h * a.slices + s;
-  if (tid == 0) {
-    int64_t q0 = 0, q1 = 0;
-    for (int k = 0; k < GW; ++k) {
-      q0 += red[k][0];
-      q1 += red[k][1];
-    }
-    a.psy[slot * 2] = q0;
-    a.psy[slot * 2 + 1] = q1;
-  }
-  int64_t* part = a.part + slot * m * 2;
-  for (int i = tid; i < 2 * m; i += GT) part[i] = (int64_t)za[i];
-}
-
-// zr = m * (M Ys) - sum_j c_j Ys[j] for the thread's rows, from the scatter's partial sums.
-__device__ void gather_partials(const WaPermLaunch& a, int h, int64_t (&zr)[PER][2]) {
+// Z of the thread's rows (rows i = tid + k NT) as the product kernels wrote it.
+__device__ void load_z(const WaPermLaunch& a, int h, int64_t (&zr)[PER][2]) {
   const int tid = threadIdx.x;
-  const int64_t m = a.m;
-  const int64_t* psy = a.psy + (int64_t)h * a.slices * 2;
-  int64_t sy0 = 0, sy1 = 0;
-  for (int s = 0; s < a.slices; ++s) {
-    sy0 += psy[2 * s];
-    sy1 += psy[2 * s + 1];
-  }
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int i = tid + k * NT;
-    zr[k][0] = 0;
-    zr[k][1] = 0;
-    if (i < a.m) {
-      int64_t z0 = 0, z1 = 0;
-      for (int s = 0; s < a.slices; ++s) {
-        const int64_t* p = a.part + (((int64_t)h * a.slices + s) * m + i) * 2;
-        z0 += p[0];
-        z1 += p[1];
-      }
-      zr[k][0] = m * z0 - sy0;
-      zr[k][1] = m * z1 - sy1;
-    }
+    zr[k][0] = i < a.m ? a.z[((int64_t)h * a.m + i) * 2] : 0;
+    zr[k][1] = i < a.m ? a.z[((int64_t)h * a.m + i) * 2 + 1] : 0;
   }
 }
 
@@ -529,22 +374,39 @@ __device__ HeadInit init_head(const WaPermLaunch& a, Shared& sh, int h) {
   const Head H = head_of(a, h);
 
   // ---- phase 0: statistics ----
+  // The word loops load 8 words at a time, so that their latencies overlap.
+  constexpr int WB = 8;
   int64_t st[4] = {0, 0, 0, 0};  // nnz, distinct, sum c^2, (unused)
   for (int j = tid; j < n; j += NT) {
     int c = 0;
-    for (int v = 0; v < H.mw; ++v) c += __popcll(H.colbits[(int64_t)v * n + j]);
+    for (int v0 = 0; v0 < H.mw; v0 += WB) {
+      uint64_t wd[WB];
+#pragma unroll
+      for (int u = 0; u < WB; ++u) wd[u] = v0 + u < H.mw ? H.colbits[(int64_t)(v0 + u) * n + j] : 0ull;
+#pragma unroll
+      for (int u = 0; u < WB; ++u) c += __popcll(wd[u]);
+    }
     a.cc[(int64_t)h * n + j] = c;
     if (a.col_cnt) a.col_cnt[(int64_t)h * n + j] = c;
     st[1] += c > 0;
     st[2] += (int64_t)c * c;
   }
   for (int i = tid; i < m; i += NT) st[0] += H.row_nnz[i];
-  int64_t adj[2] = {0, 0};
-  for (int t = tid; t < (m - 1) * H.nw; t += NT) {
-    const int w = t / (m - 1), i = t % (m - 1);
-    const uint64_t x = H.rowbits[(int64_t)w * m + i], y = H.rowbits[(int64_t)w * m + i + 1];
-    adj[0] += __popcll(x & y);
-    adj[1] += __popcll(x | y);
+  int64_t adj[2] = {0, 0};  // rows i and i + 1, word by word
+  for (int i = tid; i < m - 1; i += NT) {
+    for (int w0 = 0; w0 < H.nw; w0 += WB) {
+      uint64_t x[WB], y[WB];
+#pragma unroll
+      for (int u = 0; u < WB; ++u) {
+        x[u] = w0 + u < H.nw ? H.rowbits[(int64_t)(w0 + u) * m + i] : 0ull;
+        y[u] = w0 + u < H.nw ? H.rowbits[(int64_t)(w0 + u) * m + i + 1] : 0ull;
+      }
+#pragma unroll
+      for (int u = 0; u < WB; ++u) {
+        adj[0] += __popcll(x[u] & y[u]);
+        adj[1] += __popcll(x[u] | y[u]);
+      }
+    }
   }
   block_sum<4>(sh, st);
   block_sum<2>(sh, adj);
@@ -631,7 +493,7 @@ __global__ __launch_bounds__(NT) void orth_step_kernel(WaPermLaunch a) {
   if (!S->active) return;
   const Head H = head_of(a, h);
   int64_t zr[PER][2];
-  gather_partials(a, h, zr);
+  load_z(a, h, zr);
   const bool degen = orth(sh, H, zr);
   if (!degen) store_x(a, sh, h);
   if (threadIdx.x == 0) {
@@ -877,7 +739,7 @@ __global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
       sh.xs[2 * i] = x.x;
       sh.xs[2 * i + 1] = x.y;
     }
-    gather_partials(a, h, zr);
+    load_z(a, h, zr);
   }
   finish_head(a, sh, h, degen, S->nnz, S->sum_c2, S->flags, S->maxy, zr, S->adj_and, S->adj_or);
 }
@@ -921,7 +783,8 @@ __device__ __forceinline__ v4i bits_to_bytes(uint32_t b) {
 }
 
 // Balanced base-256 digits of v into digit rows row0 .. row0 + 3, column idx.
-__device__ __forceinline__ void put_digits(int8_t (*d)[kMfmaMax], int row0, int idx, int32_t v) {
+template <int STRIDE>
+__device__ __forceinline__ void put_digits(int8_t (*d)[STRIDE], int row0, int idx, int32_t v) {
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     const int8_t db = (int8_t)(uint8_t)(uint32_t)v;
@@ -993,34 +856,83 @@ __device__ __forceinline__ uint64_t wg_max(int64_t (*red)[4][NWAVE], int buf, ui
 }
 
 // Exact products of the digit rows dg with the bitmask of `lines` lines (word s of line j at
-// bits16[4 (s lines + j) .. +3], `words` words a line). The wavefront takes the 16-line tiles
-// w, w + NWAVE, ...; for each, f(line, column, value) is called in lanes 0-31 with the product of
-// line 16 tile + l mod 16 with column l / 16 of the digit block (line may lie past `lines`).
-template <typename F>
-__device__ __forceinline__ void mfma_product(const int8_t (*dg)[kMfmaMax], const uint16_t* bits16, int lines,
-                                             int words, F&& f) {
+// bits16[4 (s lines + j) .. +3], `words` words a line). Wavefront w of the WAVES in the workgroup takes
+// the 16-line tiles t0 + w, t0 + w + WAVES, ... below t1; for each, f(line, column, value) is called in
+// lanes 0-31 with the product of line 16 t + l mod 16 with column l / 16 of the digit block (line may
+// lie past `lines`). The bits of CH words are loaded together. With PIPE the wavefront walks its
+// (tile, chunk of CH words) steps in order and loads the bits of the next step while it multiplies the
+// current one, so that load latency overlaps the work (the product kernels of the sliced form, whose
+// workgroups are short-lived); without, each chunk's loads are waited for before its products (the
+// one-workgroup form, whose sixteen wavefronts hide each other's latency and which has no registers to
+// spare: the pipelined walk there measured 1-6% slower).
+template <int STRIDE, int WAVES, int CH, bool PIPE, typename F>
+__device__ __forceinline__ void mfma_product(const int8_t (*dg)[STRIDE], const uint16_t* bits16, int lines,
+                                             int words, int t0, int t1, F&& f) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r = lane & 15, q = lane >> 4;
   const v4i zero = {0, 0, 0, 0};
-  constexpr int CH = 4;  // words whose bits are loaded together
-  WA_PHASE_FENCE();
-  for (int tile = w; 16 * tile < lines; tile += NWAVE) {
+  const int tend = min(t1, (lines + 15) >> 4);
+  const int chunks = (words + CH - 1) / CH;
+  auto load = [&](int tile, int c, uint32_t (&bt)[CH]) {
     const int line = 16 * tile + r;
-    v4i acc = zero;
-    for (int s0 = 0; s0 < words; s0 += CH) {
-      uint32_t bt[CH];
 #pragma unroll
-      for (int u = 0; u < CH; ++u)
-        bt[u] = s0 + u < words && line < lines ? bits16[((int64_t)(s0 + u) * lines + line) * 4 + q] : 0u;
+    for (int u = 0; u < CH; ++u) {
+      const int s = c * CH + u;
+      bt[u] = s < words && line < lines ? bits16[((int64_t)s * lines + line) * 4 + q] : 0u;
+    }
+  };
+  WA_PHASE_FENCE();
+  if constexpr (!PIPE) {
+    for (int tile = t0 + w; tile < tend; tile += WAVES) {
+      v4i acc = zero;
+      for (int c = 0; c < chunks; ++c) {
+        uint32_t bt[CH];
+        load(tile, c, bt);
 #pragma unroll
-      for (int u = 0; u < CH; ++u) {
-        if (s0 + u < words) {
-          const v4i av = r < 8 ? *(const v4i*)&dg[r][64 * (s0 + u) + 16 * q] : zero;
-          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bits_to_bytes(bt[u]), acc, 0, 0, 0);
+        for (int u = 0; u < CH; ++u) {
+          const int s = c * CH + u;
+          if (s < words) {
+            const v4i av = r < 8 ? *(const v4i*)&dg[r][64 * s + 16 * q] : zero;
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bits_to_bytes(bt[u]), acc, 0, 0, 0);
+          }
         }
       }
+      if (q < 2) f(16 * tile + r, q, (int64_t)acc[0] + 256ll * acc[1] + 65536ll * acc[2] + 16777216ll * acc[3]);
     }
-    if (q < 2) f(line, q, (int64_t)acc[0] + 256ll * acc[1] + 65536ll * acc[2] + 16777216ll * acc[3]);
+    WA_PHASE_FENCE();
+    return;
+  }
+  int tile = t0 + w, c = 0;
+  if (tile < tend) {
+    uint32_t cur[CH], nxt[CH];
+    load(tile, 0, cur);
+    v4i acc = zero;
+    for (;;) {
+      // the step after (tile, c)
+      int ntile = tile, nc = c + 1;
+      if (nc == chunks) {
+        ntile = tile + WAVES;
+        nc = 0;
+      }
+      if (ntile < tend) load(ntile, nc, nxt);
+#pragma unroll
+      for (int u = 0; u < CH; ++u) {
+        const int s = c * CH + u;
+        if (s < words) {
+          const v4i av = r < 8 ? *(const v4i*)&dg[r][64 * s + 16 * q] : zero;
+          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bits_to_bytes(cur[u]), acc, 0, 0, 0);
+        }
+      }
+      if (nc == 0) {  // the tile is complete
+        if (q < 2) f(16 * tile + r, q, (int64_t)acc[0] + 256ll * acc[1] + 65536ll * acc[2] + 16777216ll * acc[3]);
+        acc = zero;
+      }
+      if (ntile >= tend) break;
+      tile = ntile;
+      c = nc;
+#pragma unroll
+      for (int u = 0; u < CH; ++u) cur[u] = nxt[u];
+    }
   }
   WA_PHASE_FENCE();
 }
@@ -1062,7 +974,7 @@ __global__ __launch_bounds__(NT) void perm_mfma_kernel(WaPermLaunch a) {
     for (int it = 0; it <= a.iters; ++it) {
       // ---- Ym = m M^T X - c (1^T X), and max |Ym| ----
       uint64_t mx = 0;
-      mfma_product(L.xd, cb16, n, H.mw, [&](int j, int k, int64_t ya) {
+      mfma_product<kMfmaMax, NWAVE, 4, false>(L.xd, cb16, n, H.mw, 0, kMfmaMax / 16, [&](int j, int k, int64_t ya) {
         if (j < n) {
           const int64_t y = mm * ya - (int64_t)L.cc[j] * (k == 0 ? sx[0] : sx[1]);
           L.v[2 * j + k] = y;
@@ -1084,7 +996,7 @@ __global__ __launch_bounds__(NT) void perm_mfma_kernel(WaPermLaunch a) {
       wg_sum<2>(L.red, rb++ & 1, py);  // its barrier also publishes the Ys digits (Ym is read)
       // ---- Z = m M Ys - 1 (c^T Ys), and max |Z| ----
       uint64_t mz = 0;
-      mfma_product(L.yd, rb16, m, H.nw, [&](int i, int k, int64_t za) {
+      mfma_product<kMfmaMax, NWAVE, 4, false>(L.yd, rb16, m, H.nw, 0, kMfmaMax / 16, [&](int i, int k, int64_t za) {
         if (i < m) {
           const int64_t z = mm * za - (k == 0 ? py[0] : py[1]);
           L.v[2 * i + k] = z;
@@ -1131,6 +1043,142 @@ __global__ __launch_bounds__(NT) void perm_mfma_kernel(WaPermLaunch a) {
   finish_head(a, sh, h, degen, hi.nnz, hi.sum_c2, hi.flags, maxy, zr, hi.adj_and, hi.adj_or);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Centred products across many workgroups, for heads of more than kMfmaMax blocks. One subspace step
+// X -> Z = m * M~ Ys, with Ys = (m * M~^T X) >> sy, runs as two product kernels and the per-head orth
+// kernel. A product workgroup (GT threads) takes kSliceTiles consecutive 16-line tiles of one head, dealt
+// to its wavefronts in turn, and computes them with the matrix-core products of perm_mfma_kernel over
+// the whole head:
+//   gather:  the digit rows of X and 1^T X (each workgroup of the head builds them in LDS), then
+//            Ym[j] = m * (M^T X)[j] - c_j * 1^T X for its columns, and an atomic max of |Ym| per head;
+//   scatter: the digit rows of Ys = Ym >> sy and c^T Ys (likewise), then Z[i] = m * (M Ys)[i] - c^T Ys
+//            for its rows;
+//   orth:    the Cholesky-QR of Z, the next X.
+// Every workgroup of a head computes the same exact sums and each line is written by one lane, so the
+// slicing does not change any result.
+constexpr int GT = 256;
+constexpr int GW = GT / 64;
+constexpr int kSliceTiles = 8;  // 16-line tiles per product workgroup (two per wavefront)
+constexpr int kLoadBatch = 8;   // X rows or Ym columns per thread whose loads are issued together
+
+struct SliceLds {
+  int8_t dg[8][MAXB];  // digit rows of X (gather) or Ys (scatter), zero past the head's last word
+  int64_t red[GW][2];
+};
+
+// Exact sums of two int64 values over a GT-thread workgroup, returned to every thread; its barrier
+// also publishes every LDS write made before the call.
+__device__ __forceinline__ void slice_sum2(int64_t (*red)[2], int64_t& v0, int64_t& v1) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v0 = wave_sum(v0);
+  v1 = wave_sum(v1);
+  if (lane == 0) {
+    red[w][0] = v0;
+    red[w][1] = v1;
+  }
+  __syncthreads();
+  v0 = 0;
+  v1 = 0;
+#pragma unroll
+  for (int k = 0; k < GW; ++k) {
+    v0 += red[k][0];
+    v1 += red[k][1];
+  }
+}
+
+__global__ __launch_bounds__(GT) void mfma_gather_kernel(WaPermLaunch a) {
+  const int h = blockIdx.x / a.slices, g = blockIdx.x % a.slices;
+  if (!a.state[h].active) return;
+  __shared__ __attribute__((aligned(16))) SliceLds L;
+  __shared__ uint64_t redm[GW];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int m = a.m, n = a.n;
+  const Head H = head_of(a, h);
+  const int2* xg = reinterpret_cast<const int2*>(a.xg) + (int64_t)h * m;
+  int64_t sx0 = 0, sx1 = 0;
+  for (int i0 = 0; i0 < 64 * H.mw; i0 += kLoadBatch * GT) {  // the rows' loads in flight together
+    int2 x[kLoadBatch];
+#pragma unroll
+    for (int u = 0; u < kLoadBatch; ++u) {
+      const int i = i0 + u * GT + tid;
+      x[u] = i < m ? xg[i] : make_int2(0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < kLoadBatch; ++u) {
+      const int i = i0 + u * GT + tid;
+      if (i < 64 * H.mw) {
+        put_digits(L.dg, 0, i, x[u].x);
+        put_digits(L.dg, 4, i, x[u].y);
+        sx0 += x[u].x;
+        sx1 += x[u].y;
+      }
+    }
+  }
+  slice_sum2(L.red, sx0, sx1);  // its barrier also publishes the digits
+  const int32_t* cc = a.cc + (int64_t)h * n;
+  int64_t* ym = a.ym + (int64_t)h * n * 2;
+  uint64_t mx = 0;
+  mfma_product<MAXB, GW, 16, true>(L.dg, reinterpret_cast<const uint16_t*>(H.colbits), n, H.mw, g * kSliceTiles,
+                             g * kSliceTiles + kSliceTiles,
+                         [&](int j, int k, int64_t ya) {
+                           if (j < n) {
+                             const int64_t y = (int64_t)m * ya - (int64_t)cc[j] * (k == 0 ? sx0 : sx1);
+                             ym[2 * j + k] = y;
+                             mx = max64(mx, uabs64(y));
+                           }
+                         });
+  mx = wave_max(mx);
+  if (lane == 0) redm[w] = mx;
+  __syncthreads();
+  if (tid == 0) {
+    for (int k = 1; k < GW; ++k) mx = max64(mx, redm[k]);
+    if (mx) atomicMax((unsigned long long*)&a.state[h].maxy, (unsigned long long)mx);
+  }
+}
+
+__global__ __launch_bounds__(GT) void mfma_scatter_kernel(WaPermLaunch a) {
+  const int h = blockIdx.x / a.slices, g = blockIdx.x % a.slices;
+  if (!a.state[h].active) return;
+  __shared__ __attribute__((aligned(16))) SliceLds L;
+  const int tid = threadIdx.x;
+  const int m = a.m, n = a.n;
+  const Head H = head_of(a, h);
+  const int bl = bitlen_u64(a.state[h].maxy);
+  const int sy = bl > 30 ? bl - 30 : 0;
+  const int32_t* cc = a.cc + (int64_t)h * n;
+  const int64_t* ym = a.ym + (int64_t)h * n * 2;
+  int64_t p0 = 0, p1 = 0;  // c^T Ys
+  for (int j0 = 0; j0 < 64 * H.nw; j0 += kLoadBatch * GT) {  // the columns' loads in flight together
+    int64_t y0[kLoadBatch], y1[kLoadBatch];
+    int32_t c[kLoadBatch];
+#pragma unroll
+    for (int u = 0; u < kLoadBatch; ++u) {
+      const int j = j0 + u * GT + tid;
+      y0[u] = j < n ? ym[2 * j] : 0;
+      y1[u] = j < n ? ym[2 * j + 1] : 0;
+      c[u] = j < n ? cc[j] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kLoadBatch; ++u) {
+      const int j = j0 + u * GT + tid;
+      if (j < 64 * H.nw) {
+        const int32_t v0 = (int32_t)(y0[u] >> sy), v1 = (int32_t)(y1[u] >> sy);
+        p0 += (int64_t)c[u] * v0;
+        p1 += (int64_t)c[u] * v1;
+        put_digits(L.dg, 0, j, v0);
+        put_digits(L.dg, 4, j, v1);
+      }
+    }
+  }
+  slice_sum2(L.red, p0, p1);  // its barrier also publishes the digits
+  int64_t* z = a.z + (int64_t)h * m * 2;
+  mfma_product<MAXB, GW, 16, true>(L.dg, reinterpret_cast<const uint16_t*>(H.rowbits), m, H.nw, g * kSliceTiles,
+                             g * kSliceTiles + kSliceTiles,
+                         [&](int i, int k, int64_t za) {
+                           if (i < m) z[2 * i + k] = (int64_t)m * za - (k == 0 ? p0 : p1);
+                         });
+}
+
 // Arithmetic self-check: the fp64 operations the permutation relies on, evaluated on the GPU.
 __global__ void fp64_probe_kernel(const double* a, const double* b, const int64_t* c, double* out, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1148,7 +1196,7 @@ __global__ void fp64_probe_kernel(const double* a, const double* b, const int64_
 
 size_t wa_perm_shared_bytes() { return sizeof(Shared); }
 
-int wa_perm_slices(int n) { return (n + GT - 1) / GT; }
+int wa_perm_slices(int n) { return (n + 16 * kSliceTiles - 1) / (16 * kSliceTiles); }
 
 // Heads of at most this many rows and columns are built by perm_mfma_kernel (one launch, one workgroup
 // a head); larger ones by the slice kernels (3 + 3 T launches), whose column slices spread a head over
@@ -1160,17 +1208,12 @@ static_assert(kMfmaLdsOffset + sizeof(MfmaLds) <= 160 * 1024, "the matrix-core f
 // orth), gather, scatter, finish. The statistics-only form runs init alone.
 hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   if (a.bh <= 0) return hipSuccess;
-  if (a.slices != wa_perm_slices(a.n) || a.m > MAXB || a.n > MAXB) return hipErrorInvalidValue;
+  if (a.slices != wa_perm_slices(a.m > a.n ? a.m : a.n) || a.m > MAXB || a.n > MAXB) return hipErrorInvalidValue;
   const size_t smem = sizeof(Shared);
-  const size_t zsmem = (size_t)2 * a.m * sizeof(unsigned long long);
   const void* big[] = {(const void*)perm_init_kernel, (const void*)orth_step_kernel, (const void*)perm_finish_kernel};
-  for (const void* f : big) {
-    hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-  }
-  hipError_t e = hipFuncSetAttribute((const void*)apply_scatter_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)zsmem);
-  if (e != hipSuccess) return e;
+  hipError_t e;
+  for (const void* f : big)
+    if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem)) != hipSuccess) return e;
   const size_t msmem = kMfmaLdsOffset + sizeof(MfmaLds);
   if (!a.stats_only && a.m <= kMfmaFormMax && a.n <= kMfmaFormMax) {
     e = hipFuncSetAttribute((const void*)perm_mfma_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
@@ -1182,9 +1225,9 @@ hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream) {
   if ((e = hipGetLastError()) != hipSuccess || a.stats_only) return e;
   const dim3 slices((unsigned)(a.bh * a.slices));
   for (int it = 0; it <= a.iters; ++it) {
-    hipLaunchKernelGGL(apply_gather_kernel, slices, dim3(GT), 0, stream, a);
+    hipLaunchKernelGGL(mfma_gather_kernel, slices, dim3(GT), 0, stream, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(apply_scatter_kernel, slices, dim3(GT), zsmem, stream, a);
+    hipLaunchKernelGGL(mfma_scatter_kernel, slices, dim3(GT), 0, stream, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (it < a.iters) {
       hipLaunchKernelGGL(orth_step_kernel, dim3(a.bh), dim3(NT), smem, stream, a);

@@ -27,8 +27,7 @@ struct WaPermLaunch {
   int32_t* col_cnt;         // [bh][n], nullable (a copy of the column counts for the caller)
   int32_t* xg;              // workspace [bh][m][2]: X of the subspace iteration (2^30 fixed point)
   int64_t* ym;              // workspace [bh][n][2]: m * M~^T X
-  int64_t* part;            // workspace [bh][slices][m][2]: per-slice partial sums of M Ys
-  int64_t* psy;             // workspace [bh][slices][2]: per-slice partial sums of c_j Ys[j]
+  int64_t* z;               // workspace [bh][m][2]: m * M~ Ys
   PermState* state;         // workspace [bh]
   int64_t* head_stats;      // [bh][6], nullable
   int32_t* perm;            // [bh][m]
@@ -45,7 +44,7 @@ struct WaPermLaunch {
 
 hipError_t wa_launch_perm(const WaPermLaunch& a, hipStream_t stream);
 size_t wa_perm_shared_bytes();
-int wa_perm_slices(int n);  // column slices of the centred-product kernels
+int wa_perm_slices(int n);  // workgroups per head of the centred-product kernels (n: the larger of m, n)
 hipError_t wa_launch_fp64_probe(const double* a, const double* b, const int64_t* c, double* out, int n,
                                 hipStream_t stream);
 hipError_t wa_launch_pack_rows(const uint8_t* mask, int64_t rows, int m, int n, uint64_t* rowbits,
