@@ -294,6 +294,19 @@ __device__ __forceinline__ bool angle_less(const Shared& sh, int a, int b) {
   return a < b;
 }
 
+// The same order on (x, y, row) entries; row -1 is +infinity.
+__device__ __forceinline__ bool entry_less(const int4& a, const int4& b) {
+  if (a.z < 0) return false;
+  if (b.z < 0) return true;
+  const int ca = angle_class(a.x, a.y), cb = angle_class(b.x, b.y);
+  if (ca != cb) return ca < cb;
+  if (ca == 0 || ca == 2) {
+    const int64_t cross = (int64_t)a.x * b.y - (int64_t)a.y * b.x;
+    if (cross != 0) return cross > 0;
+  }
+  return a.z < b.z;
+}
+
 // Work-balanced XCD segments of the order held in sh.cc[0..m): position p belongs to segment
 // min(n_xcd - 1, n_xcd * W_p / W_m) with W_p the sum of (n_i + 1) over the first p positions.
 // Fills sh.seg[0..n_xcd] (and seg_out, if given). Uses sh.xs as scratch.
@@ -630,28 +643,44 @@ __device__ void finish_head(const WaPermLaunch& a, Shared& sh, int h, bool degen
     r = group_sum(r, t);
     if (line < m && sub == 0) idx[degen ? line : (int)r] = line;  // degenerate: the identity
     __syncthreads();
+    for (int i = tid; i < m; i += NT) sh.cc[i] = idx[i];
+  } else if (degen) {
+    for (int i = tid; i < m; i += NT) sh.cc[i] = i;
   } else {
-    for (int i = tid; i < P; i += NT) idx[i] = i < m ? i : -1;
+    // bitonic sort of (x, y, row) entries, which span sh.xs and sh.ys (U is not needed after this
+    // phase): each compare reads its two entries with one 16-byte load each; padding entries
+    // (row -1) order last
+    int32_t ux[PER], uy[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = tid + k * NT;
+      ux[k] = i < m ? sh.xs[2 * i] : 0;
+      uy[k] = i < m ? sh.xs[2 * i + 1] : 0;
+    }
     __syncthreads();
-  }
-  if (!degen && m > kRankSortMax) {
+    int4* ent = reinterpret_cast<int4*>(sh.xs);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = tid + k * NT;
+      if (i < P) ent[i] = i < m ? make_int4(ux[k], uy[k], i, 0) : make_int4(0, 0, -1, 0);
+    }
+    __syncthreads();
     for (int k = 2; k <= P; k <<= 1)
       for (int j = k >> 1; j > 0; j >>= 1) {
         for (int t = tid; t < P / 2; t += NT) {
           const int i = (t / j) * 2 * j + (t % j);
           const int p = i + j;
-          const int x = idx[i], y = idx[p];
+          const int4 x = ent[i], y = ent[p];
           const bool up = (i & k) == 0;
-          const bool sw = up ? angle_less(sh, y, x) : angle_less(sh, x, y);
-          if (sw) {
-            idx[i] = y;
-            idx[p] = x;
+          if (up ? entry_less(y, x) : entry_less(x, y)) {
+            ent[i] = y;
+            ent[p] = x;
           }
         }
         __syncthreads();
       }
+    for (int i = tid; i < m; i += NT) sh.cc[i] = ent[i].z;
   }
-  for (int i = tid; i < m; i += NT) sh.cc[i] = idx[i];
   __syncthreads();
   if (a.stage1)
     for (int i = tid; i < m; i += NT) a.stage1[(int64_t)h * m + i] = sh.cc[i];
