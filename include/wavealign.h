@@ -142,8 +142,8 @@ wa_status wa_mask_stats(const uint8_t* mask, const wa_shape* shape, int32_t* row
 
 /* Workspace bytes needed by wa_build_permutation and wa_mask_stats: the bit-packed
  * rows and columns of the mask, per-head statistics, and the state of the subspace
- * iteration (X, the centred products and their per-slice partial sums, one slice
- * per 256 columns), about B*H*M_B*(2*ceil(N_B/64)*8 + 40 + 16*ceil(N_B/256)) bytes.
+ * iteration (X and the two centred products), about B*H*M_B*(2*ceil(N_B/64)*8 + 48)
+ * bytes.
  * Calls that share a workspace must not overlap. */
 wa_status wa_perm_workspace_size(const wa_shape* shape, size_t* bytes);
 
