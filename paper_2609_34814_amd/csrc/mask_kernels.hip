@@ -177,11 +177,19 @@ __global__ __launch_bounds__(256) void transpose_bits_kernel(const uint64_t* __r
   const int cw = rem / mw;   // column word
   const int v = rem % mw;    // row word
   const int r = v * 64 + lane;
-  const uint64_t mine = r < m ? rowbits[(h * nw + cw) * m + r] : 0ull;
-  uint64_t out = 0;
-  for (int c = 0; c < 64; ++c) {
-    const uint64_t b = ballot64((mine >> c) & 1ull);
-    if (lane == c) out = b;
+  uint64_t out = r < m ? rowbits[(h * nw + cw) * m + r] : 0ull;
+  // 64 x 64 bit transpose (lane = row -> lane = column) by the recursive block swap: at distance s,
+  // a lane in the lower half of each 2s group trades its columns with bit s set for the partner's
+  // columns with bit s clear (six lane exchanges in place of 64 ballots)
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) {
+    const uint64_t lo = s == 32 ? 0x00000000FFFFFFFFull : s == 16 ? 0x0000FFFF0000FFFFull
+                      : s == 8 ? 0x00FF00FF00FF00FFull : s == 4 ? 0x0F0F0F0F0F0F0F0Full
+                      : s == 2 ? 0x3333333333333333ull : 0x5555555555555555ull;  // columns with bit s clear
+    const uint32_t tlo = (uint32_t)__shfl_xor((int)(uint32_t)out, s);
+    const uint32_t thi = (uint32_t)__shfl_xor((int)(uint32_t)(out >> 32), s);
+    const uint64_t t = ((uint64_t)thi << 32) | tlo;
+    out = (lane & s) ? ((out & ~lo) | ((t >> s) & lo)) : ((out & lo) | ((t & lo) << s));
   }
   const int j = cw * 64 + lane;
   if (j < n) colbits[(h * mw + v) * n + j] = out;
