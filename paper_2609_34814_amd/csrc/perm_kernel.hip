@@ -776,9 +776,11 @@ __global__ __launch_bounds__(NT) void perm_finish_kernel(WaPermLaunch a) {
 // ---------------------------------------------------------------------------------------------
 // The whole permutation of a head in one workgroup, with both centred products on the matrix cores.
 //
-// An integer v with |v| < 2^31 - 2^23 is the sum of its four balanced base-256 digits,
+// An integer v with |v| <= 2^31 - 2^25 is the sum of its four balanced base-256 digits,
 // v = sum_b d_b 256^b with d_b in [-128, 127] (d_0 is the low byte read as a signed byte, then
-// v <- (v - d_0) / 256, exactly, and so on). So M^T X = sum_b 256^b (M^T D_b), where D_b holds digit
+// v <- (v - d_0) / 256, exactly, and so on; the last digit stays in range because the lower ones add
+// at most 128 (1 + 256 + 65536) < 2^23 to it). X (2^30 per unit, a column of an orthonormal block) and
+// Ys (30 significant bits) stay within 2^30 + 1. So M^T X = sum_b 256^b (M^T D_b), where D_b holds digit
 // b of every entry of X: each term is a product of a 0/1 matrix and an int8 matrix, whose int32
 // sums are exact (at most 1024 * 128 in magnitude), and the terms are combined exactly in int64.
 // One v_mfma_i32_16x16x64_i8 takes 64 rows of 16 columns of M: A = the eight digit rows (two
