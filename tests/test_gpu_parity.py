@@ -210,6 +210,18 @@ def test_permutation_bit_exact_form_boundaries_random(blocks):
     _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=S.SKIP_NEVER)
 
 
+@pytest.mark.parametrize("blocks", [1024, 1025])
+@pytest.mark.parametrize("kind", ["ones", "diag", "empty_rows"])
+def test_permutation_bit_exact_form_boundaries_special_masks(blocks, kind):
+    """Both forms on masks whose centred products vanish (all ones: degenerate, identity order), whose
+    singular values are all equal (diagonal) and with empty rows (a quarter of them)."""
+    rule = {"ones": dict(kind="ones"), "diag": dict(kind="diag"),
+            "empty_rows": dict(kind="empty_rows", p=0.05, empty=0.25)}[kind]
+    wl = custom(f"edge-{kind}{blocks}", heads=1, head_dim=64, block=64, grid=(blocks // 16, 16, 64),
+                seq_len=blocks * 64, rule=rule, seed=60 + blocks)
+    _perm_case(wl, make_mask(wl), wave=64, n_xcd=8, mode=S.SKIP_NEVER)
+
+
 @pytest.mark.parametrize("n_xcd,wave,seed", [(1, 132, 5), (2, 7, 99), (8, 1, 3)])
 def test_permutation_bit_exact_params(n_xcd, wave, seed):
     wl = CONFIGS["wan1.3b-480p-81f"]
