@@ -904,12 +904,14 @@ __device__ __forceinline__ void mfma_product(const int8_t (*dg)[STRIDE], const u
   const v4i zero = {0, 0, 0, 0};
   const int tend = min(t1, (lines + 15) >> 4);
   const int chunks = (words + CH - 1) / CH;
+  // A line past the head reads the head's last line instead: its products land in output columns the
+  // callers never read. Likewise A rows 8-15 repeat the digit rows: their products land in lanes 32-63.
   auto load = [&](int tile, int c, uint32_t (&bt)[CH]) {
-    const int line = 16 * tile + r;
+    const int line = min(16 * tile + r, lines - 1);
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
       const int s = c * CH + u;
-      bt[u] = s < words && line < lines ? bits16[((int64_t)s * lines + line) * 4 + q] : 0u;
+      bt[u] = s < words ? bits16[(s * lines + line) * 4 + q] : 0u;
     }
   };
   WA_PHASE_FENCE();
@@ -923,7 +925,7 @@ __device__ __forceinline__ void mfma_product(const int8_t (*dg)[STRIDE], const u
         for (int u = 0; u < CH; ++u) {
           const int s = c * CH + u;
           if (s < words) {
-            const v4i av = r < 8 ? *(const v4i*)&dg[r][64 * s + 16 * q] : zero;
+            const v4i av = *(const v4i*)&dg[r & 7][64 * s + 16 * q];
             acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bits_to_bytes(bt[u]), acc, 0, 0, 0);
           }
         }
@@ -950,7 +952,7 @@ __device__ __forceinline__ void mfma_product(const int8_t (*dg)[STRIDE], const u
       for (int u = 0; u < CH; ++u) {
         const int s = c * CH + u;
         if (s < words) {
-          const v4i av = r < 8 ? *(const v4i*)&dg[r][64 * s + 16 * q] : zero;
+          const v4i av = *(const v4i*)&dg[r & 7][64 * s + 16 * q];
           acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bits_to_bytes(cur[u]), acc, 0, 0, 0);
         }
       }
